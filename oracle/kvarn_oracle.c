@@ -1,0 +1,547 @@
+/*
+ * KVarN CPU oracle -- TEST INFRASTRUCTURE ONLY.
+ *
+ * A plain, slow, obviously-correct fp64 implementation of what the KVarN hot path
+ * computes (KVarN: Variance-Normalized KV-Cache Quantization, arXiv 2606.03458):
+ *   - per-token Hadamard rotation along head_dim            (Sec. 2.2, Sec. 3.3, App. A)
+ *   - VarN, alternating log-domain dual-scale balancing     (Sec. 3.3, App. H, Algorithm 1)
+ *   - KIVI-style asymmetric round-to-nearest per group      (Sec. 2.1, Eq. 1)
+ *   - dual-scale storage with the Sinkhorn scale absorbed   (App. D "Effective memory overhead")
+ *   - decode attention over sink + quantized body + residual (App. D "Quantization", App. I)
+ *
+ * Only the test-suite, the smoke check and the benchmark's CPU-baseline leg may load this
+ * library.  It shares no code, header, table or helper with the GPU library: the packed
+ * tile format is implemented here a second time, from its written description.
+ *
+ * Every floating-point step runs in double precision.  Values that the format stores in
+ * fp32 (the three auxiliary vectors) are rounded once, to nearest-even, when stored.
+ *
+ * Parity pins for each function live in tests/test_oracle_*.py.  The constants c_min and
+ * c_max of Algorithm 1 are not given numerically by the paper (parity unpinned; 1e-8 and
+ * 1e8 by default, see the params struct).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define D 128   /* head_dim: channels per token                       (Sec. 2.1) */
+#define G 128   /* tokens per quantization group / block              (Sec. 2.1, App. D) */
+
+enum { KVO_KEYS = 0, KVO_VALUES = 1 };
+
+typedef struct {
+    int32_t bits;        /* 2 or 4 */
+    int32_t varn_iters;  /* K of Algorithm 1 (8 in the runtime experiment, Sec. 4.2) */
+    double c_min, c_max; /* variance clamp of Algorithm 1 (values unstated in the paper) */
+    double log_lo, log_hi; /* clamp of the cumulative log-scales: -0.3 and 10.0 in Algorithm 1 */
+    double imb_floor;    /* floor on min variance inside Imb(): 1e-8 in Algorithm 1 */
+    int32_t ddof;        /* variance estimator: 1 (unbiased) by default */
+} kvo_params;
+
+/* ------------------------------------------------------------------------------------------
+ * bf16 <-> double.  bf16 is the upper half of an IEEE binary32.
+ * ------------------------------------------------------------------------------------------ */
+double kvo_bf16_to_double(uint16_t h) {
+    uint32_t u = (uint32_t)h << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return (double)f;
+}
+
+/* Round a double to bf16, nearest-even (via binary32, then binary32 -> bf16 nearest-even).
+ * Used only to store outputs; NaN is not produced by the oracle's inputs. */
+uint16_t kvo_double_to_bf16(double x) {
+    float f = (float)x;
+    uint32_t u;
+    memcpy(&u, &f, 4);
+    uint32_t lsb = (u >> 16) & 1u;
+    u += 0x7FFFu + lsb;
+    return (uint16_t)(u >> 16);
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Hadamard rotation (Sec. 2.2, Sec. 3.3, App. A).  Sylvester-ordered Walsh-Hadamard matrix
+ * H[i][j] = (-1)^popcount(i & j) / sqrt(128): symmetric, orthonormal and its own inverse.
+ * Computed with the textbook in-place butterflies, stride 1, 2, 4, ..., 64.
+ * ------------------------------------------------------------------------------------------ */
+void kvo_hadamard128(double *x) {
+    for (int h = 1; h < D; h <<= 1) {
+        for (int i = 0; i < D; i += 2 * h) {
+            for (int j = i; j < i + h; ++j) {
+                double a = x[j], b = x[j + h];
+                x[j] = a + b;
+                x[j + h] = a - b;
+            }
+        }
+    }
+    const double s = 1.0 / sqrt((double)D);
+    for (int i = 0; i < D; ++i) x[i] *= s;
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Algorithm 1 (App. H): VarN on one tile T with R rows and C columns, stored row-major.
+ * Rows are tokens and columns are channels of the cache tile.
+ *
+ * Notation of Algorithm 1:
+ *   Var_row(X): variance across the row index  -> one value per column (length C)
+ *   Var_col(X): variance across the column index -> one value per row (length R)
+ *   Imb(X) = max(v)/max(min(v), floor) summed over both variance vectors
+ *   L_c (1 x C), L_r (R x 1): log-scales; Cur = (T ./ exp(L_c)) ./ exp(L_r)
+ *   each iteration: column update from Var_row(Cur), then row update from Var_col(Cur),
+ *   then keep the scales if Imb(Cur) <= I_best.
+ * ------------------------------------------------------------------------------------------ */
+
+/* Two-pass (mean-centred) variance of n values spaced `stride` apart. */
+static double variance(const double *v, int n, int stride, int ddof) {
+    double mean = 0.0;
+    for (int i = 0; i < n; ++i) mean += v[(size_t)i * stride];
+    mean /= (double)n;
+    double ss = 0.0;
+    for (int i = 0; i < n; ++i) {
+        double d = v[(size_t)i * stride] - mean;
+        ss += d * d;
+    }
+    return ss / (double)(n - ddof);
+}
+
+static double clampd(double x, double lo, double hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+/* Cur = (T ./ exp(L_c)) ./ exp(L_r): two divisions, as written. */
+static void current_tile(const double *T, int R, int C, const double *Lc, const double *Lr, double *Cur) {
+    for (int r = 0; r < R; ++r)
+        for (int c = 0; c < C; ++c)
+            Cur[(size_t)r * C + c] = (T[(size_t)r * C + c] / exp(Lc[c])) / exp(Lr[r]);
+}
+
+/* Imb(X) of Algorithm 1. */
+double kvo_imbalance(const double *X, int R, int C, int ddof, double floor_) {
+    double vmax_r = -INFINITY, vmin_r = INFINITY, vmax_c = -INFINITY, vmin_c = INFINITY;
+    for (int r = 0; r < R; ++r) { /* variance along each row, over its C columns */
+        double v = variance(X + (size_t)r * C, C, 1, ddof);
+        vmax_r = fmax(vmax_r, v);
+        vmin_r = fmin(vmin_r, v);
+    }
+    for (int c = 0; c < C; ++c) { /* variance along each column, over its R rows */
+        double v = variance(X + c, R, C, ddof);
+        vmax_c = fmax(vmax_c, v);
+        vmin_c = fmin(vmin_c, v);
+    }
+    return vmax_r / fmax(vmin_r, floor_) + vmax_c / fmax(vmin_c, floor_);
+}
+
+/*
+ * Run Algorithm 1 on one tile.
+ *   T[R*C] (row-major) in; Sc[C], Sr[R] out (the best linear scales S_c*, S_r*);
+ *   Bal[R*C] out (optional): (T ./ S_c*) ./ S_r*.
+ * Optional histories, each indexed by iteration k = 0..K (k = 0 is the initial state):
+ *   imb_hist[K+1], Lc_hist[(K+1)*C], Lr_hist[(K+1)*R].
+ * *best_iter (optional) receives the iteration whose scales were kept (0 = initial).
+ */
+void kvo_varn(const double *T, int R, int C, const kvo_params *p, double *Sc, double *Sr, double *Bal,
+              double *imb_hist, double *Lc_hist, double *Lr_hist, int *best_iter) {
+    double *Lc = calloc((size_t)C, sizeof(double));
+    double *Lr = calloc((size_t)R, sizeof(double));
+    double *Cur = malloc((size_t)R * C * sizeof(double));
+    double *v = malloc((size_t)(R > C ? R : C) * sizeof(double));
+
+    current_tile(T, R, C, Lc, Lr, Cur);
+    double I_best = kvo_imbalance(Cur, R, C, p->ddof, p->imb_floor);
+    for (int c = 0; c < C; ++c) Sc[c] = exp(Lc[c]);
+    for (int r = 0; r < R; ++r) Sr[r] = exp(Lr[r]);
+    int best = 0;
+    if (imb_hist) imb_hist[0] = I_best;
+    if (Lc_hist) memcpy(Lc_hist, Lc, (size_t)C * sizeof(double));
+    if (Lr_hist) memcpy(Lr_hist, Lr, (size_t)R * sizeof(double));
+
+    for (int k = 1; k <= p->varn_iters; ++k) {
+        /* column scales from the variance of every column (taken across rows) */
+        for (int c = 0; c < C; ++c) v[c] = clampd(variance(Cur + c, R, C, p->ddof), p->c_min, p->c_max);
+        for (int c = 0; c < C; ++c) Lc[c] = clampd(Lc[c] + 0.5 * log(v[c]), p->log_lo, p->log_hi);
+        current_tile(T, R, C, Lc, Lr, Cur);
+        /* row scales from the variance of every row (taken across columns) */
+        for (int r = 0; r < R; ++r) v[r] = clampd(variance(Cur + (size_t)r * C, C, 1, p->ddof), p->c_min, p->c_max);
+        for (int r = 0; r < R; ++r) Lr[r] = clampd(Lr[r] + 0.5 * log(v[r]), p->log_lo, p->log_hi);
+        current_tile(T, R, C, Lc, Lr, Cur);
+
+        double I_curr = kvo_imbalance(Cur, R, C, p->ddof, p->imb_floor);
+        if (I_curr <= I_best) { /* "<=": a later iteration wins a tie */
+            I_best = I_curr;
+            for (int c = 0; c < C; ++c) Sc[c] = exp(Lc[c]);
+            for (int r = 0; r < R; ++r) Sr[r] = exp(Lr[r]);
+            best = k;
+        }
+        if (imb_hist) imb_hist[k] = I_curr;
+        if (Lc_hist) memcpy(Lc_hist + (size_t)k * C, Lc, (size_t)C * sizeof(double));
+        if (Lr_hist) memcpy(Lr_hist + (size_t)k * R, Lr, (size_t)R * sizeof(double));
+    }
+    if (Bal)
+        for (int r = 0; r < R; ++r)
+            for (int c = 0; c < C; ++c) Bal[(size_t)r * C + c] = (T[(size_t)r * C + c] / Sc[c]) / Sr[r];
+    if (best_iter) *best_iter = best;
+    free(Lc);
+    free(Lr);
+    free(Cur);
+    free(v);
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Asymmetric round-to-nearest over one group of n values (Sec. 2.1, Eq. 1):
+ *   mn = min, mx = max, s = (mx - mn) / (2^bits - 1)   (s := 1 when mx == mn)
+ *   u = (x - mn) / s, code = clamp(round-half-even(u), 0, 2^bits - 1)
+ * Eq. 1 writes the dequantized value as (code + z) * s with z = mn / s; the stored form here is
+ * the equivalent code * s + mn.  u_out (optional) receives the unrounded quotients.
+ * ------------------------------------------------------------------------------------------ */
+void kvo_rtn_group(const double *x, int n, int stride, int bits, uint8_t *codes, int code_stride,
+                   double *mn_out, double *s_out, double *u_out, int u_stride) {
+    double mn = INFINITY, mx = -INFINITY;
+    for (int i = 0; i < n; ++i) {
+        mn = fmin(mn, x[(size_t)i * stride]);
+        mx = fmax(mx, x[(size_t)i * stride]);
+    }
+    const double qmax = (double)((1 << bits) - 1);
+    double s = (mx - mn) / qmax;
+    if (s == 0.0) s = 1.0;
+    for (int i = 0; i < n; ++i) {
+        double u = (x[(size_t)i * stride] - mn) / s;
+        double q = nearbyint(u); /* default rounding mode: to nearest, ties to even */
+        if (q < 0.0) q = 0.0;
+        if (q > qmax) q = qmax;
+        codes[(size_t)i * code_stride] = (uint8_t)q;
+        if (u_out) u_out[(size_t)i * u_stride] = u;
+    }
+    *mn_out = mn;
+    *s_out = s;
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Quantize one 128-token x 128-channel tile X (token-major) of K or V (Fig. 2, Sec. 3.3):
+ *   1. T[t,:] = H X[t,:]                     Hadamard along head_dim, per token
+ *   2. (B, S_c*, S_r*) = VarN(T)             Algorithm 1, rows = tokens, columns = channels
+ *   3. RTN on B along the group axis         keys: per channel over the 128 tokens,
+ *                                            values: per token over the 128 channels (Sec. 2.1)
+ *   4. absorb the Sinkhorn scale of the group axis into the RTN scale and offset (App. D):
+ *        keys:   a[c] = s_c * S_c*[c],  b[c] = mn_c * S_c*[c],  s2[t] = S_r*[t]
+ *        values: a[t] = s_t * S_r*[t],  b[t] = mn_t * S_r*[t],  s2[c] = S_c*[c]
+ *      so that the dequantized rotated tile is  (code * a + b) * s2.
+ * Outputs: codes[128*128] token-major; a, b, s2 rounded to fp32.
+ * Optional debug outputs (NULL to skip): T_out[128*128], Bal_out[128*128], u_out[128*128]
+ * (token-major unrounded quotients), Sc_out[128], Sr_out[128], imb_hist[K+1], best_iter.
+ * ------------------------------------------------------------------------------------------ */
+void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *codes, float *a, float *b,
+                       float *s2, double *T_out, double *Bal_out, double *u_out, double *Sc_out, double *Sr_out,
+                       double *imb_hist, int *best_iter) {
+    double *T = malloc((size_t)G * D * sizeof(double));
+    double *Bal = malloc((size_t)G * D * sizeof(double));
+    double Sc[D], Sr[G];
+    memcpy(T, X, (size_t)G * D * sizeof(double));
+    for (int t = 0; t < G; ++t) kvo_hadamard128(T + (size_t)t * D);
+    kvo_varn(T, G, D, p, Sc, Sr, Bal, imb_hist, NULL, NULL, best_iter);
+
+    if (kind == KVO_KEYS) {
+        for (int c = 0; c < D; ++c) {
+            double mn, s;
+            kvo_rtn_group(Bal + c, G, D, p->bits, codes + c, D, &mn, &s, u_out ? u_out + c : NULL, D);
+            a[c] = (float)(s * Sc[c]);
+            b[c] = (float)(mn * Sc[c]);
+        }
+        for (int t = 0; t < G; ++t) s2[t] = (float)Sr[t];
+    } else {
+        for (int t = 0; t < G; ++t) {
+            double mn, s;
+            kvo_rtn_group(Bal + (size_t)t * D, D, 1, p->bits, codes + (size_t)t * D, 1, &mn, &s,
+                          u_out ? u_out + (size_t)t * D : NULL, 1);
+            a[t] = (float)(s * Sr[t]);
+            b[t] = (float)(mn * Sr[t]);
+        }
+        for (int c = 0; c < D; ++c) s2[c] = (float)Sc[c];
+    }
+    if (T_out) memcpy(T_out, T, (size_t)G * D * sizeof(double));
+    if (Bal_out) memcpy(Bal_out, Bal, (size_t)G * D * sizeof(double));
+    if (Sc_out) memcpy(Sc_out, Sc, sizeof Sc);
+    if (Sr_out) memcpy(Sr_out, Sr, sizeof Sr);
+    free(T);
+    free(Bal);
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Packed tile format (this library's own storage format; the paper fixes only what is
+ * stored per group, App. D).  A tile is
+ *     codes region: bits * 2048 bytes (128 x 128 codes of `bits` bits)
+ *     a[128], b[128], s2[128]: little-endian binary32, in index order (token or channel)
+ * Codes are grouped in "units" of 16 codes; unit u occupies bits/2 consecutive 32-bit
+ * little-endian words starting at word u * bits/2.  Inside a unit, code number e = 4*s + q
+ * (s, q in 0..3) sits in word  s / (8/bits)  at bit  8*q + bits*(s % (8/bits)).
+ * The unit index and e of code (t, c) are, with sigma = t / 64:
+ *   keys:   unit = (sigma*64 + 16*((c % 64) / 16) + t % 16) * 8 + 2*((t % 64) / 16) + c / 64,
+ *           e = c % 16
+ *   values: unit = (sigma*64 + 16*((t % 16) / 4) + c % 16) * 8 + c / 16,
+ *           e = 4*((t % 64) / 16) + t % 4
+ * ------------------------------------------------------------------------------------------ */
+size_t kvo_tile_bytes(int bits) { return (size_t)bits * 2048 + 3 * 128 * sizeof(float); }
+
+static void code_location(int kind, int bits, int t, int c, size_t *word, int *shift) {
+    int sigma = t / 64;
+    size_t unit;
+    int e;
+    if (kind == KVO_KEYS) {
+        unit = ((size_t)sigma * 64 + 16 * ((c % 64) / 16) + t % 16) * 8 + 2 * ((t % 64) / 16) + c / 64;
+        e = c % 16;
+    } else {
+        unit = ((size_t)sigma * 64 + 16 * ((t % 16) / 4) + c % 16) * 8 + c / 16;
+        e = 4 * ((t % 64) / 16) + t % 4;
+    }
+    int s = e / 4, q = e % 4, per = 8 / bits;
+    *word = unit * (size_t)(bits / 2) + (size_t)(s / per);
+    *shift = 8 * q + bits * (s % per);
+}
+
+static void put_f32(uint8_t *dst, float v) { memcpy(dst, &v, 4); } /* host is little-endian */
+static float get_f32(const uint8_t *src) { float v; memcpy(&v, src, 4); return v; }
+
+void kvo_pack_tile(const uint8_t *codes, const float *a, const float *b, const float *s2, int kind, int bits,
+                   uint8_t *dst) {
+    size_t ncode_bytes = (size_t)bits * 2048;
+    uint32_t *words = calloc(ncode_bytes / 4, sizeof(uint32_t));
+    for (int t = 0; t < G; ++t)
+        for (int c = 0; c < D; ++c) {
+            size_t w;
+            int sh;
+            code_location(kind, bits, t, c, &w, &sh);
+            words[w] |= (uint32_t)codes[(size_t)t * D + c] << sh;
+        }
+    for (size_t w = 0; w < ncode_bytes / 4; ++w) { /* little-endian words */
+        dst[4 * w + 0] = (uint8_t)(words[w]);
+        dst[4 * w + 1] = (uint8_t)(words[w] >> 8);
+        dst[4 * w + 2] = (uint8_t)(words[w] >> 16);
+        dst[4 * w + 3] = (uint8_t)(words[w] >> 24);
+    }
+    for (int i = 0; i < 128; ++i) {
+        put_f32(dst + ncode_bytes + 4 * i, a[i]);
+        put_f32(dst + ncode_bytes + 512 + 4 * i, b[i]);
+        put_f32(dst + ncode_bytes + 1024 + 4 * i, s2[i]);
+    }
+    free(words);
+}
+
+void kvo_unpack_tile(const uint8_t *src, int kind, int bits, uint8_t *codes, float *a, float *b, float *s2) {
+    size_t ncode_bytes = (size_t)bits * 2048;
+    const uint32_t mask = (1u << bits) - 1u;
+    for (int t = 0; t < G; ++t)
+        for (int c = 0; c < D; ++c) {
+            size_t w;
+            int sh;
+            code_location(kind, bits, t, c, &w, &sh);
+            uint32_t word = (uint32_t)src[4 * w] | (uint32_t)src[4 * w + 1] << 8 | (uint32_t)src[4 * w + 2] << 16 |
+                            (uint32_t)src[4 * w + 3] << 24;
+            codes[(size_t)t * D + c] = (uint8_t)((word >> sh) & mask);
+        }
+    for (int i = 0; i < 128; ++i) {
+        if (a) a[i] = get_f32(src + ncode_bytes + 4 * i);
+        if (b) b[i] = get_f32(src + ncode_bytes + 512 + 4 * i);
+        if (s2) s2[i] = get_f32(src + ncode_bytes + 1024 + 4 * i);
+    }
+}
+
+/*
+ * Dequantize a packed tile back to the unrotated domain, in double:
+ *   rotated: keys   Xr[t][c] = (code * a[c] + b[c]) * s2[t]
+ *            values Xr[t][c] = (code * a[t] + b[t]) * s2[c]
+ *   then X[t,:] = H Xr[t,:] (H is its own inverse).  Out: X[128*128] token-major.
+ */
+void kvo_dequantize_tile(const uint8_t *src, int kind, int bits, double *X) {
+    uint8_t *codes = malloc((size_t)G * D);
+    float a[128], b[128], s2[128];
+    kvo_unpack_tile(src, kind, bits, codes, a, b, s2);
+    for (int t = 0; t < G; ++t) {
+        for (int c = 0; c < D; ++c) {
+            double q = (double)codes[(size_t)t * D + c];
+            X[(size_t)t * D + c] = kind == KVO_KEYS ? (q * (double)a[c] + (double)b[c]) * (double)s2[t]
+                                                    : (q * (double)a[t] + (double)b[t]) * (double)s2[c];
+        }
+        kvo_hadamard128(X + (size_t)t * D);
+    }
+    free(codes);
+}
+
+/* Quantize + pack one tile whose input is fp32 (dtype 0) or bf16 (dtype 1) at `x` with the
+ * given token stride (in elements; channels contiguous). */
+void kvo_quantize_pack(const void *x, int dtype, int64_t token_stride, int kind, const kvo_params *p, uint8_t *dst) {
+    double *X = malloc((size_t)G * D * sizeof(double));
+    uint8_t *codes = malloc((size_t)G * D);
+    float a[128], b[128], s2[128];
+    for (int t = 0; t < G; ++t)
+        for (int c = 0; c < D; ++c)
+            X[(size_t)t * D + c] = dtype == 0 ? (double)((const float *)x)[t * token_stride + c]
+                                              : kvo_bf16_to_double(((const uint16_t *)x)[t * token_stride + c]);
+    kvo_quantize_tile(X, kind, p, codes, a, b, s2, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
+    kvo_pack_tile(codes, a, b, s2, kind, p->bits, dst);
+    free(X);
+    free(codes);
+}
+
+/*
+ * Batched quantize: tile (i, j) reads x + i*x_outer + j*x_inner (elements) and writes the packed
+ * tile to out + (i*out_outer + j*out_inner) * tile_bytes.  Tiles are independent; OpenMP
+ * distributes them over the host's threads.
+ */
+void kvo_quantize_tiles(const void *x, int dtype, int64_t n_outer, int64_t n_inner, int64_t x_outer, int64_t x_inner,
+                        int64_t token_stride, int kind, const kvo_params *p, uint8_t *out, int64_t out_outer,
+                        int64_t out_inner) {
+    const size_t tb = kvo_tile_bytes(p->bits);
+    const size_t esz = dtype == 0 ? 4 : 2;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int64_t i = 0; i < n_outer; ++i)
+        for (int64_t j = 0; j < n_inner; ++j)
+            kvo_quantize_pack((const uint8_t *)x + (size_t)(i * x_outer + j * x_inner) * esz, dtype, token_stride,
+                              kind, p, out + (size_t)(i * out_outer + j * out_inner) * tb);
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Cache regions (App. D "Quantization"): the first n_sink tokens of a sequence stay in bf16
+ * (sink), then come full groups of 128 quantized tokens (body), then the most recent
+ * (len - n_sink) % 128 tokens in bf16 (residual).  Residual and sink hold the tokens as given
+ * (unrotated); body tiles are stored in the rotated domain and un-rotated on dequantization.
+ *
+ * Host layout shared with the GPU library (described in its header, re-derived here):
+ *   k_body, v_body:   [batch][n_kv][max_blocks] packed tiles
+ *   k_resid, v_resid: [batch][n_kv][128][128] bf16
+ *   k_sink, v_sink:   [batch][n_kv][n_sink][128] bf16 (unused when n_sink == 0)
+ *   seq_len:          [batch] int32
+ * ------------------------------------------------------------------------------------------ */
+typedef struct {
+    int32_t batch, n_kv, max_blocks, n_sink, bits;
+    uint8_t *k_body, *v_body;
+    uint16_t *k_resid, *v_resid, *k_sink, *v_sink;
+    int32_t *seq_len;
+} kvo_cache;
+
+static void region_sizes(const kvo_cache *cc, int32_t len, int32_t *n_sink_used, int32_t *n_blocks, int32_t *n_resid) {
+    if (len <= cc->n_sink) {
+        *n_sink_used = len;
+        *n_blocks = 0;
+        *n_resid = 0;
+    } else {
+        *n_sink_used = cc->n_sink;
+        *n_blocks = (len - cc->n_sink) / G;
+        *n_resid = (len - cc->n_sink) % G;
+    }
+}
+
+/*
+ * Gather the full-precision view of one (sequence, kv-head) stream: keys and values of all
+ * `len` tokens in the unrotated domain, in token order (sink, body, residual).
+ * K, V: [len][128] doubles, caller-allocated.
+ */
+void kvo_gather_stream(const kvo_cache *cc, int32_t bi, int32_t kh, double *K, double *V) {
+    const int32_t len = cc->seq_len[bi];
+    int32_t ns, nb, nr;
+    region_sizes(cc, len, &ns, &nb, &nr);
+    const size_t stream = (size_t)bi * cc->n_kv + kh;
+    const size_t tb = kvo_tile_bytes(cc->bits);
+    int32_t t = 0;
+    for (int32_t i = 0; i < ns; ++i, ++t)
+        for (int c = 0; c < D; ++c) {
+            K[(size_t)t * D + c] = kvo_bf16_to_double(cc->k_sink[(stream * cc->n_sink + i) * D + c]);
+            V[(size_t)t * D + c] = kvo_bf16_to_double(cc->v_sink[(stream * cc->n_sink + i) * D + c]);
+        }
+    for (int32_t blk = 0; blk < nb; ++blk, t += G) {
+        kvo_dequantize_tile(cc->k_body + (stream * cc->max_blocks + blk) * tb, KVO_KEYS, cc->bits, K + (size_t)t * D);
+        kvo_dequantize_tile(cc->v_body + (stream * cc->max_blocks + blk) * tb, KVO_VALUES, cc->bits, V + (size_t)t * D);
+    }
+    for (int32_t i = 0; i < nr; ++i, ++t)
+        for (int c = 0; c < D; ++c) {
+            K[(size_t)t * D + c] = kvo_bf16_to_double(cc->k_resid[(stream * G + i) * D + c]);
+            V[(size_t)t * D + c] = kvo_bf16_to_double(cc->v_resid[(stream * G + i) * D + c]);
+        }
+}
+
+/* Plain attention of one query over n tokens: o = softmax(scale * K q) V, max-subtracted. */
+void kvo_attend(const double *q, const double *K, const double *V, int32_t n, double scale, double *o) {
+    double *s = malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+    double m = -INFINITY;
+    for (int32_t t = 0; t < n; ++t) {
+        double acc = 0.0;
+        for (int c = 0; c < D; ++c) acc += q[c] * K[(size_t)t * D + c];
+        s[t] = scale * acc;
+        m = fmax(m, s[t]);
+    }
+    double l = 0.0;
+    for (int c = 0; c < D; ++c) o[c] = 0.0;
+    for (int32_t t = 0; t < n; ++t) {
+        double pt = exp(s[t] - m);
+        l += pt;
+        for (int c = 0; c < D; ++c) o[c] += pt * V[(size_t)t * D + c];
+    }
+    for (int c = 0; c < D; ++c) o[c] = n > 0 ? o[c] / l : 0.0;
+    free(s);
+}
+
+/*
+ * Decode attention over the whole cache: for sequence b and query head h (kv head
+ * h / (n_q / n_kv)), out[b][h][:] = softmax(scale * q . K^T) V over every cached token.
+ * q: [batch][n_q][128] as fp32 (dtype 0) or bf16 (dtype 1); out: [batch][n_q][128] doubles.
+ */
+void kvo_decode(const kvo_cache *cc, int32_t n_q, const void *q, int dtype, double scale, double *out) {
+    const int32_t grp = n_q / cc->n_kv;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int32_t bi = 0; bi < cc->batch; ++bi)
+        for (int32_t kh = 0; kh < cc->n_kv; ++kh) {
+            const int32_t len = cc->seq_len[bi];
+            double *K = malloc((size_t)(len > 0 ? len : 1) * D * sizeof(double));
+            double *V = malloc((size_t)(len > 0 ? len : 1) * D * sizeof(double));
+            kvo_gather_stream(cc, bi, kh, K, V);
+            for (int32_t j = 0; j < grp; ++j) {
+                int32_t h = kh * grp + j;
+                double qd[D];
+                size_t qoff = ((size_t)bi * n_q + h) * D;
+                for (int c = 0; c < D; ++c)
+                    qd[c] = dtype == 0 ? (double)((const float *)q)[qoff + c]
+                                       : kvo_bf16_to_double(((const uint16_t *)q)[qoff + c]);
+                kvo_attend(qd, K, V, len, scale, out + qoff);
+            }
+            free(K);
+            free(V);
+        }
+}
+
+/*
+ * Append one token per (sequence, kv head) (the streaming write of Fig. 4's pseudo-decode and
+ * App. D's three regions): k_new, v_new are [batch][n_kv][128] bf16.  The token goes to the
+ * sink while the sequence is shorter than n_sink, otherwise to the residual; when the
+ * residual reaches 128 tokens it is quantized (keys and values) into the next body tile and
+ * emptied.  Returns 0, or -3 if a sequence has no free body slot for the flush.
+ */
+int kvo_append(kvo_cache *cc, const uint16_t *k_new, const uint16_t *v_new, const kvo_params *p) {
+    const size_t tb = kvo_tile_bytes(cc->bits);
+    for (int32_t bi = 0; bi < cc->batch; ++bi) {
+        int32_t len = cc->seq_len[bi];
+        int32_t ns, nb, nr;
+        region_sizes(cc, len, &ns, &nb, &nr);
+        if (len >= cc->n_sink && nr == G - 1 && nb >= cc->max_blocks) return -3;
+    }
+    for (int32_t bi = 0; bi < cc->batch; ++bi) {
+        int32_t len = cc->seq_len[bi];
+        int32_t ns, nb, nr;
+        region_sizes(cc, len, &ns, &nb, &nr);
+        for (int32_t kh = 0; kh < cc->n_kv; ++kh) {
+            const size_t stream = (size_t)bi * cc->n_kv + kh;
+            const uint16_t *kn = k_new + stream * D, *vn = v_new + stream * D;
+            if (len < cc->n_sink) {
+                memcpy(cc->k_sink + (stream * cc->n_sink + len) * D, kn, D * 2);
+                memcpy(cc->v_sink + (stream * cc->n_sink + len) * D, vn, D * 2);
+                continue;
+            }
+            memcpy(cc->k_resid + (stream * G + nr) * D, kn, D * 2);
+            memcpy(cc->v_resid + (stream * G + nr) * D, vn, D * 2);
+            if (nr + 1 == G) {
+                kvo_quantize_pack(cc->k_resid + stream * G * D, 1, D, KVO_KEYS, p,
+                                  cc->k_body + (stream * cc->max_blocks + nb) * tb);
+                kvo_quantize_pack(cc->v_resid + stream * G * D, 1, D, KVO_VALUES, p,
+                                  cc->v_body + (stream * cc->max_blocks + nb) * tb);
+            }
+        }
+        cc->seq_len[bi] = len + 1;
+    }
+    return 0;
+}
