@@ -1,0 +1,176 @@
+/*
+ * kvarn.h -- C ABI of libkvarn, the KVarN hot path for AMD Instinct MI355X (gfx950).
+ *
+ * KVarN (arXiv 2606.03458) stores a transformer's K/V cache in three regions (App. D,
+ * "Quantization"): the first n_sink tokens of a sequence in 16-bit, a body of quantized
+ * 128-token groups, and a residual of the most recent tokens that do not yet fill a group.
+ * A group (one 128-token x 128-channel tile of K or of V for one sequence and kv head) is
+ * quantized by (Fig. 2, Sec. 3.3):
+ *   1. a Hadamard rotation of every token along head_dim (Sec. 2.2, App. A),
+ *   2. VarN, alternating log-domain variance normalisation of columns and rows with best-
+ *      imbalance tracking (App. H, Algorithm 1; rows = tokens, columns = channels),
+ *   3. asymmetric round-to-nearest (Sec. 2.1, Eq. 1): keys per channel, values per token,
+ *   4. dual-scale storage with the Sinkhorn scale of the group axis absorbed into the RTN
+ *      scale and offset (App. D, "Effective memory overhead").
+ * Decode attention reads the packed body, dequantizes with the second scale fused (App. I)
+ * and attends over sink + body + residual.
+ *
+ * Conventions for every entry point:
+ *   - All pointers to tensors are DEVICE pointers, owned by the caller, and must stay valid
+ *     until the work queued on `stream` has run.  The library allocates no device memory.
+ *   - Every call only enqueues work on `stream` (asynchronous); none synchronizes.
+ *   - Arguments are validated on the host before anything is enqueued.  A failed check
+ *     returns a negative kvarn_status and enqueues nothing.  KVARN_EHIP reports a failed
+ *     kernel launch.  The library never aborts and throws nothing across this ABI.
+ *   - Calls on different caches may run concurrently; calls that touch the same cache must
+ *     be ordered by the caller (same stream or events).
+ *   - head_dim and the group size are fixed at 128.
+ *
+ * Packed tile (the library's storage format; the paper fixes only what is stored per group):
+ *   bytes [0, bits*2048)          128 x 128 codes of `bits` bits (layout below)
+ *   next 512 bytes                a[128]  fp32   keys: RTN scale of channel c times its
+ *                                                 Sinkhorn channel scale; values: of token t
+ *   next 512 bytes                b[128]  fp32   the matching offset (group minimum times
+ *                                                 the same Sinkhorn scale)
+ *   next 512 bytes                s2[128] fp32   second scale: keys per token, values per
+ *                                                 channel (the other Sinkhorn scale)
+ *   Dequantized rotated tile: keys (code[t][c]*a[c] + b[c]) * s2[t]; values
+ *   (code[t][c]*a[t] + b[t]) * s2[c]; un-rotate each token with the orthonormal Hadamard
+ *   matrix.  Tile size: 5632 bytes at 2 bits (2.75 bits/element), 9728 at 4 bits.
+ *   Code layout: codes form units of 16; unit u is bits/2 little-endian 32-bit words starting
+ *   at word u*bits/2.  Code e = 4*s + q (s, q in 0..3) of a unit sits in word s/(8/bits) of
+ *   the unit, at bit 8*q + bits*(s % (8/bits)).  For token t, channel c, sigma = t/64:
+ *     keys:   u = (sigma*64 + 16*((c%64)/16) + t%16)*8 + 2*((t%64)/16) + c/64,  e = c % 16
+ *     values: u = (sigma*64 + 16*((t%16)/4) + c%16)*8 + c/16,  e = 4*((t%64)/16) + t%4
+ *   (Each 64-token half of a tile is the register image of 64 GPU lanes x 8 units.)
+ */
+#ifndef KVARN_H
+#define KVARN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVARN_API __attribute__((visibility("default")))
+
+typedef enum {
+    KVARN_OK = 0,
+    KVARN_EINVAL = -1,       /* null pointer, bad size, stride or dtype                      */
+    KVARN_EUNSUPPORTED = -2, /* valid request this build does not implement (e.g. bits=3)    */
+    KVARN_ECAPACITY = -3,    /* the cache has no room for the requested tokens              */
+    KVARN_EHIP = -4,         /* a HIP launch or query failed                                */
+    KVARN_EWORKSPACE = -5    /* workspace missing or smaller than kvarn_decode_workspace_bytes */
+} kvarn_status;
+
+typedef enum { KVARN_F32 = 0, KVARN_BF16 = 1 } kvarn_dtype;
+typedef enum { KVARN_KEYS = 0, KVARN_VALUES = 1 } kvarn_kind;
+
+/* Quantizer constants (App. H, Algorithm 1).  kvarn_params_init fills the defaults. */
+typedef struct {
+    int32_t bits;       /* 2 or 4                                                      */
+    int32_t varn_iters; /* K of Algorithm 1: 8 (runtime experiment, Sec. 4.2); 0..64      */
+    int32_t n_sink;     /* tokens kept in bf16 at the start of a sequence: 0 or up to 1024 */
+    float var_min;      /* c_min: variances are clamped to [var_min, var_max]; 1e-8     */
+    float var_max;      /* c_max: 1e8 (the paper gives no values for c_min, c_max)      */
+    float log_lo;       /* clamp of the cumulative log-scales: -0.3 (Algorithm 1)       */
+    float log_hi;       /* 10.0 (Algorithm 1)                                           */
+} kvarn_params;
+
+/* The cache of `batch` sequences with n_kv kv heads each (a model's layers may be folded
+ * into batch).  Device buffers, all caller-allocated (sizes from kvarn_cache_sizes):
+ *   k_body, v_body   [batch][n_kv][max_blocks] packed tiles of kvarn_tile_bytes(bits)
+ *   k_resid, v_resid [batch][n_kv][128][128]    bf16, tokens as given (unrotated)
+ *   k_sink, v_sink   [batch][n_kv][n_sink][128] bf16, or NULL when n_sink == 0
+ *   seq_len          [batch] int32: tokens held by each sequence (all regions)
+ *   err_word         one uint32 or NULL: a kernel that finds no room sets bit 0 and drops
+ *                    the write instead of writing out of bounds (a backstop only: the host
+ *                    check of kvarn_append_token catches overflow from its length hint).
+ * A sequence of length L holds min(L, n_sink) sink tokens, (L - n_sink)/128 body tiles and
+ * (L - n_sink) % 128 residual tokens (0 body and residual tokens while L <= n_sink). */
+typedef struct {
+    int32_t batch, n_kv, max_blocks;
+    void *k_body, *v_body;
+    void *k_resid, *v_resid;
+    void *k_sink, *v_sink;
+    int32_t *seq_len;
+    uint32_t *err_word;
+} kvarn_cache;
+
+/* Fill `p` with the defaults for `bits` (2 or 4).  Returns KVARN_EINVAL for a null `p`,
+ * KVARN_EUNSUPPORTED for other bit widths. */
+KVARN_API int kvarn_params_init(kvarn_params *p, int32_t bits);
+
+/* Bytes of one packed tile: 5632 for bits = 2, 9728 for bits = 4, 0 otherwise. */
+KVARN_API size_t kvarn_tile_bytes(int32_t bits);
+
+/* Byte sizes of the seven cache buffers, in the order k_body, v_body, k_resid, v_resid,
+ * k_sink, v_sink, seq_len.  Returns KVARN_EINVAL for null pointers or non-positive sizes. */
+KVARN_API int kvarn_cache_sizes(const kvarn_params *p, int32_t batch, int32_t n_kv, int32_t max_blocks, size_t sizes[7]);
+
+/*
+ * Quantize n_outer x n_inner independent tiles (Fig. 2: Hadamard, VarN, RTN, pack).
+ *   kind    KVARN_KEYS (RTN per channel) or KVARN_VALUES (RTN per token)
+ *   x       tile (i, j) starts at element x + i*x_outer_stride + j*x_inner_stride; token t of
+ *           it at + t*x_token_stride; its 128 channels are contiguous.  dtype fp32 or bf16.
+ *           The input is unrotated: the library applies the Hadamard rotation.
+ *   out     tile (i, j) is written at byte out + (i*out_outer_stride + j*out_inner_stride) *
+ *           kvarn_tile_bytes(bits) (strides counted in tiles).
+ *   best_iter  optional [n_outer*n_inner] int32 (row-major over (i, j)): the VarN iteration
+ *           whose scales were kept (0 = the initial unit scales); NULL to skip.
+ * Strides must be non-negative, x_token_stride >= 128; x, and every x stride times the
+ * element size, must be multiples of 16 bytes (rows are read as 16-byte vectors); out must
+ * be 16-byte aligned.  n_outer or n_inner == 0 is a no-op.
+ * Prefill: quantize [batch*n_kv][T/128] tiles straight into k_body / v_body and set seq_len.
+ */
+KVARN_API int kvarn_quantize_block(const kvarn_params *p, int32_t kind, const void *x, int32_t x_dtype, int64_t n_outer,
+                         int64_t n_inner, int64_t x_outer_stride, int64_t x_inner_stride, int64_t x_token_stride,
+                         void *out, int64_t out_outer_stride, int64_t out_inner_stride, int32_t *best_iter,
+                         hipStream_t stream);
+
+/*
+ * Append one token to every (sequence, kv head) (the streaming write of Fig. 4's pseudo-decode):
+ *   k_new, v_new  [batch][n_kv][128] in `dtype` (fp32 or bf16; stored as bf16, unrotated).
+ * The token goes to the sink while a sequence is shorter than n_sink, otherwise to the
+ * residual; a residual that reaches 128 tokens is quantized (keys and values) into the next
+ * body tile and emptied, within this call.  seq_len is incremented on the device.
+ *   host_len_before  the common length of all sequences before this call (lock-step decode),
+ *           used to check capacity on the host and to launch the flush only when one is due;
+ *           pass -1 if lengths differ or are unknown: the flush kernel then runs every call
+ *           and each sequence decides on the device, and overflow is caught by err_word only.
+ * Returns KVARN_ECAPACITY (enqueuing nothing) if the hint shows that a flush would need body
+ * tile max_blocks.
+ */
+KVARN_API int kvarn_append_token(const kvarn_params *p, const kvarn_cache *cache, const void *k_new, const void *v_new,
+                       int32_t dtype, int32_t host_len_before, hipStream_t stream);
+
+/* Workspace bytes that kvarn_decode_attention needs for these sizes (split partials). */
+KVARN_API size_t kvarn_decode_workspace_bytes(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q,
+                                    int32_t max_len_hint);
+
+/*
+ * Decode attention of one query token per sequence over its whole cache:
+ *   out[b][h][:] = softmax(sm_scale * q[b][h] . K^T) V over the sink, body and residual of
+ *   sequence b, kv head h / (n_q / n_kv).  The body is dequantized in registers with both
+ *   scales fused (App. I); the query is rotated once so body logits are computed in the
+ *   rotated domain, and the body's output is rotated back once per query head (App. A).
+ *   q    [batch][n_q][128] fp32 or bf16 (post-RoPE, unrotated)
+ *   out  [batch][n_q][128] in out_dtype (fp32 or bf16)
+ *   max_len_hint  an upper bound of every seq_len (sizes the split-K plan)
+ *   workspace  device buffer of at least kvarn_decode_workspace_bytes(...) bytes
+ * n_q must be a positive multiple of n_kv with n_q / n_kv <= 16.  A sequence of length 0
+ * produces zeros.
+ */
+KVARN_API int kvarn_decode_attention(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q, const void *q,
+                           int32_t q_dtype, void *out, int32_t out_dtype, float sm_scale, int32_t max_len_hint,
+                           void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVARN_H */

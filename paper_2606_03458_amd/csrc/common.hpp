@@ -1,0 +1,60 @@
+// Shared device/host definitions of libkvarn (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kvarn.h"
+
+namespace kvarn {
+
+constexpr int kD = 128;  // head_dim (channels per token)
+constexpr int kG = 128;  // tokens per quantization group / body tile
+
+// 1/sqrt(128), rounded to fp32.
+constexpr float kInvSqrt128 = 0.08838834764831845f;
+constexpr float kLog2e = 1.4426950408889634f;
+
+__host__ __device__ inline size_t tile_bytes(int bits) { return (size_t)bits * 2048 + 3 * 128 * sizeof(float); }
+__host__ __device__ inline size_t code_bytes(int bits) { return (size_t)bits * 2048; }
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+// Quantizer constants, as passed to kernels.
+struct QParams {
+    int bits;
+    int iters;
+    float var_min, var_max, log_lo, log_hi;
+};
+
+// Kernel launchers (defined in the .hip files; called by the host API).
+hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, bool x_bf16, int64_t n_outer,
+                                 int64_t n_inner, int64_t x_outer, int64_t x_inner, int64_t x_token, void* out,
+                                 int64_t out_outer, int64_t out_inner, int32_t* best_iter, hipStream_t stream);
+
+hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream);
+
+hipError_t launch_append(const kvarn_cache& c, int n_sink, const void* k_new, const void* v_new, bool bf16,
+                         hipStream_t stream);
+
+struct DecodePlan {
+    int n_split;           // body splits per (sequence, kv head)
+    int blocks_per_split;  // body tiles per split
+    int max_blocks_used;   // upper bound of body tiles over the batch
+};
+
+DecodePlan plan_decode(int batch, int n_kv, int max_len, int n_sink, int max_blocks);
+size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan);
+
+hipError_t launch_decode(const kvarn_cache& c, int bits, int n_sink, int n_q, const void* q, bool q_bf16, void* out,
+                         bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws, hipStream_t stream);
+
+}  // namespace kvarn

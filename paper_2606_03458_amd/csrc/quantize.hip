@@ -1,0 +1,491 @@
+// KVarN tile quantizer for gfx950: Hadamard rotation (Sec. 2.2, App. A), VarN (App. H,
+// Algorithm 1), asymmetric RTN (Sec. 2.1, Eq. 1) and bit-packing with the dual-scale aux of
+// App. D.  One 256-thread workgroup quantizes one 128-token x 128-channel tile held entirely
+// in registers: thread (tr, tc) owns tokens 8*tr..8*tr+7 and channels 8*tc..8*tc+7, with
+// tc = lane % 16 (a DPP row of 16 lanes spans all 128 channels of a token) and
+// tr = 4*wave + lane / 16.  Row (per-token) reductions stay inside a 16-lane row; column
+// (per-channel) reductions cross the four 16-lane groups of a wave and then the four waves
+// through LDS, in a fixed order so that every thread sees bit-identical results.
+#include "common.hpp"
+
+namespace kvarn {
+namespace {
+
+constexpr int kThreads = 256;
+
+struct QuantSmem {
+    float red[2][4][kD];          // column partials [buffer][wave][channel]
+    float rstat[2][4][2];         // per-wave row max / min [buffer][wave][max, min]
+    alignas(16) uint8_t codes[kG * kD];  // keys: [token][channel]; values: [channel][token]
+};
+
+struct Lane {
+    int tid, lane, wave, tc, tr;
+    __device__ Lane() {
+        tid = threadIdx.x;
+        lane = tid & 63;
+        wave = tid >> 6;
+        tc = lane & 15;
+        tr = wave * 4 + (lane >> 4);
+    }
+};
+
+// ---- reductions ---------------------------------------------------------------------------
+struct OpSum {
+    __device__ static float f(float a, float b) { return a + b; }
+};
+struct OpMax {
+    __device__ static float f(float a, float b) { return fmaxf(a, b); }
+};
+struct OpMin {
+    __device__ static float f(float a, float b) { return fminf(a, b); }
+};
+
+// Across the 16 threads that share a channel block (all token blocks): lanes ^16, ^32, then
+// the four waves through LDS.  Every thread of a channel block ends with the same values.
+template <class Op>
+__device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& buf, const Lane& L) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        s[j] = Op::f(s[j], __shfl_xor(s[j], 16));
+        s[j] = Op::f(s[j], __shfl_xor(s[j], 32));
+    }
+    if (L.lane < 16) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) sm.red[buf][L.wave][8 * L.tc + j] = s[j];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int c = 8 * L.tc + j;
+        s[j] = Op::f(Op::f(Op::f(sm.red[buf][0][c], sm.red[buf][1][c]), sm.red[buf][2][c]), sm.red[buf][3][c]);
+    }
+    buf ^= 1;
+}
+
+// Across the 16 channel-block threads of a token row (lanes ^1, ^2, ^4, ^8 of a DPP row).
+template <class Op>
+__device__ __forceinline__ void reduce_rows(float (&s)[8]) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+        for (int m = 1; m < 16; m <<= 1) s[i] = Op::f(s[i], __shfl_xor(s[i], m));
+    }
+}
+
+// Variance over tokens of every column of T*w (two-pass, ddof = 1).
+__device__ __forceinline__ void column_var(const float (&x)[8][8], const float (&w)[8], float (&var)[8],
+                                           QuantSmem& sm, int& buf, const Lane& L) {
+    float s[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) acc += x[i][j] * w[i];
+        s[j] = acc;
+    }
+    reduce_cols<OpSum>(s, sm, buf, L);
+    float mean[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mean[j] = s[j] * (1.0f / kG);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float d = x[i][j] * w[i] - mean[j];
+            acc += d * d;
+        }
+        s[j] = acc;
+    }
+    reduce_cols<OpSum>(s, sm, buf, L);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) var[j] = s[j] * (1.0f / (kG - 1));
+}
+
+// Variance over channels of every row of T*u (two-pass, ddof = 1).
+__device__ __forceinline__ void row_var(const float (&x)[8][8], const float (&u)[8], float (&var)[8]) {
+    float s[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc += x[i][j] * u[j];
+        s[i] = acc;
+    }
+    reduce_rows<OpSum>(s);
+    float mean[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) mean[i] = s[i] * (1.0f / kD);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        float acc = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float d = x[i][j] * u[j] - mean[i];
+            acc += d * d;
+        }
+        s[i] = acc;
+    }
+    reduce_rows<OpSum>(s);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) var[i] = s[i] * (1.0f / (kD - 1));
+}
+
+// Imb of Algorithm 1 from the row variances (per token, replicated over tc) and the column
+// variances (per channel, replicated over tr).  Uniform over the workgroup.
+__device__ __forceinline__ float imbalance(const float (&vr)[8], const float (&vc)[8], QuantSmem& sm, int& buf,
+                                           const Lane& L) {
+    float rmax = vr[0], rmin = vr[0], cmax = vc[0], cmin = vc[0];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) {
+        rmax = fmaxf(rmax, vr[k]);
+        rmin = fminf(rmin, vr[k]);
+        cmax = fmaxf(cmax, vc[k]);
+        cmin = fminf(cmin, vc[k]);
+    }
+    // columns: all 128 channels live in one 16-lane row
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {
+        cmax = fmaxf(cmax, __shfl_xor(cmax, m));
+        cmin = fminf(cmin, __shfl_xor(cmin, m));
+    }
+    // rows: token blocks span the four lane groups and the four waves
+    rmax = fmaxf(rmax, __shfl_xor(rmax, 16));
+    rmin = fminf(rmin, __shfl_xor(rmin, 16));
+    rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
+    rmin = fminf(rmin, __shfl_xor(rmin, 32));
+    if (L.lane == 0) {
+        sm.rstat[buf][L.wave][0] = rmax;
+        sm.rstat[buf][L.wave][1] = rmin;
+    }
+    __syncthreads();
+    rmax = fmaxf(fmaxf(sm.rstat[buf][0][0], sm.rstat[buf][1][0]), fmaxf(sm.rstat[buf][2][0], sm.rstat[buf][3][0]));
+    rmin = fminf(fminf(sm.rstat[buf][0][1], sm.rstat[buf][1][1]), fminf(sm.rstat[buf][2][1], sm.rstat[buf][3][1]));
+    buf ^= 1;
+    return rmax / fmaxf(rmin, 1e-8f) + cmax / fmaxf(cmin, 1e-8f);
+}
+
+__device__ __forceinline__ float clampf(float v, float lo, float hi) { return fminf(fmaxf(v, lo), hi); }
+
+// Quantize one tile.  src: token t at src + t*tstride elements, channels contiguous (16-byte
+// aligned rows).  dst: the packed tile (16-byte aligned).
+__device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int kind, const QParams& P, uint8_t* dst,
+                              int32_t* best_out, QuantSmem& sm) {
+    const Lane L;
+    int buf = 0;
+    float x[8][8];
+
+    // ---- a1: load -------------------------------------------------------------------------
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        const int64_t t = 8 * L.tr + i;
+        if (bf16) {
+            const uint4 v = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(src) + t * tstride + 8 * L.tc);
+            const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                x[i][2 * k] = __uint_as_float(w[k] << 16);
+                x[i][2 * k + 1] = __uint_as_float(w[k] & 0xFFFF0000u);
+            }
+        } else {
+            const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(src) + t * tstride + 8 * L.tc);
+            const float4 a = p[0], b = p[1];
+            x[i][0] = a.x; x[i][1] = a.y; x[i][2] = a.z; x[i][3] = a.w;
+            x[i][4] = b.x; x[i][5] = b.y; x[i][6] = b.z; x[i][7] = b.w;
+        }
+    }
+
+    // ---- a2: Hadamard along channels, butterflies of stride 1, 2, ..., 64 ------------------
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+        for (int h = 1; h < 8; h <<= 1) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                if (!(j & h)) {
+                    const float a = x[i][j], b = x[i][j + h];
+                    x[i][j] = a + b;
+                    x[i][j + h] = a - b;
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int m = 1; m < 16; m <<= 1) {  // channel stride 8*m lives in lane tc ^ m
+        const bool upper = (L.tc & m) != 0;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float p = __shfl_xor(x[i][j], m);
+                x[i][j] = upper ? (p - x[i][j]) : (x[i][j] + p);
+            }
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[i][j] *= kInvSqrt128;
+    }
+
+    // ---- a3/a4: VarN (Algorithm 1), Cur = T * u[c] * w[t] with u = exp(-L_c), w = exp(-L_r) -
+    float Lc[8], Lr[8], u[8], w[8], bLc[8], bLr[8], cv[8], rv[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+        Lc[k] = Lr[k] = bLc[k] = bLr[k] = 0.f;
+        u[k] = w[k] = 1.f;
+    }
+    column_var(x, w, cv, sm, buf, L);  // variance over tokens of T's columns
+    row_var(x, u, rv);                 // variance over channels of T's rows
+    float I_best = imbalance(rv, cv, sm, buf, L);
+    int best = 0;
+    for (int k = 1; k <= P.iters; ++k) {
+        // column update from the current column variances u^2 * var_t(T w)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float v = clampf(u[j] * u[j] * cv[j], P.var_min, P.var_max);
+            Lc[j] = clampf(Lc[j] + 0.5f * __logf(v), P.log_lo, P.log_hi);
+            u[j] = __expf(-Lc[j]);
+        }
+        // row update from the row variances w^2 * var_c(T u)
+        row_var(x, u, rv);
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const float v = clampf(w[i] * w[i] * rv[i], P.var_min, P.var_max);
+            Lr[i] = clampf(Lr[i] + 0.5f * __logf(v), P.log_lo, P.log_hi);
+            w[i] = __expf(-Lr[i]);
+        }
+        // imbalance of the new Cur; its column statistics seed the next column update
+        column_var(x, w, cv, sm, buf, L);
+        float vr[8], vc[8];
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            vr[m] = w[m] * w[m] * rv[m];
+            vc[m] = u[m] * u[m] * cv[m];
+        }
+        const float I = imbalance(vr, vc, sm, buf, L);
+        if (I <= I_best) {  // later iteration wins ties
+            I_best = I;
+            best = k;
+#pragma unroll
+            for (int m = 0; m < 8; ++m) {
+                bLc[m] = Lc[m];
+                bLr[m] = Lr[m];
+            }
+        }
+    }
+
+    // ---- a5: balanced tile B = T / S_c* / S_r* ---------------------------------------------
+    float Sc[8], Sr[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        Sc[m] = __expf(bLc[m]);
+        Sr[m] = __expf(bLr[m]);
+        u[m] = __expf(-bLc[m]);
+        w[m] = __expf(-bLr[m]);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[i][j] = x[i][j] * u[j] * w[i];
+    }
+
+    // ---- a6: RTN along the group axis (keys: per channel, values: per token) ----------------
+    const float qmax = (float)((1 << P.bits) - 1);
+    float mn[8], mx[8];
+    if (kind == KVARN_KEYS) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            mn[j] = mx[j] = x[0][j];
+#pragma unroll
+            for (int i = 1; i < 8; ++i) {
+                mn[j] = fminf(mn[j], x[i][j]);
+                mx[j] = fmaxf(mx[j], x[i][j]);
+            }
+        }
+        reduce_cols<OpMin>(mn, sm, buf, L);
+        reduce_cols<OpMax>(mx, sm, buf, L);
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            mn[i] = mx[i] = x[i][0];
+#pragma unroll
+            for (int j = 1; j < 8; ++j) {
+                mn[i] = fminf(mn[i], x[i][j]);
+                mx[i] = fmaxf(mx[i], x[i][j]);
+            }
+        }
+        reduce_rows<OpMin>(mn);
+        reduce_rows<OpMax>(mx);
+    }
+    float s[8], inv_s[8];
+#pragma unroll
+    for (int m = 0; m < 8; ++m) {
+        s[m] = (mx[m] - mn[m]) / qmax;
+        if (s[m] == 0.f) s[m] = 1.f;
+        inv_s[m] = 1.0f / s[m];
+    }
+    // codes -> LDS (keys [t][c], values [c][t]), 8 bytes per thread per token / channel
+    if (kind == KVARN_KEYS) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - mn[j]) * inv_s[j]), 0.f, qmax);
+                if (j < 4) lo |= q << (8 * j); else hi |= q << (8 * (j - 4));
+            }
+            *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tr + i) * kD + 8 * L.tc]) = make_uint2(lo, hi);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - mn[i]) * inv_s[i]), 0.f, qmax);
+                if (i < 4) lo |= q << (8 * i); else hi |= q << (8 * (i - 4));
+            }
+            *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tc + j) * kG + 8 * L.tr]) = make_uint2(lo, hi);
+        }
+    }
+
+    // ---- a7: aux (absorbed scales) --------------------------------------------------------
+    float* aux = reinterpret_cast<float*>(dst + code_bytes(P.bits));
+    if (kind == KVARN_KEYS) {
+        if (L.tr == 0) {  // per channel: a = s * S_c*, b = mn * S_c*
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                aux[8 * L.tc + j] = s[j] * Sc[j];
+                aux[kD + 8 * L.tc + j] = mn[j] * Sc[j];
+            }
+        }
+        if (L.tc == 0) {  // s2 per token
+#pragma unroll
+            for (int i = 0; i < 8; ++i) aux[2 * kD + 8 * L.tr + i] = Sr[i];
+        }
+    } else {
+        if (L.tc == 0) {  // per token: a = s * S_r*, b = mn * S_r*
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                aux[8 * L.tr + i] = s[i] * Sr[i];
+                aux[kD + 8 * L.tr + i] = mn[i] * Sr[i];
+            }
+        }
+        if (L.tr == 0) {  // s2 per channel
+#pragma unroll
+            for (int j = 0; j < 8; ++j) aux[2 * kD + 8 * L.tc + j] = Sc[j];
+        }
+    }
+    if (best_out && L.tid == 0) *best_out = best;
+    __syncthreads();
+
+    // ---- a7: pack; thread tid assembles units 4*tid .. 4*tid+3 -----------------------------
+    // Unit u: sigma = u / 512, lane' = (u / 8) % 64, w = u % 8.  Its 16 codes e = 4s + q come
+    // from four 4-byte LDS reads d_s (byte q = code e); code e goes to bit 8q + bits*(s % per)
+    // of word s / per, per = 8 / bits, so a word is the OR of d_s shifted by bits*(s % per).
+    uint32_t words[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const int unit = 4 * L.tid + k;
+        const int sigma = unit >> 9, lanep = (unit >> 3) & 63, wsel = unit & 7;
+        const int m = lanep & 15, G4 = lanep >> 4;
+        uint32_t d[4];
+        if (kind == KVARN_KEYS) {
+            const int t = 64 * sigma + 16 * (wsel >> 1) + m;
+            const int c0 = 64 * (wsel & 1) + 16 * G4;
+            const uint4 v = *reinterpret_cast<const uint4*>(&sm.codes[t * kD + c0]);
+            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+        } else {
+            const int c = 16 * wsel + m;
+#pragma unroll
+            for (int ss = 0; ss < 4; ++ss)
+                d[ss] = *reinterpret_cast<const uint32_t*>(&sm.codes[c * kG + 64 * sigma + 16 * ss + 4 * G4]);
+        }
+        if (P.bits == 2) {
+            words[k] = d[0] | (d[1] << 2) | (d[2] << 4) | (d[3] << 6);
+        } else {
+            words[2 * k] = d[0] | (d[1] << 4);
+            words[2 * k + 1] = d[2] | (d[3] << 4);
+        }
+    }
+    if (P.bits == 2) {
+        reinterpret_cast<uint4*>(dst)[L.tid] = make_uint4(words[0], words[1], words[2], words[3]);
+    } else {
+        reinterpret_cast<uint4*>(dst)[2 * L.tid] = make_uint4(words[0], words[1], words[2], words[3]);
+        reinterpret_cast<uint4*>(dst)[2 * L.tid + 1] = make_uint4(words[4], words[5], words[6], words[7]);
+    }
+}
+
+struct TileArgs {
+    QParams P;
+    int kind;
+    int x_bf16;
+    const void* x;
+    int64_t tile0, n_inner, x_outer, x_inner, x_token;
+    uint8_t* out;
+    int64_t out_outer, out_inner;
+    int32_t* best_iter;
+};
+
+__global__ __launch_bounds__(kThreads) void k_quantize_tiles(TileArgs a) {
+    __shared__ QuantSmem sm;
+    const int64_t tile = a.tile0 + blockIdx.x;
+    const int64_t i = tile / a.n_inner, j = tile % a.n_inner;
+    const size_t esz = a.x_bf16 ? 2 : 4;
+    const char* src = static_cast<const char*>(a.x) + (size_t)(i * a.x_outer + j * a.x_inner) * esz;
+    uint8_t* dst = a.out + (size_t)(i * a.out_outer + j * a.out_inner) * tile_bytes(a.P.bits);
+    quantize_tile(src, a.x_bf16 != 0, a.x_token, a.kind, a.P, dst, a.best_iter ? a.best_iter + tile : nullptr, sm);
+}
+
+struct FlushArgs {
+    QParams P;
+    kvarn_cache c;
+    int n_sink;
+};
+
+// One workgroup per (sequence, kv head, K|V).  Runs after the append kernel has incremented
+// seq_len: a sequence whose residual just reached 128 tokens quantizes it into body tile
+// (len - n_sink)/128 - 1; every other workgroup exits at once.
+__global__ __launch_bounds__(kThreads) void k_flush(FlushArgs a) {
+    __shared__ QuantSmem sm;
+    const int kind = blockIdx.x & 1;
+    const int64_t stream = blockIdx.x >> 1;
+    const int b = (int)(stream / a.c.n_kv);
+    const int len = a.c.seq_len[b];
+    if (len <= a.n_sink || (len - a.n_sink) % kG != 0) return;
+    const int nb = (len - a.n_sink) / kG - 1;
+    if (nb >= a.c.max_blocks) return;  // the append kernel refused the token and flagged it
+    const uint16_t* src = static_cast<const uint16_t*>(kind ? a.c.v_resid : a.c.k_resid) + (size_t)stream * kG * kD;
+    uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) +
+                   ((size_t)stream * a.c.max_blocks + nb) * tile_bytes(a.P.bits);
+    quantize_tile(src, true, kD, kind, a.P, dst, nullptr, sm);
+}
+
+}  // namespace
+
+hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, bool x_bf16, int64_t n_outer,
+                                 int64_t n_inner, int64_t x_outer, int64_t x_inner, int64_t x_token, void* out,
+                                 int64_t out_outer, int64_t out_inner, int32_t* best_iter, hipStream_t stream) {
+    const int64_t total = n_outer * n_inner;
+    const int64_t kMaxGrid = 1 << 30;
+    for (int64_t t0 = 0; t0 < total; t0 += kMaxGrid) {
+        const int64_t n = total - t0 < kMaxGrid ? total - t0 : kMaxGrid;
+        TileArgs a{qp, kind, x_bf16 ? 1 : 0, x, t0, n_inner, x_outer, x_inner, x_token,
+                   static_cast<uint8_t*>(out), out_outer, out_inner, best_iter};
+        hipLaunchKernelGGL(k_quantize_tiles, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
+hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream) {
+    FlushArgs a{qp, c, n_sink};
+    const int64_t n = (int64_t)c.batch * c.n_kv * 2;
+    hipLaunchKernelGGL(k_flush, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace kvarn

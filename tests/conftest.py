@@ -17,3 +17,27 @@ def orc():
     import oracle
     oracle.lib()
     return oracle
+
+
+@pytest.fixture(autouse=True)
+def _announce_gpu_case(request):
+    """Name every GPU test on the real stderr (not captured) before it touches the device."""
+    if request.node.get_closest_marker("gpu") is not None:
+        sys.__stderr__.write(f"\n[gpu case] {request.node.nodeid}\n")
+        sys.__stderr__.flush()
+    yield
+
+
+def pytest_collection_modifyitems(config, items):
+    """GPU tests are skipped with a reason when no GPU is visible (never silently passed)."""
+    try:
+        import torch
+        has_gpu = torch.cuda.is_available()
+    except Exception:
+        has_gpu = False
+    if has_gpu:
+        return
+    skip = pytest.mark.skip(reason="no GPU visible")
+    for item in items:
+        if item.get_closest_marker("gpu") is not None:
+            item.add_marker(skip)

@@ -1,0 +1,244 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, on the same seeded
+inputs (exact bytes copied to the host).  Tolerances are defined in gpu_util."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import (check_output, compare_tiles, host_cache, q_to_host, tiles_to_host)
+
+pytestmark = pytest.mark.gpu
+
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+@pytest.fixture(scope="module")
+def K():
+    from paper_2606_03458_amd import kvarn
+    kvarn.lib()
+    torch.cuda.set_device(0)
+    return kvarn
+
+
+def _quantize(K, x: torch.Tensor, kind: int, bits: int, **pover):
+    """x [n, 128, 128] on the GPU -> (tiles uint8 [n, tile_bytes], best [n])."""
+    n = x.shape[0]
+    p = K.kvarn_params_init(bits, **pover)
+    out = torch.zeros((n, K.kvarn_tile_bytes(bits)), dtype=torch.uint8, device="cuda")
+    best = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    dt = K.KVARN_F32 if x.dtype == torch.float32 else K.KVARN_BF16
+    K.kvarn_quantize_block(p, kind, x, dt, n, 1, 128 * 128, 0, 128, out, 1, 0, best)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), best.cpu().numpy()
+
+
+def _sample_tiles(dist, n, dtype, seed):
+    from paper_2606_03458_amd import datagen
+    Kx, Vx = datagen.kv_tokens(seed, 0, 1, 2, n * 64, dist, dtype=dtype, device="cuda")
+    return Kx.reshape(n, 128, 128).contiguous(), Vx.reshape(n, 128, 128).contiguous()
+
+
+# ---- quantizer --------------------------------------------------------------------------
+
+def test_quantize_tiny_fp32(K):
+    """Tiny workload: 256 tokens of fp32 K and V (2 tiles each), 2-bit, seed 0."""
+    from paper_2606_03458_amd import datagen
+    Kx, Vx = datagen.kv_tokens(0, 0, 1, 1, 256, "llama", dtype=torch.float32, device="cuda")
+    for kind, x in ((0, Kx), (1, Vx)):
+        xt = x.reshape(2, 128, 128).contiguous()
+        tiles, best = _quantize(K, xt, kind, 2)
+        st = compare_tiles(tiles, tiles_to_host(xt), kind, 2, best)
+        assert st["codes"] == 2 * 16384
+
+
+@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("dist", ["llama", "stress"])
+def test_quantize_bf16_tiles(K, bits, dist):
+    """32 bf16 tiles of each of K and V drawn like the llama / heavy-tailed workloads."""
+    Kx, Vx = _sample_tiles(dist, 32, torch.bfloat16, seed=11 + bits)
+    for kind, x in ((0, Kx), (1, Vx)):
+        tiles, best = _quantize(K, x, kind, bits)
+        compare_tiles(tiles, tiles_to_host(x), kind, bits, best)
+
+
+def test_quantize_degenerate_tiles(K):
+    """Zero, constant, single-outlier and huge-range tiles, and iteration counts 0 and 1."""
+    x = torch.zeros((5, 128, 128), dtype=torch.float32, device="cuda")
+    x[1] = 0.75
+    x[2, 17, 33] = 40.0
+    x[3] = torch.randn((128, 128), device="cuda") * 1e4
+    x[4] = torch.randn((128, 128), device="cuda") * 1e-3
+    for kind in (0, 1):
+        for iters in (8, 0, 1):
+            tiles, best = _quantize(K, x, kind, 2, varn_iters=iters)
+            compare_tiles(tiles, tiles_to_host(x), kind, 2, best, params=oracle.Params(bits=2, varn_iters=iters))
+
+
+def test_quantize_strided_views(K):
+    """Tiles read through strides: a [T][H][128] token-major layout (token stride H*128),
+    several outer/inner tiles, written to a strided output."""
+    H, T, S = 3, 256, 2
+    x = torch.randn((S, T, H, 128), device="cuda", dtype=torch.bfloat16) * 2
+    p = K.kvarn_params_init(2)
+    tb = K.kvarn_tile_bytes(2)
+    out = torch.zeros((S * H, 5, tb), dtype=torch.uint8, device="cuda")
+    for s in range(S):
+        # outer = head, inner = block; out row s*H + h, tiles at blocks 1 and 3 (stride 2)
+        K.kvarn_quantize_block(p, 1, x[s], K.KVARN_BF16, H, T // 128, 128, 128 * H * 128, H * 128,
+                               out[s * H:, 1:], 5, 2, None)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    for s in range(S):
+        for h in range(H):
+            for blk in range(2):
+                X = x[s, blk * 128:(blk + 1) * 128, h].float().cpu().numpy().astype(np.float64)
+                compare_tiles(o[s * H + h, 1 + 2 * blk][None], X[None], 1, 2)
+            for untouched in (0, 2, 4):
+                assert not o[s * H + h, untouched].any()
+
+
+def test_quantize_deterministic(K):
+    Kx, _ = _sample_tiles("llama", 16, torch.bfloat16, seed=5)
+    t1, _ = _quantize(K, Kx, 0, 2)
+    t2, _ = _quantize(K, Kx, 0, 2)
+    np.testing.assert_array_equal(t1, t2)
+
+
+# ---- decode attention ---------------------------------------------------------------------
+
+def _decode(K, built, q, out_dtype=torch.float32, max_len=None):
+    p, cache = built.params, built.cache
+    max_len = built.length + 1 if max_len is None else max_len
+    ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, built.n_q, max_len)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty(q.shape, dtype=out_dtype, device="cuda")
+    qd = K.KVARN_F32 if q.dtype == torch.float32 else K.KVARN_BF16
+    od = K.KVARN_F32 if out_dtype == torch.float32 else K.KVARN_BF16
+    K.kvarn_decode_attention(p, cache, built.n_q, q, qd, out, od, SCALE, max_len, ws, ws_bytes)
+    torch.cuda.synchronize()
+    return out
+
+
+def _ref(built, q):
+    return oracle.decode(host_cache(built.cache), q_to_host(q), SCALE)
+
+
+def test_decode_tiny(K):
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("tiny")
+    q = workloads.decode_queries(built, seed=0)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_decode_llama_layer(K, out_dtype):
+    """Llama-3-8B-shaped layer: 32 q / 8 kv heads, 8192-token prefill, then one appended
+    token (residual = 1), bf16 q."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama")
+    kt, vt = workloads.step_tokens(built, seed=1, step=0)
+    K.kvarn_append_token(built.params, built.cache, kt, vt, K.KVARN_BF16, built.length)
+    built.length += 1
+    q = workloads.decode_queries(built, seed=1)
+    out = _decode(K, built, q, out_dtype)
+    assert int(built.cache.seq_len[0]) == 8193
+    check_output(out.float().cpu().numpy(), _ref(built, q), bf16_out=out_dtype == torch.bfloat16)
+
+
+@pytest.mark.parametrize("bits,n_sink,name", [(2, 128, "llama"), (4, 0, "llama"), (2, 0, "stress"),
+                                              (4, 128, "stress")])
+def test_decode_variants(K, bits, n_sink, name):
+    """Sink region, 4-bit codes, GQA 5, ragged lengths (including 0 and sink-only) and a
+    residual, on a small batch that the split-K plan divides into many splits."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build(name, bits=bits, n_sink=n_sink, context=n_sink + 3 * 128 + 77, batch=5)
+    lens = [built.length, n_sink + 2 * 128, n_sink + 131, n_sink // 2 if n_sink else 0, 0]
+    built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    q = workloads.decode_queries(built, seed=3)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
+def test_decode_length_above_hint(K):
+    """A max_len_hint below the true length still attends every token (last split extends)."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", context=2048, batch=1)
+    q = workloads.decode_queries(built, seed=4)
+    out = _decode(K, built, q, max_len=300)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
+def test_decode_deterministic(K):
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", context=1024 + 5, batch=2)
+    q = workloads.decode_queries(built, seed=5)
+    o1 = _decode(K, built, q)
+    o2 = _decode(K, built, q)
+    assert torch.equal(o1, o2)
+
+
+# ---- streaming append ---------------------------------------------------------------------
+
+@pytest.mark.parametrize("bits,n_sink,hint", [(2, 0, True), (4, 128, True), (2, 128, False)])
+def test_append_stream(K, bits, n_sink, hint):
+    """Append tokens one by one from an empty cache (flushes included), on the GPU and in
+    the oracle, from the same bf16 tokens."""
+    B, H, steps = 2, 2, n_sink + 2 * 128 + 9
+    p = K.kvarn_params_init(bits)
+    p.n_sink = n_sink
+    cache = K.Cache(p, B, H, max_blocks=3)
+    hc = oracle.HostCache(B, H, 3, bits=bits, n_sink=n_sink)
+    po = oracle.Params(bits=bits)
+    g = torch.Generator(device="cuda").manual_seed(7)
+    scales = torch.exp(torch.randn((1, H, 128), generator=g, device="cuda"))
+    ks, vs = [], []
+    for t in range(steps):
+        kt = (torch.randn((B, H, 128), generator=g, device="cuda") * scales).to(torch.bfloat16)
+        vt = torch.randn((B, H, 128), generator=g, device="cuda").to(torch.bfloat16)
+        K.kvarn_append_token(p, cache, kt, vt, K.KVARN_BF16, t if hint else -1)
+        ks.append(q_to_host(kt))
+        vs.append(q_to_host(vt))
+        assert oracle.append(hc, ks[-1], vs[-1], po) == 0
+    torch.cuda.synchronize()
+    gc = host_cache(cache)
+    np.testing.assert_array_equal(gc.seq_len, hc.seq_len)
+    np.testing.assert_array_equal(gc.k_resid, hc.k_resid)
+    np.testing.assert_array_equal(gc.v_resid, hc.v_resid)
+    if n_sink:
+        np.testing.assert_array_equal(gc.k_sink, hc.k_sink)
+        np.testing.assert_array_equal(gc.v_sink, hc.v_sink)
+    # body tiles: both sides quantized the same 128 bf16 tokens of each stream
+    toks = {0: np.stack(ks), 1: np.stack(vs)}  # [steps, B, H, 128]
+    for kind, body in ((0, gc.k_body), (1, gc.v_body)):
+        for blk in range(2):
+            t0 = n_sink + blk * 128
+            for b in range(B):
+                for h in range(H):
+                    X = oracle.bf16_bits_to_f64(toks[kind][t0:t0 + 128, b, h])
+                    compare_tiles(body[b, h, blk][None], X[None], kind, bits)
+    assert not gc.k_body[:, :, 2].any() and not gc.v_body[:, :, 2].any()
+    assert int(cache.err_word[0]) == 0
+    # the oracle's own flushes agree with the GPU's codes up to ties as well
+    for kind, gb, ob in ((0, gc.k_body, hc.k_body), (1, gc.v_body, hc.v_body)):
+        g_codes = oracle.unpack_tile(gb[0, 0, 0], kind, bits)[0]
+        o_codes = oracle.unpack_tile(ob[0, 0, 0], kind, bits)[0]
+        assert (g_codes != o_codes).mean() <= 1e-3
+
+
+def test_append_overflow_flag(K):
+    """With no length hint, a flush that has no body tile left is refused on the device: the
+    token is dropped, err_word is set, and nothing is written out of bounds."""
+    p = K.kvarn_params_init(2)
+    cache = K.Cache(p, 1, 1, max_blocks=1)
+    tok = torch.ones((1, 1, 128), dtype=torch.bfloat16, device="cuda")
+    for t in range(128 + 127):
+        K.kvarn_append_token(p, cache, tok, tok, K.KVARN_BF16, -1)
+    torch.cuda.synchronize()
+    assert int(cache.err_word[0]) == 0 and int(cache.seq_len[0]) == 255
+    K.kvarn_append_token(p, cache, tok, tok, K.KVARN_BF16, -1)
+    torch.cuda.synchronize()
+    assert int(cache.err_word[0]) == 1 and int(cache.seq_len[0]) == 255
+    with pytest.raises(K.KVarNError) as e:
+        K.kvarn_append_token(p, cache, tok, tok, K.KVARN_BF16, 255)
+    assert e.value.status == -3
