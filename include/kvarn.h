@@ -148,7 +148,8 @@ KVARN_API int kvarn_quantize_block(const kvarn_params *p, int32_t kind, const vo
 KVARN_API int kvarn_append_token(const kvarn_params *p, const kvarn_cache *cache, const void *k_new, const void *v_new,
                        int32_t dtype, int32_t host_len_before, hipStream_t stream);
 
-/* Workspace bytes that kvarn_decode_attention needs for these sizes (split partials). */
+/* Workspace bytes that kvarn_decode_attention needs for these sizes (split partials); 0 when
+ * the plan keeps every (sequence, kv head) in one split, or when an argument is invalid. */
 KVARN_API size_t kvarn_decode_workspace_bytes(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q,
                                     int32_t max_len_hint);
 
@@ -161,9 +162,10 @@ KVARN_API size_t kvarn_decode_workspace_bytes(const kvarn_params *p, const kvarn
  *   q    [batch][n_q][128] fp32 or bf16 (post-RoPE, unrotated)
  *   out  [batch][n_q][128] in out_dtype (fp32 or bf16)
  *   max_len_hint  an upper bound of every seq_len (sizes the split-K plan)
- *   workspace  device buffer of at least kvarn_decode_workspace_bytes(...) bytes
- * n_q must be a positive multiple of n_kv with n_q / n_kv <= 16.  A sequence of length 0
- * produces zeros.
+ *   workspace  device buffer of at least kvarn_decode_workspace_bytes(...) bytes, 16-byte
+ *           aligned; may be NULL when that size is 0
+ * n_q must be a positive multiple of n_kv with n_q / n_kv <= 16; q 4-byte and out 8-byte
+ * aligned.  A sequence of length 0 produces zeros.
  */
 KVARN_API int kvarn_decode_attention(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q, const void *q,
                            int32_t q_dtype, void *out, int32_t out_dtype, float sm_scale, int32_t max_len_hint,

@@ -146,10 +146,10 @@ int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int3
     if (n_q <= 0 || n_q % cache->n_kv != 0 || n_q / cache->n_kv > 16) return KVARN_EINVAL;
     if (check_dtype(q_dtype) || check_dtype(out_dtype)) return KVARN_EINVAL;
     if (!q || !out || !std::isfinite(sm_scale) || max_len_hint < 0) return KVARN_EINVAL;
-    if (!aligned(q, 4) || !aligned(out, 4)) return KVARN_EINVAL;
+    if (!aligned(q, 4) || !aligned(out, 8)) return KVARN_EINVAL;
     const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, max_len_hint, p->n_sink, cache->max_blocks);
     const size_t need = decode_workspace_bytes(cache->batch, n_q, plan);
-    if (!workspace || workspace_bytes < need || !aligned(workspace, 16)) return KVARN_EWORKSPACE;
+    if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return KVARN_EWORKSPACE;
     hipError_t e = launch_decode(*cache, p->bits, p->n_sink, n_q, q, q_dtype == KVARN_BF16, out,
                                  out_dtype == KVARN_BF16, sm_scale, plan, static_cast<float*>(workspace), stream);
     return e == hipSuccess ? KVARN_OK : KVARN_EHIP;

@@ -1,23 +1,42 @@
 // KVarN decode attention for gfx950 (App. D three-region cache, App. I fused second scale,
 // App. A rotation layout).
 //
-// Body (quantized) tokens are attended in the rotated domain: with q_rot = H q and the packed
-// tile's aux, a key's logit is
-//     s2K[t] * (sum_c q_rot[c] a_K[c] code[t][c] + sum_c q_rot[c] b_K[c])
-// and a value tile adds  s2V[c] * (sum_t p[t] a_V[t] code[t][c] + sum_t p[t] b_V[t])  to the
-// rotated output, so each body tile costs one pass over its codes with both scales fused.
-// Sink and residual tokens (bf16, unrotated) are attended with q itself.  Every
-// (sequence, kv head) is split into n_split ranges of body tiles plus one range for sink +
-// residual; each range writes a partial (running max m in log2 units, sum l, output o).  The
-// merge kernel combines the partials by log-sum-exp, rotates the body part back with H and
-// adds the plain part.
+// Body tiles are attended in the rotated domain.  With q_rot = H q and a tile's aux
+//   logit[t]  = s2K[t] * (sum_c q~[c] code[t][c] + beta),   q~ = q_rot * a_K, beta = q_rot . b_K
+//   o_rot[c] += s2V[c] * (sum_t p~[t] code[t][c] + gamma),  p~ = p * a_V,   gamma = p . b_V
+// so both dual-scale products are fused into one pass over the codes (App. I).
+//
+// The two sums over codes are matrix products on the int8 matrix cores
+// (v_mfma_i32_16x16x64_i8).  The codes are exact int8 operands taken straight from the packed
+// words (the tile format stores them in the MFMA register order).  The real-valued side is
+// written as a fixed-point integer split into signed base-256 digits, one MFMA per digit,
+// recombined exactly in int32: q~ uses three digits (22 bits at 2-bit codes, 20 at 4-bit),
+// p~ two (15 bits).  Integer accumulation is exact, so the only rounding is that of q~ and p~
+// to their fixed-point grids.  beta and gamma are formed from the same rounded integers (with
+// the per-element offset ratios b / a), so code term and offset term of every dequantized
+// value carry identical weights and the rounding cannot leave a common-mode offset behind.
+//
+// Layout per wave (64 lanes, lane = 16*G + n): QK computes S^T = codes x q~^T with rows =
+// 16 tokens and columns = query heads of the kv head's group, so lane (G, n) receives tokens
+// 16*tau + 4*G + i of head n.  Those are exactly the K-slice of lane (G, n) in the PV product
+// O^T = codes_V^T x p~^T, so probabilities never leave their lane between the two products.
+// Columns n >= g (the group size) carry unused values.
+//
+// Sink and residual tokens (bf16, unrotated) use the bf16 matrix cores for q . k (q as a bf16
+// pair hi + lo when it is fp32) and plain FMAs for p . v.  One wave owns a (split, sequence,
+// kv head); the last split also takes sink + residual.  A single split writes the final
+// output directly (inverse rotation in LDS); several splits write partials that the merge
+// kernel combines by log-sum-exp.
 #include "common.hpp"
 
 namespace kvarn {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kPart = 132;  // floats per partial: m, l, 2 pad, o[128]
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+
+constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
 
 struct DecodeArgs {
     const uint8_t* k_body;
@@ -29,347 +48,482 @@ struct DecodeArgs {
     const int32_t* seq_len;
     const void* q;
     int q_bf16;
-    int n_kv, n_q, g, max_blocks, n_sink, bits;
+    void* out;
+    int out_bf16;
+    int n_kv, n_q, g, max_blocks, n_sink;
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
     int n_split, bps;  // body splits per stream and body tiles per split
-    float* ws;         // [batch][n_q][n_split + 1][kPart]
+    float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
 };
 
-__device__ __forceinline__ float load_q(const DecodeArgs& a, size_t idx) {
-    return a.q_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.q)[idx]) : static_cast<const float*>(a.q)[idx];
+__device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
+    return __builtin_amdgcn_mfma_i32_16x16x64_i8(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ v4f mfma_bf16(v8bf a, v8bf b, v4f c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+// v_perm_b32: byte selector 0-3 picks from `lo`, 4-7 from `hi`, 0x0c gives zero.
+__device__ __forceinline__ uint32_t perm(uint32_t hi, uint32_t lo, uint32_t sel) {
+    return __builtin_amdgcn_perm(hi, lo, sel);
 }
 
-__device__ __forceinline__ float* partial(const DecodeArgs& a, int b, int h, int s) {
-    return a.ws + (((size_t)b * a.n_q + h) * (a.n_split + 1) + s) * kPart;
+// The 16 codes of one unit as an int8 MFMA operand: byte q of dword s is code 4*s + q.
+template <int BITS>
+__device__ __forceinline__ v4i unit_i8(const uint32_t* w) {
+    if constexpr (BITS == 2) {
+        const uint32_t x = w[0], M = 0x03030303u;
+        return v4i{(int)(x & M), (int)((x >> 2) & M), (int)((x >> 4) & M), (int)((x >> 6) & M)};
+    } else {
+        const uint32_t M = 0x0F0F0F0Fu;
+        return v4i{(int)(w[0] & M), (int)((w[0] >> 4) & M), (int)(w[1] & M), (int)((w[1] >> 4) & M)};
+    }
 }
 
-// Code e (0..15) of a unit whose words start at w: word e/4/(8/bits), bit 8*(e%4) + bits*((e/4)%(8/bits)).
-__device__ __forceinline__ float unit_code(const uint32_t* w, int bits, int e) {
-    const int s = e >> 2, q = e & 3;
-    if (bits == 2) return (float)((w[0] >> (8 * q + 2 * s)) & 3u);
-    return (float)((w[s >> 1] >> (8 * q + 4 * (s & 1))) & 15u);
-}
+__device__ __forceinline__ float xor_max(float v, int m) { return fmaxf(v, __shfl_xor(v, m)); }
+__device__ __forceinline__ float xor_sum(float v, int m) { return v + __shfl_xor(v, m); }
 
-// Per-head reduction of 16 lanes (lanes ^1..^8 of a DPP row).
-__device__ __forceinline__ float row16_sum(float v) {
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) v += __shfl_xor(v, m);
-    return v;
+// Four values y0..y3, each a fixed-point integer plus 0x808080 (0x8080 for two digits), to
+// one dword per digit k whose byte i is the signed digit k of value i ((byte k of y_i) ^ 0x80).
+__device__ __forceinline__ void digits4(uint32_t y0, uint32_t y1, uint32_t y2, uint32_t y3, uint32_t& d0,
+                                        uint32_t& d1, uint32_t& d2) {
+    const uint32_t t01 = perm(y1, y0, 0x05010400u), t23 = perm(y3, y2, 0x05010400u);
+    d0 = perm(t23, t01, 0x05040100u) ^ 0x80808080u;
+    d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
+    const uint32_t u01 = perm(y1, y0, 0x0c0c0602u), u23 = perm(y3, y2, 0x0c0c0602u);
+    d2 = perm(u23, u01, 0x05040100u) ^ 0x80808080u;
 }
-__device__ __forceinline__ float row16_max(float v) {
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) v = fmaxf(v, __shfl_xor(v, m));
-    return v;
+__device__ __forceinline__ void digits4_2(uint32_t y0, uint32_t y1, uint32_t y2, uint32_t y3, uint32_t& d0,
+                                          uint32_t& d1) {
+    const uint32_t t01 = perm(y1, y0, 0x05010400u), t23 = perm(y3, y2, 0x05010400u);
+    d0 = perm(t23, t01, 0x05040100u) ^ 0x80808080u;
+    d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
 }
 
 template <int GQ>
-struct BodySmem {
-    float qrot[GQ][kD];
-    float qt[GQ][kD];   // q_rot * a_K of the current tile
-    float pt[GQ][kG];   // logits, then p * a_V
-    float aux[6][128];  // a_K b_K s2_K a_V b_V s2_V
-    float hs[GQ][4];    // per head: running max, running sum, rescale, beta / gamma
+struct Smem {
+    float q[GQ][kD];        // rotated q; reused for the inverse rotation of the output
+    float aux[6][kD];       // a_K b_K s2_K a_V b_V s2_V of the current tile
+    uint4 qp[3][2][4][GQ];  // q~ digits in B-operand order [digit][kappa][G][head]
+    float hv[GQ][4];        // per head: beta, q~ step, alpha, l
+    float p[GQ][kG];        // probabilities of a bf16 chunk (sink / residual)
 };
 
-// Online-softmax update of one tile's logits held in sm.pt (log2 units): per head, new max,
-// rescale factor, p (optionally times a_V) back into sm.pt, and returns via sm.hs.
+// LDS butterflies (stride 1..64) over rows [0, g) of x; 64 threads.  Unnormalized.
 template <int GQ>
-__device__ __forceinline__ void softmax_tile(BodySmem<GQ>& sm, int g, int n_valid, const float* aV, const float* bV,
-                                             float* m_run, float* l_run) {
-    const int tid = threadIdx.x;
-    const int j = tid >> 4, part = tid & 15;
-    if (j < g) {
-        float mx = -INFINITY;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int t = part * 8 + k;
-            if (t < n_valid) mx = fmaxf(mx, sm.pt[j][t]);
+__device__ __forceinline__ void lds_hadamard(float (&x)[GQ][kD], int g) {
+    const int l = threadIdx.x;
+    for (int h = 1; h < kD; h <<= 1) {
+        for (int idx = l; idx < g * 64; idx += 64) {
+            const int j = idx >> 6, r = idx & 63;
+            const int i0 = (r / h) * 2 * h + (r % h);
+            const float x0 = x[j][i0], x1 = x[j][i0 + h];
+            x[j][i0] = x0 + x1;
+            x[j][i0 + h] = x0 - x1;
         }
-        mx = row16_max(mx);
-        const float m_new = fmaxf(m_run[j], mx);
-        const float alpha = m_run[j] == -INFINITY ? 0.f : exp2f(m_run[j] - m_new);
-        float lsum = 0.f, gsum = 0.f;
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-            const int t = part * 8 + k;
-            float p = 0.f;
-            if (t < n_valid) p = exp2f(sm.pt[j][t] - m_new);
-            lsum += p;
-            if (bV) gsum += p * bV[t];
-            sm.pt[j][t] = aV ? p * aV[t] : p;
-        }
-        lsum = row16_sum(lsum);
-        gsum = row16_sum(gsum);
-        if (part == 0) {
-            sm.hs[j][0] = m_new;
-            sm.hs[j][1] = l_run[j] * alpha + lsum;
-            sm.hs[j][2] = alpha;
-            sm.hs[j][3] = gsum;
-        }
-    }
-    __syncthreads();
-    for (int jj = 0; jj < g; ++jj) {
-        m_run[jj] = sm.hs[jj][0];
-        l_run[jj] = sm.hs[jj][1];
+        __syncthreads();
     }
 }
 
-template <int GQ>
-__device__ void write_partials(const DecodeArgs& a, int b, int kvh, int s, const float* m_run, const float* l_run,
-                               const float* o, bool have_o) {
-    const int tid = threadIdx.x, c = tid >> 1, hf = tid & 1;
-    for (int j = 0; j < a.g; ++j) {
-        float* P = partial(a, b, kvh * a.g + j, s);
-        if (tid == 0) {
-            P[0] = m_run[j];
-            P[1] = l_run[j];
-        }
-        if (hf == 0) P[4 + c] = have_o ? o[j] : 0.f;
-    }
-}
-
-// One workgroup per (body split, sequence, kv head).
-template <int GQ>
-__global__ __launch_bounds__(kThreads) void k_decode_body(DecodeArgs a) {
-    __shared__ BodySmem<GQ> sm;
-    const int tid = threadIdx.x;
+template <int BITS, int GQ>
+__global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
+    __shared__ Smem<GQ> sm;
+    constexpr int WPU = BITS / 2;                        // words per 16-code unit
+    constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // |q~ fixed point| < 2^22 (2^20)
+    // p~ fixed point in [0, 32639]: the largest value whose two balanced base-256 digits
+    // (x + 0x8080 split into bytes, each minus 128) stay in range
+    constexpr float PMAX = 32639.f;
+    const int l = threadIdx.x, G = l >> 4, n = l & 15;
+    const int g = a.g;
+    const bool head_lane = n < g;
+    const int hn = n < GQ ? n : GQ - 1;
     const int split = blockIdx.x % a.n_split;
     const int stream = blockIdx.x / a.n_split;
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
-    const int g = a.g;
-    const int len = max(a.seq_len[b], 0);
-    // never read past the cache, whatever seq_len holds
-    const int nb = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
-    const int blk0 = split * a.bps;
-    // the last split also takes any tiles beyond the planned range (length above the hint)
-    const int blk1 = split == a.n_split - 1 ? nb : min(blk0 + a.bps, nb);
-
-    float m_run[GQ], l_run[GQ], o[GQ];
-#pragma unroll
-    for (int j = 0; j < GQ; ++j) {
-        m_run[j] = -INFINITY;
-        l_run[j] = 0.f;
-        o[j] = 0.f;
-    }
-    if (blk0 >= blk1) {
-        write_partials<GQ>(a, b, kvh, split, m_run, l_run, o, false);
-        return;
-    }
-
-    // q of the kv head's query group, rotated: butterflies in LDS
-    for (int idx = tid; idx < g * kD; idx += kThreads)
-        sm.qrot[idx >> 7][idx & 127] = load_q(a, ((size_t)b * a.n_q + kvh * g) * kD + idx);
-    __syncthreads();
-    for (int h = 1; h < kD; h <<= 1) {
-        for (int idx = tid; idx < g * 64; idx += kThreads) {
-            const int j = idx >> 6, r = idx & 63;
-            const int i0 = (r / h) * 2 * h + (r % h);
-            const float x0 = sm.qrot[j][i0], x1 = sm.qrot[j][i0 + h];
-            sm.qrot[j][i0] = x0 + x1;
-            sm.qrot[j][i0 + h] = x0 - x1;
-        }
-        __syncthreads();
-    }
-    for (int idx = tid; idx < g * kD; idx += kThreads) sm.qrot[idx >> 7][idx & 127] *= kInvSqrt128;
-    __syncthreads();
-
-    const size_t tb = tile_bytes(a.bits), cb = code_bytes(a.bits);
-    const int words_per_unit = a.bits / 2;
-    for (int blk = blk0; blk < blk1; ++blk) {
-        const uint8_t* kt = a.k_body + ((size_t)stream * a.max_blocks + blk) * tb;
-        const uint8_t* vt = a.v_body + ((size_t)stream * a.max_blocks + blk) * tb;
-        if (tid < 192) {
-            const int which = tid >> 5, part = tid & 31;
-            const uint8_t* base = (which < 3 ? kt : vt) + cb + (which % 3) * 512 + part * 16;
-            *reinterpret_cast<float4*>(&sm.aux[which][part * 4]) = *reinterpret_cast<const float4*>(base);
-        }
-        __syncthreads();
-        // q~ = q_rot * a_K and beta = q_rot . b_K per head
-        for (int idx = tid; idx < g * kD; idx += kThreads) {
-            const int j = idx >> 7, c = idx & 127;
-            sm.qt[j][c] = sm.qrot[j][c] * sm.aux[0][c];
-        }
-        {
-            const int j = tid >> 4, part = tid & 15;
-            if (j < g) {
-                float s = 0.f;
-#pragma unroll
-                for (int k = 0; k < 8; ++k) s += sm.qrot[j][part * 8 + k] * sm.aux[1][part * 8 + k];
-                s = row16_sum(s);
-                if (part == 0) sm.hs[j][3] = s;
-            }
-        }
-        __syncthreads();
-
-        // logits: thread (t, half) sums channels 64*half .. 64*half+63 of token t
-        {
-            const int t = tid >> 1, hf = tid & 1;
-            const int sigma = t >> 6, m = t & 15, tau = (t & 63) >> 4;
-            float acc[GQ];
-#pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] = 0.f;
-            for (int G4 = 0; G4 < 4; ++G4) {
-                const int unit = (sigma * 64 + 16 * G4 + m) * 8 + 2 * tau + hf;
-                uint32_t w[2];
-                w[0] = reinterpret_cast<const uint32_t*>(kt)[unit * words_per_unit];
-                w[1] = words_per_unit > 1 ? reinterpret_cast<const uint32_t*>(kt)[unit * words_per_unit + 1] : 0u;
-                for (int e = 0; e < 16; ++e) {
-                    const float code = unit_code(w, a.bits, e);
-                    const int c = 64 * hf + 16 * G4 + e;
-#pragma unroll
-                    for (int j = 0; j < GQ; ++j)
-                        if (j < g) acc[j] += sm.qt[j][c] * code;
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] += __shfl_xor(acc[j], 1);
-            if (hf == 0) {
-                const float sc = a.scale_log2 * sm.aux[2][t];
-#pragma unroll
-                for (int j = 0; j < GQ; ++j)
-                    if (j < g) sm.pt[j][t] = sc * (acc[j] + sm.hs[j][3]);
-            }
-        }
-        __syncthreads();
-        softmax_tile<GQ>(sm, g, kG, sm.aux[3], sm.aux[4], m_run, l_run);
-
-        // values: thread (c, half) sums tokens 64*half .. 64*half+63 of channel c
-        {
-            const int c = tid >> 1, hf = tid & 1;
-            float acc[GQ];
-#pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] = 0.f;
-            for (int G4 = 0; G4 < 4; ++G4) {
-                const int unit = (hf * 64 + 16 * G4 + (c & 15)) * 8 + (c >> 4);
-                uint32_t w[2];
-                w[0] = reinterpret_cast<const uint32_t*>(vt)[unit * words_per_unit];
-                w[1] = words_per_unit > 1 ? reinterpret_cast<const uint32_t*>(vt)[unit * words_per_unit + 1] : 0u;
-                for (int e = 0; e < 16; ++e) {
-                    const float code = unit_code(w, a.bits, e);
-                    const int t = 64 * hf + 16 * (e >> 2) + 4 * G4 + (e & 3);
-#pragma unroll
-                    for (int j = 0; j < GQ; ++j)
-                        if (j < g) acc[j] += sm.pt[j][t] * code;
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] += __shfl_xor(acc[j], 1);
-            if (hf == 0) {
-                const float s2 = sm.aux[5][c];
-#pragma unroll
-                for (int j = 0; j < GQ; ++j)
-                    if (j < g) o[j] = o[j] * sm.hs[j][2] + s2 * (acc[j] + sm.hs[j][3]);
-            }
-        }
-        __syncthreads();
-    }
-    write_partials<GQ>(a, b, kvh, split, m_run, l_run, o, true);
-}
-
-// One workgroup per (sequence, kv head): sink + residual tokens, bf16, unrotated.
-template <int GQ>
-__global__ __launch_bounds__(kThreads) void k_decode_plain(DecodeArgs a) {
-    __shared__ BodySmem<GQ> sm;  // qrot holds the unrotated q here
-    const int tid = threadIdx.x;
-    const int stream = blockIdx.x;
-    const int b = stream / a.n_kv, kvh = stream % a.n_kv;
-    const int g = a.g;
     const int len = max(a.seq_len[b], 0);
     const int ns = min(len, a.n_sink);
+    const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
-    const int total = ns + nr;
+    const bool last = split == a.n_split - 1;
+    const int blk0 = split * a.bps;
+    const int blk1 = last ? nbody : min(blk0 + a.bps, nbody);  // the last split takes any excess
+    const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;    // first query head of the group
+    const size_t tb = tile_bytes(BITS), cb = code_bytes(BITS);
 
-    float m_run[GQ], l_run[GQ], o[GQ];
+    float m_run = -INFINITY, l_run = 0.f;  // per head n; l_run is this lane's partial sum
+    float orot[8][4];                      // head n, channel 16*mt + 4*G + i (rotated domain)
+    float oplain[GQ][2];                   // head h, channel 2*l + j (unrotated)
 #pragma unroll
-    for (int j = 0; j < GQ; ++j) {
-        m_run[j] = -INFINITY;
-        l_run[j] = 0.f;
-        o[j] = 0.f;
-    }
-    if (total == 0) {
-        write_partials<GQ>(a, b, kvh, a.n_split, m_run, l_run, o, false);
-        return;
-    }
-    for (int idx = tid; idx < g * kD; idx += kThreads)
-        sm.qrot[idx >> 7][idx & 127] = load_q(a, ((size_t)b * a.n_q + kvh * g) * kD + idx);
-    __syncthreads();
+    for (int mt = 0; mt < 8; ++mt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) orot[mt][i] = 0.f;
+#pragma unroll
+    for (int h = 0; h < GQ; ++h) oplain[h][0] = oplain[h][1] = 0.f;
 
-    auto key_ptr = [&](int tok) -> const uint16_t* {
-        return tok < ns ? a.k_sink + ((size_t)stream * a.n_sink + tok) * kD
-                        : a.k_resid + ((size_t)stream * kG + (tok - ns)) * kD;
-    };
-    auto val_ptr = [&](int tok) -> const uint16_t* {
-        return tok < ns ? a.v_sink + ((size_t)stream * a.n_sink + tok) * kD
-                        : a.v_resid + ((size_t)stream * kG + (tok - ns)) * kD;
+    auto load_q = [&](size_t idx) -> float {
+        return a.q_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.q)[idx]) : static_cast<const float*>(a.q)[idx];
     };
 
-    for (int t0 = 0; t0 < total; t0 += kG) {
-        const int n = min(kG, total - t0);
-        {
-            const int t = tid >> 1, hf = tid & 1;
-            float acc[GQ];
+    // Online-softmax step shared by body tiles and bf16 chunks: lg holds 32 logits of head n
+    // (log2 units, -inf for absent tokens); turns lg into p and returns the rescale factor.
+    auto softmax_update = [&](float (&lg)[32]) -> float {
+        float mx = lg[0];
 #pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] = 0.f;
-            if (t < n) {
-                const uint16_t* kp = key_ptr(t0 + t) + 64 * hf;
-                for (int c = 0; c < 64; ++c) {
-                    const float kv = bf16_to_f32(kp[c]);
+        for (int k = 1; k < 32; ++k) mx = fmaxf(mx, lg[k]);
+        mx = xor_max(xor_max(mx, 16), 32);
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
+        float s = 0.f;
 #pragma unroll
-                    for (int j = 0; j < GQ; ++j)
-                        if (j < g) acc[j] += sm.qrot[j][64 * hf + c] * kv;
+        for (int k = 0; k < 32; ++k) {
+            lg[k] = lg[k] == -INFINITY ? 0.f : exp2f(lg[k] - m_new);
+            s += lg[k];
+        }
+        l_run = l_run * alpha + s;
+        m_run = m_new;
+        return alpha;
+    };
+
+    if (blk0 < blk1) {
+        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] = load_q(qrow * kD + idx);
+        __syncthreads();
+        lds_hadamard<GQ>(sm.q, g);
+        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
+
+        // Lane l's part of a tile: its K and V code units (32*WPU bytes per 64-token half) and
+        // one 16-byte piece of the 3 KB of aux (pieces l, l + 64, l + 128 of K aux || V aux).
+        uint4 kc[2][2 * WPU], vc[2][2 * WPU], ax0, ax1, ax2;
+        const int ax1_off = l < 32 ? (64 + l) * 16 : (l - 32) * 16;  // piece l + 64: K aux or V aux
+        auto load_tile = [&](int blk) {
+            const uint8_t* kt = a.k_body + ((size_t)stream * a.max_blocks + blk) * tb;
+            const uint8_t* vt = a.v_body + ((size_t)stream * a.max_blocks + blk) * tb;
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int k = 0; k < 2 * WPU; ++k) {
+                    kc[s][k] = reinterpret_cast<const uint4*>(kt)[(s * 64 + l) * 2 * WPU + k];
+                    vc[s][k] = reinterpret_cast<const uint4*>(vt)[(s * 64 + l) * 2 * WPU + k];
+                }
+            ax0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
+            ax1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + ax1_off);
+            ax2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
+        };
+        load_tile(blk0);
+
+        for (int blk = blk0; blk < blk1; ++blk) {
+            __syncthreads();  // the previous tile is done with sm.aux / sm.qp
+            reinterpret_cast<uint4*>(&sm.aux[0][0])[l] = ax0;
+            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 64] = ax1;
+            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 128] = ax2;
+            uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int k = 0; k < 2 * WPU; ++k) {
+                    kw[s][4 * k] = kc[s][k].x; kw[s][4 * k + 1] = kc[s][k].y;
+                    kw[s][4 * k + 2] = kc[s][k].z; kw[s][4 * k + 3] = kc[s][k].w;
+                    vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
+                    vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
+                }
+            if (blk + 1 < blk1) load_tile(blk + 1);  // prefetch, consumed next iteration
+            __syncthreads();
+            // value offsets as ratios b_V / a_V (read after the next barrier)
+            sm.aux[4][2 * l] *= __frcp_rn(sm.aux[3][2 * l]);
+            sm.aux[4][2 * l + 1] *= __frcp_rn(sm.aux[3][2 * l + 1]);
+
+            // ---- q~ = q_rot * a_K as three base-256 digits, spread over all 64 lanes ----------
+            // group gi = (head, kappa, G', s) covers channels 64*kappa + 16*G' + 4*s .. +3
+            for (int gi0 = 0; gi0 < g * 32; gi0 += 64) {
+                const int gi = gi0 + l;
+                const bool valid = gi < g * 32;
+                const int h = min(gi >> 5, g - 1), rem = gi & 31;
+                const int kap = rem >> 4, Gp = (rem >> 2) & 3, s = rem & 3;
+                const int c0 = 64 * kap + 16 * Gp + 4 * s;
+                float qt[4], mx = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float qv = valid ? sm.q[h][c0 + k] : 0.f;
+                    qt[k] = qv * sm.aux[0][c0 + k];
+                    mx = fmaxf(mx, fabsf(qt[k]));
+                }
+#pragma unroll
+                for (int m = 1; m < 32; m <<= 1) mx = xor_max(mx, m);
+                const float sc = mx > 0.f ? (float)QMAX / mx : 0.f;
+                // beta in q~ grid units: sum over channels of the rounded q~ times b_K / a_K
+                float bs = 0.f;
+                uint32_t y[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const int xi = __float2int_rn(qt[k] * sc);
+                    bs = fmaf((float)xi, sm.aux[1][c0 + k] * __frcp_rn(sm.aux[0][c0 + k]), bs);
+                    y[k] = (uint32_t)(xi + 0x808080);
+                }
+#pragma unroll
+                for (int m = 1; m < 32; m <<= 1) bs = xor_sum(bs, m);
+                uint32_t d0, d1, d2;
+                digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
+                if (valid) {
+                    reinterpret_cast<uint32_t*>(&sm.qp[0][kap][Gp][h])[s] = d0;
+                    reinterpret_cast<uint32_t*>(&sm.qp[1][kap][Gp][h])[s] = d1;
+                    reinterpret_cast<uint32_t*>(&sm.qp[2][kap][Gp][h])[s] = d2;
+                    if ((l & 31) == 0) {
+                        sm.hv[h][0] = bs;
+                        sm.hv[h][1] = mx / (float)QMAX;
+                    }
                 }
             }
+            __syncthreads();
+            v4i bq[3][2];
 #pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] += __shfl_xor(acc[j], 1);
-            if (hf == 0) {
+            for (int d = 0; d < 3; ++d)
 #pragma unroll
-                for (int j = 0; j < GQ; ++j)
-                    if (j < g) sm.pt[j][t] = t < n ? a.scale_log2 * acc[j] : -INFINITY;
+                for (int kap = 0; kap < 2; ++kap) {
+                    const uint4 u = sm.qp[d][kap][G][hn];
+                    bq[d][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+                }
+            const float beta = head_lane ? sm.hv[hn][0] : 0.f;  // in q~ grid units
+            const float fq = head_lane ? sm.hv[hn][1] : 0.f;    // q~ grid step
+
+            // ---- logits: S^T = codes x q~^T, token 64*sg + 16*tau + 4*G + i -------------------
+            float lg[32];
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    v4i c0 = {0, 0, 0, 0}, c1 = {0, 0, 0, 0}, c2 = {0, 0, 0, 0};
+#pragma unroll
+                    for (int kap = 0; kap < 2; ++kap) {
+                        const v4i A = unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]);
+                        c0 = mfma_i8(A, bq[0][kap], c0);
+                        c1 = mfma_i8(A, bq[1][kap], c1);
+                        c2 = mfma_i8(A, bq[2][kap], c2);
+                    }
+                    const float4 s2 = *reinterpret_cast<const float4*>(&sm.aux[2][64 * sg + 16 * tau + 4 * G]);
+                    const float s2v[4] = {s2.x, s2.y, s2.z, s2.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int raw = (int)((uint32_t)c2[i] << 16) + (int)((uint32_t)c1[i] << 8) + c0[i];
+                        lg[16 * sg + 4 * tau + i] = ((float)raw + beta) * (fq * a.scale_log2 * s2v[i]);
+                    }
+                }
+            const float alpha = softmax_update(lg);  // lg now holds p
+
+            // ---- p~ = p * a_V as two base-256 digits; gamma from the same digits ----------------
+            float pmx = 0.f;
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    const float4 av = *reinterpret_cast<const float4*>(&sm.aux[3][64 * sg + 16 * tau + 4 * G]);
+                    float* p = &lg[16 * sg + 4 * tau];
+                    p[0] *= av.x;
+                    p[1] *= av.y;
+                    p[2] *= av.z;
+                    p[3] *= av.w;
+                    pmx = fmaxf(pmx, fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])));
+                }
+            pmx = xor_max(xor_max(pmx, 16), 32);
+            const float psc = pmx > 0.f ? PMAX / pmx : 0.f;
+            float gam = 0.f;  // gamma in p~ grid units: sum of rounded p~ times b_V / a_V
+            v4i bp[2][2];
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg) {
+                uint32_t d0[4], d1[4];
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    const float* p = &lg[16 * sg + 4 * tau];
+                    const float4 rv = *reinterpret_cast<const float4*>(&sm.aux[4][64 * sg + 16 * tau + 4 * G]);
+                    const float r[4] = {rv.x, rv.y, rv.z, rv.w};
+                    uint32_t y[4];
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const int xi = __float2int_rn(p[i] * psc);
+                        gam = fmaf((float)xi, r[i], gam);
+                        y[i] = (uint32_t)(xi + 0x8080);
+                    }
+                    digits4_2(y[0], y[1], y[2], y[3], d0[tau], d1[tau]);
+                }
+                bp[sg][0] = v4i{(int)d0[0], (int)d0[1], (int)d0[2], (int)d0[3]};
+                bp[sg][1] = v4i{(int)d1[0], (int)d1[1], (int)d1[2], (int)d1[3]};
+            }
+            gam = xor_sum(xor_sum(gam, 16), 32);
+
+            // ---- O^T += codes_V^T x p~^T, channel 16*mt + 4*G + i ------------------------------
+            v4i acc[8][2];
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) acc[mt][0] = acc[mt][1] = v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) {
+                    const v4i A = unit_i8<BITS>(&vw[sg][mt * WPU]);
+                    acc[mt][0] = mfma_i8(A, bp[sg][0], acc[mt][0]);
+                    acc[mt][1] = mfma_i8(A, bp[sg][1], acc[mt][1]);
+                }
+            const float fp = pmx / PMAX;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                const float4 s2 = *reinterpret_cast<const float4*>(&sm.aux[5][16 * mt + 4 * G]);
+                const float s2v[4] = {s2.x, s2.y, s2.z, s2.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int cint = (int)((uint32_t)acc[mt][1][i] << 8) + acc[mt][0][i];
+                    orot[mt][i] = fmaf((float)cint + gam, fp * s2v[i], orot[mt][i] * alpha);
+                }
             }
         }
-        __syncthreads();
-        softmax_tile<GQ>(sm, g, n, nullptr, nullptr, m_run, l_run);
-        {
-            const int c = tid >> 1, hf = tid & 1;
-            float acc[GQ];
-#pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] = 0.f;
-            for (int t = 64 * hf; t < min(n, 64 * hf + 64); ++t) {
-                const float vv = bf16_to_f32(val_ptr(t0 + t)[c]);
-#pragma unroll
-                for (int j = 0; j < GQ; ++j)
-                    if (j < g) acc[j] += sm.pt[j][t] * vv;
-            }
-#pragma unroll
-            for (int j = 0; j < GQ; ++j) acc[j] += __shfl_xor(acc[j], 1);
-            if (hf == 0) {
-#pragma unroll
-                for (int j = 0; j < GQ; ++j)
-                    if (j < g) o[j] = o[j] * sm.hs[j][2] + acc[j];
-            }
-        }
-        __syncthreads();
     }
-    write_partials<GQ>(a, b, kvh, a.n_split, m_run, l_run, o, true);
+
+    // ---- sink and residual (bf16, unrotated): last split only ------------------------------
+    if (last && ns + nr > 0) {
+        // q as the bf16 B operand (hi, plus lo when q is fp32): lane (G, n) holds q[n][32k + 8G ..]
+        v8bf qh[4], ql[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float v = head_lane ? load_q((qrow + hn) * kD + 32 * k + 8 * G + e) : 0.f;
+                const __bf16 hi = (__bf16)v;
+                qh[k][e] = hi;
+                ql[k][e] = (__bf16)(v - (float)hi);
+            }
+        }
+        const bool two = !a.q_bf16;
+        const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
+        for (int chunk = 0; chunk <= nsc; ++chunk) {
+            const bool in_sink = chunk < nsc;
+            const int t0 = in_sink ? chunk * kG : 0;
+            const int cn = in_sink ? min(kG, ns - t0) : nr;
+            if (cn <= 0) continue;
+            const uint16_t* Kp = in_sink ? a.k_sink + ((size_t)stream * a.n_sink + t0) * kD
+                                         : a.k_resid + (size_t)stream * kG * kD;
+            const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
+                                         : a.v_resid + (size_t)stream * kG * kD;
+            float lg[32];
+#pragma unroll
+            for (int tau = 0; tau < 8; ++tau) {
+                v4f acc = {0.f, 0.f, 0.f, 0.f};
+                const int arow = 16 * tau + (l & 15);  // A row of this lane
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    uint4 u = {0u, 0u, 0u, 0u};
+                    if (arow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)arow * kD + 32 * k + 8 * G);
+                    v8bf A;
+                    __builtin_memcpy(&A, &u, 16);
+                    acc = mfma_bf16(A, qh[k], acc);
+                    if (two) acc = mfma_bf16(A, ql[k], acc);
+                }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int t = 16 * tau + 4 * G + i;
+                    lg[4 * tau + i] = t < cn ? acc[i] * a.scale_log2 : -INFINITY;
+                }
+            }
+            const float alpha = softmax_update(lg);
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) orot[mt][i] *= alpha;
+            __syncthreads();  // the previous chunk is done with sm.p / sm.hv
+            if (head_lane) {
+#pragma unroll
+                for (int tau = 0; tau < 8; ++tau)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) sm.p[hn][16 * tau + 4 * G + i] = lg[4 * tau + i];
+                if (G == 0) sm.hv[hn][2] = alpha;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int h = 0; h < GQ; ++h) {
+                if (h < g) {
+                    const float al = sm.hv[h][2];
+                    oplain[h][0] *= al;
+                    oplain[h][1] *= al;
+                }
+            }
+            for (int t = 0; t < cn; ++t) {
+                const uint32_t v2 = reinterpret_cast<const uint32_t*>(Vp + (size_t)t * kD)[l];
+                const float v0 = __uint_as_float(v2 << 16), v1 = __uint_as_float(v2 & 0xFFFF0000u);
+#pragma unroll
+                for (int h = 0; h < GQ; ++h) {
+                    if (h < g) {
+                        const float ph = sm.p[h][t];
+                        oplain[h][0] = fmaf(ph, v0, oplain[h][0]);
+                        oplain[h][1] = fmaf(ph, v1, oplain[h][1]);
+                    }
+                }
+            }
+        }
+    }
+
+    // ---- finish: per-head sum, then the output or a partial --------------------------------
+    const float lt = xor_sum(xor_sum(l_run, 16), 32);
+    if (a.n_split == 1) {
+        __syncthreads();
+        if (head_lane) {
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) sm.q[hn][16 * mt + 4 * G + i] = orot[mt][i];
+            if (G == 0) sm.hv[hn][3] = lt;
+        }
+        __syncthreads();
+        lds_hadamard<GQ>(sm.q, g);
+#pragma unroll
+        for (int h = 0; h < GQ; ++h) {
+            if (h < g) {
+                const float L = sm.hv[h][3];
+                float o0 = sm.q[h][2 * l] * kInvSqrt128 + oplain[h][0];
+                float o1 = sm.q[h][2 * l + 1] * kInvSqrt128 + oplain[h][1];
+                o0 = L > 0.f ? o0 / L : 0.f;
+                o1 = L > 0.f ? o1 / L : 0.f;
+                const size_t idx = (qrow + h) * kD + 2 * l;
+                if (a.out_bf16)
+                    reinterpret_cast<uint32_t*>(a.out)[idx >> 1] =
+                        (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
+                else
+                    *reinterpret_cast<float2*>(static_cast<float*>(a.out) + idx) = make_float2(o0, o1);
+            }
+        }
+    } else {
+        if (head_lane) {
+            float* P = a.ws + ((qrow + hn) * a.n_split + split) * kPart;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt)
+                *reinterpret_cast<float4*>(P + 4 + 16 * mt + 4 * G) =
+                    make_float4(orot[mt][0], orot[mt][1], orot[mt][2], orot[mt][3]);
+            if (G == 0) {
+                P[0] = m_run;
+                P[1] = lt;
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < GQ; ++h) {
+            if (h < g) {
+                float* P = a.ws + ((qrow + h) * a.n_split + split) * kPart;
+                *reinterpret_cast<float2*>(P + 132 + 2 * l) = make_float2(oplain[h][0], oplain[h][1]);
+            }
+        }
+    }
 }
 
-// One 128-thread workgroup per (sequence, query head): log-sum-exp merge of the partials,
-// inverse rotation of the body part, normalisation.
-__global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a, void* out, int out_bf16) {
+// One 128-thread workgroup per (sequence, query head): log-sum-exp merge of the split
+// partials, inverse rotation of the body part, normalisation.
+__global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
     __shared__ float orot[kD];
     const int c = threadIdx.x;
-    const int bh = blockIdx.x;
-    const float* P = a.ws + (size_t)bh * (a.n_split + 1) * kPart;
+    const size_t bh = blockIdx.x;
+    const float* P = a.ws + bh * a.n_split * kPart;
     float M = -INFINITY;
-    for (int s = 0; s <= a.n_split; ++s)
+    for (int s = 0; s < a.n_split; ++s)
         if (P[s * kPart + 1] > 0.f) M = fmaxf(M, P[s * kPart]);
-    float L = 0.f, acc = 0.f;
+    float L = 0.f, acc = 0.f, pl = 0.f;
     for (int s = 0; s < a.n_split; ++s) {
         const float l = P[s * kPart + 1];
         if (l > 0.f) {
             const float w = exp2f(P[s * kPart] - M);
             L += w * l;
             acc += w * P[s * kPart + 4 + c];
+            pl += w * P[s * kPart + 132 + c];
         }
     }
     orot[c] = acc;
@@ -389,33 +543,30 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a, void* out, i
         }
         __syncthreads();
     }
-    float o = orot[c] * kInvSqrt128;
-    const float* Pp = P + (size_t)a.n_split * kPart;
-    if (Pp[1] > 0.f) {
-        const float w = exp2f(Pp[0] - M);
-        L += w * Pp[1];
-        o += w * Pp[4 + c];
-    }
+    float o = orot[c] * kInvSqrt128 + pl;
     o = L > 0.f ? o / L : 0.f;
-    const size_t idx = (size_t)bh * kD + c;
-    if (out_bf16)
-        static_cast<uint16_t*>(out)[idx] = f32_to_bf16(o);
+    const size_t idx = bh * kD + c;
+    if (a.out_bf16)
+        static_cast<uint16_t*>(a.out)[idx] = f32_to_bf16(o);
     else
-        static_cast<float*>(out)[idx] = o;
+        static_cast<float*>(a.out)[idx] = o;
 }
 
-template <int GQ>
-hipError_t launch_g(const DecodeArgs& a, int batch, void* out, bool out_bf16, hipStream_t stream) {
+template <int BITS, int GQ>
+hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
-    hipLaunchKernelGGL(k_decode_body<GQ>, dim3((unsigned)(streams * a.n_split)), dim3(kThreads), 0, stream, a);
+    hipLaunchKernelGGL((k_decode<BITS, GQ>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_decode_plain<GQ>, dim3((unsigned)streams), dim3(kThreads), 0, stream, a);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_decode_merge, dim3((unsigned)(batch * a.n_q)), dim3(128), 0, stream, a, out,
-                       out_bf16 ? 1 : 0);
+    if (e != hipSuccess || a.n_split == 1) return e;
+    hipLaunchKernelGGL(k_decode_merge, dim3((unsigned)(batch * a.n_q)), dim3(128), 0, stream, a);
     return hipGetLastError();
+}
+
+template <int BITS>
+hipError_t launch_bits(const DecodeArgs& a, int batch, hipStream_t stream) {
+    if (a.g <= 4) return launch_cfg<BITS, 4>(a, batch, stream);
+    if (a.g <= 8) return launch_cfg<BITS, 8>(a, batch, stream);
+    return launch_cfg<BITS, 16>(a, batch, stream);
 }
 
 }  // namespace
@@ -426,22 +577,22 @@ DecodePlan plan_decode(int batch, int n_kv, int max_len, int n_sink, int max_blo
     if (nb > max_blocks) nb = max_blocks;
     p.max_blocks_used = nb;
     const int streams = batch * n_kv;
-    // aim for about 2048 workgroups (8 per CU) but never split below one tile
-    int want = (2048 + streams - 1) / streams;
-    if (want < 1) want = 1;
-    if (nb < 1) {
+    // one wave per (split, stream): aim for about 4096 waves (4 per SIMD), at least one tile each
+    int want = (4096 + streams - 1) / streams;
+    if (want > nb) want = nb;
+    if (want <= 1) {
         p.n_split = 1;
-        p.blocks_per_split = 1;
+        p.blocks_per_split = nb > 0 ? nb : 1;
         return p;
     }
-    if (want > nb) want = nb;
     p.blocks_per_split = (nb + want - 1) / want;
     p.n_split = (nb + p.blocks_per_split - 1) / p.blocks_per_split;
     return p;
 }
 
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan) {
-    return (size_t)batch * n_q * (plan.n_split + 1) * kPart * sizeof(float);
+    if (plan.n_split == 1) return 0;
+    return (size_t)batch * n_q * plan.n_split * kPart * sizeof(float);
 }
 
 hipError_t launch_decode(const kvarn_cache& c, int bits, int n_sink, int n_q, const void* q, bool q_bf16, void* out,
@@ -456,21 +607,18 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int n_sink, int n_q, co
     a.seq_len = c.seq_len;
     a.q = q;
     a.q_bf16 = q_bf16 ? 1 : 0;
+    a.out = out;
+    a.out_bf16 = out_bf16 ? 1 : 0;
     a.n_kv = c.n_kv;
     a.n_q = n_q;
     a.g = n_q / c.n_kv;
     a.max_blocks = c.max_blocks;
     a.n_sink = n_sink;
-    a.bits = bits;
     a.scale_log2 = sm_scale * kLog2e;
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
     a.ws = ws;
-    if (a.g <= 1) return launch_g<1>(a, c.batch, out, out_bf16, stream);
-    if (a.g <= 2) return launch_g<2>(a, c.batch, out, out_bf16, stream);
-    if (a.g <= 4) return launch_g<4>(a, c.batch, out, out_bf16, stream);
-    if (a.g <= 8) return launch_g<8>(a, c.batch, out, out_bf16, stream);
-    return launch_g<16>(a, c.batch, out, out_bf16, stream);
+    return bits == 2 ? launch_bits<2>(a, c.batch, stream) : launch_bits<4>(a, c.batch, stream);
 }
 
 }  // namespace kvarn
