@@ -506,6 +506,395 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     }
 }
 
+// ---- group size <= 4: digit planes in the MFMA columns ------------------------------------
+// Column n = 4*h + j of an MFMA carries digit j (j < 3; j = 3 is zero) of head h.  After a
+// product, the four lanes of a quad (j = 0..3, same head) hold digit-partial sums of four rows;
+// a reduce-scatter inside the quad (two DPP exchanges) leaves lane j with the full, digit-
+// weighted sum of row j.  One MFMA then serves all three digits, and every lane finishes
+// exactly one useful value per 16 rows: per-value VALU work is not replicated across columns.
+
+__device__ __forceinline__ int quad_x1(int v) { return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true); }
+__device__ __forceinline__ int quad_x2(int v) { return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true); }
+__device__ __forceinline__ float quad_x1f(float v) { return __int_as_float(quad_x1(__float_as_int(v))); }
+__device__ __forceinline__ float quad_x2f(float v) { return __int_as_float(quad_x2(__float_as_int(v))); }
+// max / sum over the 16 lanes of a head: the quad, then the four lane groups G
+__device__ __forceinline__ float head_max(float v) {
+    v = fmaxf(v, quad_x1f(v));
+    v = fmaxf(v, quad_x2f(v));
+    return xor_max(xor_max(v, 16), 32);
+}
+__device__ __forceinline__ float head_sum(float v) {
+    v += quad_x1f(v);
+    v += quad_x2f(v);
+    return xor_sum(xor_sum(v, 16), 32);
+}
+
+// c: digit-j partial sums of rows 0..3 (this lane's slot j); returns sum_j 256^j c_j[row j]
+// for row j of this lane.
+__device__ __forceinline__ int quad_combine(v4i c, int j) {
+    const uint32_t sh = 8u * (uint32_t)j;
+    const int r0 = (int)((uint32_t)c[0] << sh), r1 = (int)((uint32_t)c[1] << sh);
+    const int r2 = (int)((uint32_t)c[2] << sh), r3 = (int)((uint32_t)c[3] << sh);
+    const bool hi = (j & 2) != 0, lo = (j & 1) != 0;
+    const int k0 = hi ? r2 : r0, k1 = hi ? r3 : r1, s0 = hi ? r0 : r2, s1 = hi ? r1 : r3;
+    const int a0 = k0 + quad_x2(s0), a1 = k1 + quad_x2(s1);  // rows {2hi, 2hi+1}, digits j, j^2
+    const int k = lo ? a1 : a0, s = lo ? a0 : a1;
+    return k + quad_x1(s);                                   // row j, all four digits
+}
+
+// Lane j of a quad holds y (row j of a 4 x 4 byte matrix); returns column j: byte i of the
+// result is byte j of lane i's y.  Two exchanges (partners j ^ 2, then j ^ 1), each a DPP move
+// and a byte permute.
+__device__ __forceinline__ uint32_t quad_transpose_bytes(uint32_t y, int j) {
+    const uint32_t selA = j < 2 ? 0x05040100u : 0x03020706u;
+    const uint32_t selB = (j & 1) ? 0x03070105u : 0x06020400u;
+    const uint32_t t = perm((uint32_t)quad_x2((int)y), y, selA);
+    return perm((uint32_t)quad_x1((int)t), t, selB);
+}
+
+struct Smem4 {
+    float q[4][kD];        // rotated q; reused for the inverse rotation of the output
+    float aux[6][kD];      // a_K b_K s2_K a_V b_V s2_V of the current tile (b_V becomes b_V / a_V)
+    uint4 qp[4][2][4][4];  // q~ digit planes [digit slot][kappa][G][head]; slot 3 stays zero
+    float hv[4][4];        // per head: beta, q~ step, alpha, l
+    float p[4][kG];        // probabilities of a bf16 chunk (sink / residual)
+};
+
+template <int BITS>
+__global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
+    __shared__ Smem4 sm;
+    constexpr int WPU = BITS / 2;
+    constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // fixed-point bound of q~ and p~
+    constexpr float MAGIC = 12582912.f;                  // 1.5 * 2^23: x + MAGIC rounds x to an integer
+    constexpr uint32_t MAGIC_BITS = 0x4B400000u;
+    const int l = threadIdx.x, G = l >> 4, n = l & 15, h = n >> 2, j = n & 3;
+    const int g = a.g;
+    const bool head_ok = h < g;
+    const int split = blockIdx.x % a.n_split;
+    const int stream = blockIdx.x / a.n_split;
+    const int b = stream / a.n_kv, kvh = stream % a.n_kv;
+    const int len = max(a.seq_len[b], 0);
+    const int ns = min(len, a.n_sink);
+    const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
+    const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
+    const bool last = split == a.n_split - 1;
+    const int blk0 = split * a.bps;
+    const int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
+    const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
+    const size_t tb = tile_bytes(BITS), cb = code_bytes(BITS);
+
+    float m_run = -INFINITY, l_run = 0.f;  // head h; l_run is this lane's partial sum
+    float orot[8];                         // head h, channel 16*mt + 4*G + j (rotated domain)
+    float oplain[4][2];                    // head hh, channel 2*l + jj (unrotated)
+#pragma unroll
+    for (int mt = 0; mt < 8; ++mt) orot[mt] = 0.f;
+#pragma unroll
+    for (int hh = 0; hh < 4; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
+
+    auto load_q = [&](size_t idx) -> float {
+        return a.q_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.q)[idx]) : static_cast<const float*>(a.q)[idx];
+    };
+    // online softmax over this lane's 8 logits (log2 units; -inf = absent) -> p, returns alpha
+    auto softmax_update = [&](float (&lg)[8], bool maybe_absent) -> float {
+        float mx = lg[0];
+#pragma unroll
+        for (int k = 1; k < 8; ++k) mx = fmaxf(mx, lg[k]);
+        mx = head_max(mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        float s = 0.f;
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+            float p = __builtin_amdgcn_exp2f(lg[k] - m_new);
+            if (maybe_absent) p = lg[k] == -INFINITY ? 0.f : p;
+            lg[k] = p;
+            s += p;
+        }
+        l_run = l_run * alpha + s;
+        m_run = m_new;
+        return alpha;
+    };
+
+    if (blk0 < blk1) {
+        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] = load_q(qrow * kD + idx);
+        if (l < 32) sm.qp[3][l >> 4][(l >> 2) & 3][l & 3] = make_uint4(0u, 0u, 0u, 0u);
+        __syncthreads();
+        lds_hadamard<4>(sm.q, g);
+        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
+
+        uint4 kc[2][2 * WPU], vc[2][2 * WPU], ax0, ax1, ax2;
+        const int ax1_off = l < 32 ? (64 + l) * 16 : (l - 32) * 16;
+        auto load_tile = [&](int blk) {
+            const uint8_t* kt = a.k_body + ((size_t)stream * a.max_blocks + blk) * tb;
+            const uint8_t* vt = a.v_body + ((size_t)stream * a.max_blocks + blk) * tb;
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int k = 0; k < 2 * WPU; ++k) {
+                    kc[s][k] = reinterpret_cast<const uint4*>(kt)[(s * 64 + l) * 2 * WPU + k];
+                    vc[s][k] = reinterpret_cast<const uint4*>(vt)[(s * 64 + l) * 2 * WPU + k];
+                }
+            ax0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
+            ax1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + ax1_off);
+            ax2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
+        };
+        load_tile(blk0);
+
+        for (int blk = blk0; blk < blk1; ++blk) {
+            __syncthreads();
+            reinterpret_cast<uint4*>(&sm.aux[0][0])[l] = ax0;
+            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 64] = ax1;
+            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 128] = ax2;
+            uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int k = 0; k < 2 * WPU; ++k) {
+                    kw[s][4 * k] = kc[s][k].x; kw[s][4 * k + 1] = kc[s][k].y;
+                    kw[s][4 * k + 2] = kc[s][k].z; kw[s][4 * k + 3] = kc[s][k].w;
+                    vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
+                    vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
+                }
+            if (blk + 1 < blk1) load_tile(blk + 1);
+            __syncthreads();
+            sm.aux[4][2 * l] *= __frcp_rn(sm.aux[3][2 * l]);  // b_V / a_V, read after the next barrier
+            sm.aux[4][2 * l + 1] *= __frcp_rn(sm.aux[3][2 * l + 1]);
+
+            // q~ digit planes, spread over all lanes: group (head, kappa, G', s) = 4 channels
+            for (int gi0 = 0; gi0 < g * 32; gi0 += 64) {
+                const int gi = gi0 + l;
+                const bool valid = gi < g * 32;
+                const int hh = min(gi >> 5, g - 1), rem = gi & 31;
+                const int kap = rem >> 4, Gp = (rem >> 2) & 3, s = rem & 3;
+                const int c0 = 64 * kap + 16 * Gp + 4 * s;
+                const float4 q4 = *reinterpret_cast<const float4*>(&sm.q[hh][c0]);
+                const float4 a4 = *reinterpret_cast<const float4*>(&sm.aux[0][c0]);
+                const float4 b4 = *reinterpret_cast<const float4*>(&sm.aux[1][c0]);
+                const float qv[4] = {q4.x, q4.y, q4.z, q4.w}, av[4] = {a4.x, a4.y, a4.z, a4.w};
+                const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                float qt[4], mx = 0.f;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    qt[k] = valid ? qv[k] * av[k] : 0.f;
+                    mx = fmaxf(mx, fabsf(qt[k]));
+                }
+#pragma unroll
+                for (int m = 1; m < 32; m <<= 1) mx = xor_max(mx, m);
+                const float sc = mx > 0.f ? (float)QMAX / mx : 0.f;
+                float bs = 0.f;  // beta in q~ grid units: rounded q~ times b_K / a_K
+                uint32_t y[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float yf = fmaf(qt[k], sc, MAGIC);
+                    bs = fmaf(yf - MAGIC, bv[k] * __frcp_rn(av[k]), bs);
+                    y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
+                }
+#pragma unroll
+                for (int m = 1; m < 32; m <<= 1) bs = xor_sum(bs, m);
+                uint32_t d0, d1, d2;
+                digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
+                if (valid) {
+                    reinterpret_cast<uint32_t*>(&sm.qp[0][kap][Gp][hh])[s] = d0;
+                    reinterpret_cast<uint32_t*>(&sm.qp[1][kap][Gp][hh])[s] = d1;
+                    reinterpret_cast<uint32_t*>(&sm.qp[2][kap][Gp][hh])[s] = d2;
+                    if ((l & 31) == 0) {
+                        sm.hv[hh][0] = bs;
+                        sm.hv[hh][1] = mx / (float)QMAX;
+                    }
+                }
+            }
+            __syncthreads();
+            v4i bq[2];
+#pragma unroll
+            for (int kap = 0; kap < 2; ++kap) {
+                const uint4 u = sm.qp[j][kap][G][h];
+                bq[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+            }
+            const float beta = head_ok ? sm.hv[h][0] : 0.f;                  // q~ grid units
+            const float fqs = head_ok ? sm.hv[h][1] * a.scale_log2 : 0.f;  // grid step * scale
+
+            // logits of token 64*sg + 16*tau + 4*G + j
+            float lg[8];
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    v4i c = {0, 0, 0, 0};
+#pragma unroll
+                    for (int kap = 0; kap < 2; ++kap) c = mfma_i8(unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]), bq[kap], c);
+                    const int v = quad_combine(c, j);
+                    lg[4 * sg + tau] = ((float)v + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + 4 * G + j]);
+                }
+            const float alpha = softmax_update(lg, false);
+
+            // p~ = p * a_V as digit planes; gamma from the same rounded integers
+            float pmx = 0.f;
+#pragma unroll
+            for (int k = 0; k < 8; ++k) {
+                lg[k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + 4 * G + j];
+                pmx = fmaxf(pmx, lg[k]);
+            }
+            pmx = head_max(pmx);
+            const float psc = pmx > 0.f ? (float)QMAX / pmx : 0.f;
+            float gam = 0.f;
+            v4i bp[2];
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg) {
+                uint32_t D[4];
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    const float yf = fmaf(lg[4 * sg + tau], psc, MAGIC);
+                    gam = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + 4 * G + j], gam);
+                    // bytes of y: the three digits plus 128 each, and 0x80 on top (digit slot 3
+                    // becomes zero); lane j takes digit j of the quad's four rows
+                    const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
+                    D[tau] = quad_transpose_bytes(y, j) ^ 0x80808080u;
+                }
+                bp[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
+            }
+            gam = head_sum(gam);
+
+            // PV: channel 16*mt + 4*G + j
+            v4i acc[8];
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) acc[mt] = v4i{0, 0, 0, 0};
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) acc[mt] = mfma_i8(unit_i8<BITS>(&vw[sg][mt * WPU]), bp[sg], acc[mt]);
+            const float fp = pmx / (float)QMAX;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                const int v = quad_combine(acc[mt], j);
+                orot[mt] = fmaf((float)v + gam, fp * sm.aux[5][16 * mt + 4 * G + j], orot[mt] * alpha);
+            }
+        }
+    }
+
+    // ---- sink and residual (bf16, unrotated): last split only ------------------------------
+    if (last && ns + nr > 0) {
+        // q of head h as the bf16 B operand in every column of the head's quad (hi, plus lo
+        // when q is fp32); lane (G, 4h + j) holds q[h][32k + 8G ..]
+        v8bf qh[4], ql[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const float v = head_ok ? load_q((qrow + h) * kD + 32 * k + 8 * G + e) : 0.f;
+                const __bf16 hi = (__bf16)v;
+                qh[k][e] = hi;
+                ql[k][e] = (__bf16)(v - (float)hi);
+            }
+        }
+        const bool two = !a.q_bf16;
+        const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
+        for (int chunk = 0; chunk <= nsc; ++chunk) {
+            const bool in_sink = chunk < nsc;
+            const int t0 = in_sink ? chunk * kG : 0;
+            const int cn = in_sink ? min(kG, ns - t0) : nr;
+            if (cn <= 0) continue;
+            const uint16_t* Kp = in_sink ? a.k_sink + ((size_t)stream * a.n_sink + t0) * kD
+                                         : a.k_resid + (size_t)stream * kG * kD;
+            const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
+                                         : a.v_resid + (size_t)stream * kG * kD;
+            float lg[8];
+#pragma unroll
+            for (int tau = 0; tau < 8; ++tau) {
+                v4f acc = {0.f, 0.f, 0.f, 0.f};
+                const int arow = 16 * tau + (l & 15);
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    uint4 u = {0u, 0u, 0u, 0u};
+                    if (arow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)arow * kD + 32 * k + 8 * G);
+                    v8bf A;
+                    __builtin_memcpy(&A, &u, 16);
+                    acc = mfma_bf16(A, qh[k], acc);
+                    if (two) acc = mfma_bf16(A, ql[k], acc);
+                }
+                // all four columns of the quad hold the same logits; lane j keeps row j
+                const float v = j == 0 ? acc[0] : (j == 1 ? acc[1] : (j == 2 ? acc[2] : acc[3]));
+                lg[tau] = 16 * tau + 4 * G + j < cn ? v * a.scale_log2 : -INFINITY;
+            }
+            const float alpha = softmax_update(lg, true);
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) orot[mt] *= alpha;
+            __syncthreads();  // the previous chunk is done with sm.p / sm.hv
+            if (head_ok) {
+#pragma unroll
+                for (int tau = 0; tau < 8; ++tau) sm.p[h][16 * tau + 4 * G + j] = lg[tau];
+                if (G == 0 && j == 0) sm.hv[h][2] = alpha;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int hh = 0; hh < 4; ++hh) {
+                if (hh < g) {
+                    const float al = sm.hv[hh][2];
+                    oplain[hh][0] *= al;
+                    oplain[hh][1] *= al;
+                }
+            }
+            for (int t = 0; t < cn; ++t) {
+                const uint32_t v2 = reinterpret_cast<const uint32_t*>(Vp + (size_t)t * kD)[l];
+                const float v0 = __uint_as_float(v2 << 16), v1 = __uint_as_float(v2 & 0xFFFF0000u);
+#pragma unroll
+                for (int hh = 0; hh < 4; ++hh) {
+                    if (hh < g) {
+                        const float ph = sm.p[hh][t];
+                        oplain[hh][0] = fmaf(ph, v0, oplain[hh][0]);
+                        oplain[hh][1] = fmaf(ph, v1, oplain[hh][1]);
+                    }
+                }
+            }
+        }
+    }
+
+    // ---- finish ------------------------------------------------------------------------------
+    const float lt = head_sum(l_run);
+    if (a.n_split == 1) {
+        __syncthreads();
+        if (head_ok) {
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) sm.q[h][16 * mt + 4 * G + j] = orot[mt];
+            if (G == 0 && j == 0) sm.hv[h][3] = lt;
+        }
+        __syncthreads();
+        lds_hadamard<4>(sm.q, g);
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+            if (hh < g) {
+                const float L = sm.hv[hh][3];
+                float o0 = sm.q[hh][2 * l] * kInvSqrt128 + oplain[hh][0];
+                float o1 = sm.q[hh][2 * l + 1] * kInvSqrt128 + oplain[hh][1];
+                o0 = L > 0.f ? o0 / L : 0.f;
+                o1 = L > 0.f ? o1 / L : 0.f;
+                const size_t idx = (qrow + hh) * kD + 2 * l;
+                if (a.out_bf16)
+                    reinterpret_cast<uint32_t*>(a.out)[idx >> 1] =
+                        (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
+                else
+                    *reinterpret_cast<float2*>(static_cast<float*>(a.out) + idx) = make_float2(o0, o1);
+            }
+        }
+    } else {
+        if (head_ok) {
+            float* P = a.ws + ((qrow + h) * a.n_split + split) * kPart;
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) P[4 + 16 * mt + 4 * G + j] = orot[mt];
+            if (G == 0 && j == 0) {
+                P[0] = m_run;
+                P[1] = lt;
+            }
+        }
+#pragma unroll
+        for (int hh = 0; hh < 4; ++hh) {
+            if (hh < g) {
+                float* P = a.ws + ((qrow + hh) * a.n_split + split) * kPart;
+                *reinterpret_cast<float2*>(P + 132 + 2 * l) = make_float2(oplain[hh][0], oplain[hh][1]);
+            }
+        }
+    }
+}
+
 // One 128-thread workgroup per (sequence, query head): log-sum-exp merge of the split
 // partials, inverse rotation of the body part, normalisation.
 __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
@@ -555,7 +944,10 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
 template <int BITS, int GQ>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
-    hipLaunchKernelGGL((k_decode<BITS, GQ>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+    if constexpr (GQ == 4)
+        hipLaunchKernelGGL((k_decode4<BITS>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+    else
+        hipLaunchKernelGGL((k_decode<BITS, GQ>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_split == 1) return e;
     hipLaunchKernelGGL(k_decode_merge, dim3((unsigned)(batch * a.n_q)), dim3(128), 0, stream, a);
