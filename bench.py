@@ -33,6 +33,9 @@ def parse():
     ap.add_argument("--workload", default="throughput")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target wall time of the oracle sample")
+    ap.add_argument("--calib-copy-gib", type=float, default=0.0,
+                    help="after the run, copy this many GiB device-to-device (a known-size reference for "
+                         "hardware byte counters)")
     return ap.parse_args()
 
 
@@ -164,6 +167,15 @@ def main():
         "quantize": q_res,
     }
     print(json.dumps(line), flush=True)
+
+    if args.calib_copy_gib > 0:
+        nbytes = int(args.calib_copy_gib * (1 << 30))
+        src = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] calibration copy: {nbytes} bytes read + {nbytes} bytes written", file=sys.stderr, flush=True)
 
 
 def cpu_baseline(built, q, length, scale, target_s):

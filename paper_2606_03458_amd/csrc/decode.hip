@@ -227,8 +227,8 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
             if (blk + 1 < blk1) load_tile(blk + 1);  // prefetch, consumed next iteration
             __syncthreads();
             // value offsets as ratios b_V / a_V (read after the next barrier)
-            sm.aux[4][2 * l] *= __frcp_rn(sm.aux[3][2 * l]);
-            sm.aux[4][2 * l + 1] *= __frcp_rn(sm.aux[3][2 * l + 1]);
+            sm.aux[4][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l]);
+            sm.aux[4][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l + 1]);
 
             // ---- q~ = q_rot * a_K as three base-256 digits, spread over all 64 lanes ----------
             // group gi = (head, kappa, G', s) covers channels 64*kappa + 16*G' + 4*s .. +3
@@ -254,7 +254,7 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const int xi = __float2int_rn(qt[k] * sc);
-                    bs = fmaf((float)xi, sm.aux[1][c0 + k] * __frcp_rn(sm.aux[0][c0 + k]), bs);
+                    bs = fmaf((float)xi, sm.aux[1][c0 + k] * __builtin_amdgcn_rcpf(sm.aux[0][c0 + k]), bs);
                     y[k] = (uint32_t)(xi + 0x808080);
                 }
 #pragma unroll
@@ -561,7 +561,7 @@ struct Smem4 {
 };
 
 template <int BITS>
-__global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 3 : 2, 8))) void k_decode4(DecodeArgs a) {
     __shared__ Smem4 sm;
     constexpr int WPU = BITS / 2;
     constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // fixed-point bound of q~ and p~
@@ -622,29 +622,46 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
         lds_hadamard<4>(sm.q, g);
         for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
 
+        // Tiles are double-buffered in registers: while one buffer is consumed, the next
+        // tile's loads are in flight into the other (the loop is unrolled by two).
+        // One register buffer per tile part, refilled as soon as its current contents are
+        // consumed: the next tile's aux right after it is staged in LDS, its key codes right
+        // after the QK products, its value codes right after the PV products.
         uint4 kc[2][2 * WPU], vc[2][2 * WPU], ax0, ax1, ax2;
         const int ax1_off = l < 32 ? (64 + l) * 16 : (l - 32) * 16;
-        auto load_tile = [&](int blk) {
-            const uint8_t* kt = a.k_body + ((size_t)stream * a.max_blocks + blk) * tb;
-            const uint8_t* vt = a.v_body + ((size_t)stream * a.max_blocks + blk) * tb;
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) {
-                    kc[s][k] = reinterpret_cast<const uint4*>(kt)[(s * 64 + l) * 2 * WPU + k];
-                    vc[s][k] = reinterpret_cast<const uint4*>(vt)[(s * 64 + l) * 2 * WPU + k];
-                }
+        auto tile_k = [&](int b_) { return a.k_body + ((size_t)stream * a.max_blocks + b_) * tb; };
+        auto tile_v = [&](int b_) { return a.v_body + ((size_t)stream * a.max_blocks + b_) * tb; };
+        auto load_aux = [&](int b_) {
+            const uint8_t* kt = tile_k(b_);
+            const uint8_t* vt = tile_v(b_);
             ax0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
             ax1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + ax1_off);
             ax2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
         };
-        load_tile(blk0);
+        auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = reinterpret_cast<const uint4*>(t)[(s * 64 + l) * 2 * WPU + k];
+        };
+        load_codes(tile_k(blk0), kc);
+        load_codes(tile_v(blk0), vc);
+        load_aux(blk0);
 
         for (int blk = blk0; blk < blk1; ++blk) {
-            __syncthreads();
+            const bool more = blk + 1 < blk1;
+            __syncthreads();  // the previous tile is done with sm.aux / sm.qp
             reinterpret_cast<uint4*>(&sm.aux[0][0])[l] = ax0;
             reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 64] = ax1;
             reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 128] = ax2;
+            __syncthreads();
+            if (more) load_aux(blk + 1);
+            // offsets as ratios b / a: keys per channel, values per token
+            sm.aux[1][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l]);
+            sm.aux[1][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l + 1]);
+            sm.aux[4][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l]);
+            sm.aux[4][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l + 1]);
+            __syncthreads();
             uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -655,11 +672,6 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
                     vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
                     vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
                 }
-            if (blk + 1 < blk1) load_tile(blk + 1);
-            __syncthreads();
-            sm.aux[4][2 * l] *= __frcp_rn(sm.aux[3][2 * l]);  // b_V / a_V, read after the next barrier
-            sm.aux[4][2 * l + 1] *= __frcp_rn(sm.aux[3][2 * l + 1]);
-
             // q~ digit planes, spread over all lanes: group (head, kappa, G', s) = 4 channels
             for (int gi0 = 0; gi0 < g * 32; gi0 += 64) {
                 const int gi = gi0 + l;
@@ -669,9 +681,9 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
                 const int c0 = 64 * kap + 16 * Gp + 4 * s;
                 const float4 q4 = *reinterpret_cast<const float4*>(&sm.q[hh][c0]);
                 const float4 a4 = *reinterpret_cast<const float4*>(&sm.aux[0][c0]);
-                const float4 b4 = *reinterpret_cast<const float4*>(&sm.aux[1][c0]);
+                const float4 r4 = *reinterpret_cast<const float4*>(&sm.aux[1][c0]);
                 const float qv[4] = {q4.x, q4.y, q4.z, q4.w}, av[4] = {a4.x, a4.y, a4.z, a4.w};
-                const float bv[4] = {b4.x, b4.y, b4.z, b4.w};
+                const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
                 float qt[4], mx = 0.f;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
@@ -680,13 +692,13 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
                 }
 #pragma unroll
                 for (int m = 1; m < 32; m <<= 1) mx = xor_max(mx, m);
-                const float sc = mx > 0.f ? (float)QMAX / mx : 0.f;
+                const float sc = mx > 0.f ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
                 float bs = 0.f;  // beta in q~ grid units: rounded q~ times b_K / a_K
                 uint32_t y[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const float yf = fmaf(qt[k], sc, MAGIC);
-                    bs = fmaf(yf - MAGIC, bv[k] * __frcp_rn(av[k]), bs);
+                    bs = fmaf(yf - MAGIC, rk[k], bs);
                     y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
                 }
 #pragma unroll
@@ -699,7 +711,7 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
                     reinterpret_cast<uint32_t*>(&sm.qp[2][kap][Gp][hh])[s] = d2;
                     if ((l & 31) == 0) {
                         sm.hv[hh][0] = bs;
-                        sm.hv[hh][1] = mx / (float)QMAX;
+                        sm.hv[hh][1] = mx * (1.0f / (float)QMAX);
                     }
                 }
             }
@@ -725,6 +737,7 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
                     const int v = quad_combine(c, j);
                     lg[4 * sg + tau] = ((float)v + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + 4 * G + j]);
                 }
+            if (more) load_codes(tile_k(blk + 1), kc);
             const float alpha = softmax_update(lg, false);
 
             // p~ = p * a_V as digit planes; gamma from the same rounded integers
@@ -735,7 +748,7 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
                 pmx = fmaxf(pmx, lg[k]);
             }
             pmx = head_max(pmx);
-            const float psc = pmx > 0.f ? (float)QMAX / pmx : 0.f;
+            const float psc = pmx > 0.f ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
             float gam = 0.f;
             v4i bp[2];
 #pragma unroll
@@ -761,8 +774,10 @@ __global__ __launch_bounds__(64) void k_decode4(DecodeArgs a) {
 #pragma unroll
             for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
-                for (int mt = 0; mt < 8; ++mt) acc[mt] = mfma_i8(unit_i8<BITS>(&vw[sg][mt * WPU]), bp[sg], acc[mt]);
-            const float fp = pmx / (float)QMAX;
+                for (int mt = 0; mt < 8; ++mt)
+                    acc[mt] = mfma_i8(unit_i8<BITS>(&vw[sg][mt * WPU]), bp[sg], acc[mt]);
+            if (more) load_codes(tile_v(blk + 1), vc);
+            const float fp = pmx * (1.0f / (float)QMAX);
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) {
                 const int v = quad_combine(acc[mt], j);
