@@ -506,40 +506,47 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     }
 }
 
-// ---- group size <= 4: digit planes in the MFMA columns ------------------------------------
-// Column n = 4*h + j of an MFMA carries digit j (j < 3; j = 3 is zero) of head h.  After a
-// product, the four lanes of a quad (j = 0..3, same head) hold digit-partial sums of four rows;
-// a reduce-scatter inside the quad (two DPP exchanges) leaves lane j with the full, digit-
-// weighted sum of row j.  One MFMA then serves all three digits, and every lane finishes
-// exactly one useful value per 16 rows: per-value VALU work is not replicated across columns.
+// ---- group size <= 4: digit planes in the MFMA rows ----------------------------------------
+// Both products take the real-valued side (q~ or p~, as base-256 digit planes) as the A operand
+// and the codes as B.  Row 4*h + j of A is digit j of head h (j = 3 is zero).  The A and B
+// register layouts of the 16x16x64 product are mirror images, so the code operands are the same
+// registers as with codes in A.  Output lane (G, n) then receives, in its four accumulator
+// registers, the digit partial sums of head G for column n (a token in QK, a channel in PV) and
+// recombines them in-lane with two shifted adds.  One MFMA serves all three digits, and each
+// lane finishes exactly one useful value per product.
+//
+// Between the products the probabilities move from the QK output layout (lane (G, n) = head G,
+// token n of each 16) to the PV A layout (lane (G, 4h + j) = digit j of head h, tokens 4G..4G+3
+// of each 16): a byte transpose inside each quad, then one lane permutation (ds_bpermute).
 
-__device__ __forceinline__ int quad_x1(int v) { return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true); }
-__device__ __forceinline__ int quad_x2(int v) { return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true); }
-__device__ __forceinline__ float quad_x1f(float v) { return __int_as_float(quad_x1(__float_as_int(v))); }
-__device__ __forceinline__ float quad_x2f(float v) { return __int_as_float(quad_x2(__float_as_int(v))); }
-// max / sum over the 16 lanes of a head: the quad, then the four lane groups G
-__device__ __forceinline__ float head_max(float v) {
-    v = fmaxf(v, quad_x1f(v));
-    v = fmaxf(v, quad_x2f(v));
-    return xor_max(xor_max(v, 16), 32);
+__device__ __forceinline__ int dpp_x1(int v) { return __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true); }
+__device__ __forceinline__ int dpp_x2(int v) { return __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true); }
+__device__ __forceinline__ int dpp_half_mirror(int v) { return __builtin_amdgcn_mov_dpp(v, 0x141, 0xF, 0xF, true); }
+__device__ __forceinline__ int dpp_mirror(int v) { return __builtin_amdgcn_mov_dpp(v, 0x140, 0xF, 0xF, true); }
+__device__ __forceinline__ float fdpp_x1(float v) { return __int_as_float(dpp_x1(__float_as_int(v))); }
+__device__ __forceinline__ float fdpp_x2(float v) { return __int_as_float(dpp_x2(__float_as_int(v))); }
+__device__ __forceinline__ float fdpp_half_mirror(float v) { return __int_as_float(dpp_half_mirror(__float_as_int(v))); }
+__device__ __forceinline__ float fdpp_mirror(float v) { return __int_as_float(dpp_mirror(__float_as_int(v))); }
+// max / sum over the 16 lanes of a row (lanes 16G .. 16G + 15): the quad (partners ^1, ^2), then
+// the other quad of the half (mirror within 8), then the other half (mirror within 16).  Every
+// step combines two equal-shaped partial results, so all 16 lanes end with identical values.
+__device__ __forceinline__ float row_max(float v) {
+    v = fmaxf(v, fdpp_x1(v));
+    v = fmaxf(v, fdpp_x2(v));
+    v = fmaxf(v, fdpp_half_mirror(v));
+    return fmaxf(v, fdpp_mirror(v));
 }
-__device__ __forceinline__ float head_sum(float v) {
-    v += quad_x1f(v);
-    v += quad_x2f(v);
-    return xor_sum(xor_sum(v, 16), 32);
+__device__ __forceinline__ float row_sum(float v) {
+    v += fdpp_x1(v);
+    v += fdpp_x2(v);
+    v += fdpp_half_mirror(v);
+    return v + fdpp_mirror(v);
 }
 
-// c: digit-j partial sums of rows 0..3 (this lane's slot j); returns sum_j 256^j c_j[row j]
-// for row j of this lane.
-__device__ __forceinline__ int quad_combine(v4i c, int j) {
-    const uint32_t sh = 8u * (uint32_t)j;
-    const int r0 = (int)((uint32_t)c[0] << sh), r1 = (int)((uint32_t)c[1] << sh);
-    const int r2 = (int)((uint32_t)c[2] << sh), r3 = (int)((uint32_t)c[3] << sh);
-    const bool hi = (j & 2) != 0, lo = (j & 1) != 0;
-    const int k0 = hi ? r2 : r0, k1 = hi ? r3 : r1, s0 = hi ? r0 : r2, s1 = hi ? r1 : r3;
-    const int a0 = k0 + quad_x2(s0), a1 = k1 + quad_x2(s1);  // rows {2hi, 2hi+1}, digits j, j^2
-    const int k = lo ? a1 : a0, s = lo ? a0 : a1;
-    return k + quad_x1(s);                                   // row j, all four digits
+// The digit-weighted sum of one output lane: register i holds the partial sum of digit i.  The
+// true sum fits int32, so the wrapping arithmetic below is exact.
+__device__ __forceinline__ int digit_sum(v4i c) {
+    return (int)(((uint32_t)c[2] << 16) + ((uint32_t)c[1] << 8) + (uint32_t)c[0]);
 }
 
 // Lane j of a quad holds y (row j of a 4 x 4 byte matrix); returns column j: byte i of the
@@ -548,13 +555,13 @@ __device__ __forceinline__ int quad_combine(v4i c, int j) {
 __device__ __forceinline__ uint32_t quad_transpose_bytes(uint32_t y, int j) {
     const uint32_t selA = j < 2 ? 0x05040100u : 0x03020706u;
     const uint32_t selB = (j & 1) ? 0x03070105u : 0x06020400u;
-    const uint32_t t = perm((uint32_t)quad_x2((int)y), y, selA);
-    return perm((uint32_t)quad_x1((int)t), t, selB);
+    const uint32_t t = perm((uint32_t)dpp_x2((int)y), y, selA);
+    return perm((uint32_t)dpp_x1((int)t), t, selB);
 }
 
 struct Smem4 {
-    float q[4][kD];        // rotated q; reused for the inverse rotation of the output
-    float aux[6][kD];      // a_K b_K s2_K a_V b_V s2_V of the current tile (b_V becomes b_V / a_V)
+    float q[4][kD];        // rotated q (rows >= g zero); reused for the inverse rotation of the output
+    float aux[6][kD];      // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
     uint4 qp[4][2][4][4];  // q~ digit planes [digit slot][kappa][G][head]; slot 3 stays zero
     float hv[4][4];        // per head: beta, q~ step, alpha, l
     float p[4][kG];        // probabilities of a bf16 chunk (sink / residual)
@@ -567,9 +574,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
     constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // fixed-point bound of q~ and p~
     constexpr float MAGIC = 12582912.f;                  // 1.5 * 2^23: x + MAGIC rounds x to an integer
     constexpr uint32_t MAGIC_BITS = 0x4B400000u;
-    const int l = threadIdx.x, G = l >> 4, n = l & 15, h = n >> 2, j = n & 3;
+    // output role: head G, column n; A-operand role: row 4*h + j (digit j of head h)
+    const int l = threadIdx.x, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
     const int g = a.g;
-    const bool head_ok = h < g;
+    const bool head_ok = G < g;
     const int split = blockIdx.x % a.n_split;
     const int stream = blockIdx.x / a.n_split;
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
@@ -583,8 +591,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
     const size_t tb = tile_bytes(BITS), cb = code_bytes(BITS);
 
-    float m_run = -INFINITY, l_run = 0.f;  // head h; l_run is this lane's partial sum
-    float orot[8];                         // head h, channel 16*mt + 4*G + j (rotated domain)
+    float m_run = -INFINITY, l_run = 0.f;  // head G; l_run is this lane's partial sum
+    float orot[8];                         // head G, channel 16*mt + n (rotated domain)
     float oplain[4][2];                    // head hh, channel 2*l + jj (unrotated)
 #pragma unroll
     for (int mt = 0; mt < 8; ++mt) orot[mt] = 0.f;
@@ -599,7 +607,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
         float mx = lg[0];
 #pragma unroll
         for (int k = 1; k < 8; ++k) mx = fmaxf(mx, lg[k]);
-        mx = head_max(mx);
+        mx = row_max(mx);
         const float m_new = fmaxf(m_run, mx);
         const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
         float s = 0.f;
@@ -616,14 +624,18 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
     };
 
     if (blk0 < blk1) {
-        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] = load_q(qrow * kD + idx);
+        for (int idx = l; idx < 4 * kD; idx += 64)
+            sm.q[idx >> 7][idx & 127] = idx < g * kD ? load_q(qrow * kD + idx) : 0.f;
         if (l < 32) sm.qp[3][l >> 4][(l >> 2) & 3][l & 3] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
         lds_hadamard<4>(sm.q, g);
-        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
+        // q~ role: head G, channels 8n .. 8n + 7 (rotated, normalized)
+        float qr[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) qr[k] = sm.q[G][8 * n + k] * kInvSqrt128;
+        // source lane of the PV operand permutation (see above), as a byte address
+        const int perm_addr = (16 * h + 4 * G + j) * 4;
 
-        // Tiles are double-buffered in registers: while one buffer is consumed, the next
-        // tile's loads are in flight into the other (the loop is unrolled by two).
         // One register buffer per tile part, refilled as soon as its current contents are
         // consumed: the next tile's aux right after it is staged in LDS, its key codes right
         // after the QK products, its value codes right after the PV products.
@@ -650,7 +662,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
 
         for (int blk = blk0; blk < blk1; ++blk) {
             const bool more = blk + 1 < blk1;
-            __syncthreads();  // the previous tile is done with sm.aux / sm.qp
+            __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
             reinterpret_cast<uint4*>(&sm.aux[0][0])[l] = ax0;
             reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 64] = ax1;
             reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 128] = ax2;
@@ -672,60 +684,56 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                     vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
                     vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
                 }
-            // q~ digit planes, spread over all lanes: group (head, kappa, G', s) = 4 channels
-            for (int gi0 = 0; gi0 < g * 32; gi0 += 64) {
-                const int gi = gi0 + l;
-                const bool valid = gi < g * 32;
-                const int hh = min(gi >> 5, g - 1), rem = gi & 31;
-                const int kap = rem >> 4, Gp = (rem >> 2) & 3, s = rem & 3;
-                const int c0 = 64 * kap + 16 * Gp + 4 * s;
-                const float4 q4 = *reinterpret_cast<const float4*>(&sm.q[hh][c0]);
-                const float4 a4 = *reinterpret_cast<const float4*>(&sm.aux[0][c0]);
-                const float4 r4 = *reinterpret_cast<const float4*>(&sm.aux[1][c0]);
-                const float qv[4] = {q4.x, q4.y, q4.z, q4.w}, av[4] = {a4.x, a4.y, a4.z, a4.w};
-                const float rk[4] = {r4.x, r4.y, r4.z, r4.w};
-                float qt[4], mx = 0.f;
+            // q~ = q_rot * a_K as fixed point on a per-head grid, then three digit planes; beta
+            // in grid units from the same rounded integers times b_K / a_K
+            {
+                const float4 a0 = *reinterpret_cast<const float4*>(&sm.aux[0][8 * n]);
+                const float4 a1 = *reinterpret_cast<const float4*>(&sm.aux[0][8 * n + 4]);
+                const float4 r0 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n]);
+                const float4 r1 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n + 4]);
+                const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+                const float rk[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+                float qt[8], mx = 0.f;
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    qt[k] = valid ? qv[k] * av[k] : 0.f;
+                for (int k = 0; k < 8; ++k) {
+                    qt[k] = qr[k] * av[k];
                     mx = fmaxf(mx, fabsf(qt[k]));
                 }
-#pragma unroll
-                for (int m = 1; m < 32; m <<= 1) mx = xor_max(mx, m);
+                mx = row_max(mx);
                 const float sc = mx > 0.f ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
-                float bs = 0.f;  // beta in q~ grid units: rounded q~ times b_K / a_K
-                uint32_t y[4];
+                float bs = 0.f;
+                uint32_t y[8];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
+                for (int k = 0; k < 8; ++k) {
                     const float yf = fmaf(qt[k], sc, MAGIC);
                     bs = fmaf(yf - MAGIC, rk[k], bs);
                     y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
                 }
-#pragma unroll
-                for (int m = 1; m < 32; m <<= 1) bs = xor_sum(bs, m);
-                uint32_t d0, d1, d2;
+                bs = row_sum(bs);
+                uint32_t d0, d1, d2, e0, e1, e2;
                 digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
-                if (valid) {
-                    reinterpret_cast<uint32_t*>(&sm.qp[0][kap][Gp][hh])[s] = d0;
-                    reinterpret_cast<uint32_t*>(&sm.qp[1][kap][Gp][hh])[s] = d1;
-                    reinterpret_cast<uint32_t*>(&sm.qp[2][kap][Gp][hh])[s] = d2;
-                    if ((l & 31) == 0) {
-                        sm.hv[hh][0] = bs;
-                        sm.hv[hh][1] = mx * (1.0f / (float)QMAX);
-                    }
+                digits4(y[4], y[5], y[6], y[7], e0, e1, e2);
+                // channels 8n .. 8n + 7 = kappa n / 8, group (n % 8) / 2, components 2 (n % 2) + {0, 1}
+                const int kap = n >> 3, Gq = (n >> 1) & 3, half = n & 1;
+                reinterpret_cast<uint2*>(&sm.qp[0][kap][Gq][G])[half] = make_uint2(d0, e0);
+                reinterpret_cast<uint2*>(&sm.qp[1][kap][Gq][G])[half] = make_uint2(d1, e1);
+                reinterpret_cast<uint2*>(&sm.qp[2][kap][Gq][G])[half] = make_uint2(d2, e2);
+                if (n == 0) {
+                    sm.hv[G][0] = bs;
+                    sm.hv[G][1] = mx * (1.0f / (float)QMAX);
                 }
             }
             __syncthreads();
-            v4i bq[2];
+            v4i aq[2];
 #pragma unroll
             for (int kap = 0; kap < 2; ++kap) {
                 const uint4 u = sm.qp[j][kap][G][h];
-                bq[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+                aq[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
             }
-            const float beta = head_ok ? sm.hv[h][0] : 0.f;                  // q~ grid units
-            const float fqs = head_ok ? sm.hv[h][1] * a.scale_log2 : 0.f;  // grid step * scale
+            const float beta = sm.hv[G][0];                  // q~ grid units
+            const float fqs = sm.hv[G][1] * a.scale_log2;   // grid step * scale
 
-            // logits of token 64*sg + 16*tau + 4*G + j
+            // logits of head G, token 64*sg + 16*tau + n
             float lg[8];
 #pragma unroll
             for (int sg = 0; sg < 2; ++sg)
@@ -733,41 +741,42 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                 for (int tau = 0; tau < 4; ++tau) {
                     v4i c = {0, 0, 0, 0};
 #pragma unroll
-                    for (int kap = 0; kap < 2; ++kap) c = mfma_i8(unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]), bq[kap], c);
-                    const int v = quad_combine(c, j);
-                    lg[4 * sg + tau] = ((float)v + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + 4 * G + j]);
+                    for (int kap = 0; kap < 2; ++kap) c = mfma_i8(aq[kap], unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]), c);
+                    lg[4 * sg + tau] = ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
                 }
             if (more) load_codes(tile_k(blk + 1), kc);
             const float alpha = softmax_update(lg, false);
 
-            // p~ = p * a_V as digit planes; gamma from the same rounded integers
+            // p~ = p * a_V as fixed point on a per-head grid; gamma from the same rounded integers
             float pmx = 0.f;
 #pragma unroll
             for (int k = 0; k < 8; ++k) {
-                lg[k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + 4 * G + j];
+                lg[k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + n];
                 pmx = fmaxf(pmx, lg[k]);
             }
-            pmx = head_max(pmx);
+            pmx = row_max(pmx);
             const float psc = pmx > 0.f ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
             float gam = 0.f;
-            v4i bp[2];
+            v4i ap[2];
 #pragma unroll
             for (int sg = 0; sg < 2; ++sg) {
                 uint32_t D[4];
 #pragma unroll
                 for (int tau = 0; tau < 4; ++tau) {
                     const float yf = fmaf(lg[4 * sg + tau], psc, MAGIC);
-                    gam = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + 4 * G + j], gam);
+                    gam = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam);
                     // bytes of y: the three digits plus 128 each, and 0x80 on top (digit slot 3
-                    // becomes zero); lane j takes digit j of the quad's four rows
+                    // becomes zero); after the transpose lane (head, 4m + i) holds digit i of
+                    // tokens 16 tau + 4m + {0..3}, which lane (m, 4 head + i) takes as A operand
                     const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
-                    D[tau] = quad_transpose_bytes(y, j) ^ 0x80808080u;
+                    const uint32_t t = quad_transpose_bytes(y, j);
+                    D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t) ^ 0x80808080u;
                 }
-                bp[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
+                ap[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
             }
-            gam = head_sum(gam);
+            gam = row_sum(gam);
 
-            // PV: channel 16*mt + 4*G + j
+            // PV: head G, channel 16*mt + n
             v4i acc[8];
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) acc[mt] = v4i{0, 0, 0, 0};
@@ -775,33 +784,29 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
             for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
                 for (int mt = 0; mt < 8; ++mt)
-                    acc[mt] = mfma_i8(unit_i8<BITS>(&vw[sg][mt * WPU]), bp[sg], acc[mt]);
+                    acc[mt] = mfma_i8(ap[sg], unit_i8<BITS>(&vw[sg][mt * WPU]), acc[mt]);
             if (more) load_codes(tile_v(blk + 1), vc);
             const float fp = pmx * (1.0f / (float)QMAX);
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                const int v = quad_combine(acc[mt], j);
-                orot[mt] = fmaf((float)v + gam, fp * sm.aux[5][16 * mt + 4 * G + j], orot[mt] * alpha);
-            }
+            for (int mt = 0; mt < 8; ++mt)
+                orot[mt] = fmaf((float)digit_sum(acc[mt]) + gam, fp * sm.aux[5][16 * mt + n], orot[mt] * alpha);
         }
     }
 
     // ---- sink and residual (bf16, unrotated): last split only ------------------------------
     if (last && ns + nr > 0) {
-        // q of head h as the bf16 B operand in every column of the head's quad (hi, plus lo
-        // when q is fp32); lane (G, 4h + j) holds q[h][32k + 8G ..]
-        v8bf qh[4], ql[4];
+        // A operand: row 4h holds q of head h rounded to bf16, row 4h + 1 the remainder (zero
+        // for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds q[h][32k + 8G ..]
+        v8bf aq[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                const float v = head_ok ? load_q((qrow + h) * kD + 32 * k + 8 * G + e) : 0.f;
+                const float v = (h < g && j < 2) ? load_q((qrow + h) * kD + 32 * k + 8 * G + e) : 0.f;
                 const __bf16 hi = (__bf16)v;
-                qh[k][e] = hi;
-                ql[k][e] = (__bf16)(v - (float)hi);
+                aq[k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
             }
         }
-        const bool two = !a.q_bf16;
         const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
         for (int chunk = 0; chunk <= nsc; ++chunk) {
             const bool in_sink = chunk < nsc;
@@ -812,23 +817,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                                          : a.k_resid + (size_t)stream * kG * kD;
             const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
                                          : a.v_resid + (size_t)stream * kG * kD;
+            // logits of head G, token 16*tau + n
             float lg[8];
 #pragma unroll
             for (int tau = 0; tau < 8; ++tau) {
                 v4f acc = {0.f, 0.f, 0.f, 0.f};
-                const int arow = 16 * tau + (l & 15);
+                const int trow = 16 * tau + n;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     uint4 u = {0u, 0u, 0u, 0u};
-                    if (arow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)arow * kD + 32 * k + 8 * G);
-                    v8bf A;
-                    __builtin_memcpy(&A, &u, 16);
-                    acc = mfma_bf16(A, qh[k], acc);
-                    if (two) acc = mfma_bf16(A, ql[k], acc);
+                    if (trow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)trow * kD + 32 * k + 8 * G);
+                    v8bf B;
+                    __builtin_memcpy(&B, &u, 16);
+                    acc = mfma_bf16(aq[k], B, acc);
                 }
-                // all four columns of the quad hold the same logits; lane j keeps row j
-                const float v = j == 0 ? acc[0] : (j == 1 ? acc[1] : (j == 2 ? acc[2] : acc[3]));
-                lg[tau] = 16 * tau + 4 * G + j < cn ? v * a.scale_log2 : -INFINITY;
+                lg[tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
             }
             const float alpha = softmax_update(lg, true);
 #pragma unroll
@@ -836,8 +839,8 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
             __syncthreads();  // the previous chunk is done with sm.p / sm.hv
             if (head_ok) {
 #pragma unroll
-                for (int tau = 0; tau < 8; ++tau) sm.p[h][16 * tau + 4 * G + j] = lg[tau];
-                if (G == 0 && j == 0) sm.hv[h][2] = alpha;
+                for (int tau = 0; tau < 8; ++tau) sm.p[G][16 * tau + n] = lg[tau];
+                if (n == 0) sm.hv[G][2] = alpha;
             }
             __syncthreads();
 #pragma unroll
@@ -864,13 +867,13 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
     }
 
     // ---- finish ------------------------------------------------------------------------------
-    const float lt = head_sum(l_run);
+    const float lt = row_sum(l_run);
     if (a.n_split == 1) {
         __syncthreads();
         if (head_ok) {
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) sm.q[h][16 * mt + 4 * G + j] = orot[mt];
-            if (G == 0 && j == 0) sm.hv[h][3] = lt;
+            for (int mt = 0; mt < 8; ++mt) sm.q[G][16 * mt + n] = orot[mt];
+            if (n == 0) sm.hv[G][3] = lt;
         }
         __syncthreads();
         lds_hadamard<4>(sm.q, g);
@@ -892,10 +895,10 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
         }
     } else {
         if (head_ok) {
-            float* P = a.ws + ((qrow + h) * a.n_split + split) * kPart;
+            float* P = a.ws + ((qrow + G) * a.n_split + split) * kPart;
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) P[4 + 16 * mt + 4 * G + j] = orot[mt];
-            if (G == 0 && j == 0) {
+            for (int mt = 0; mt < 8; ++mt) P[4 + 16 * mt + n] = orot[mt];
+            if (n == 0) {
                 P[0] = m_run;
                 P[1] = lt;
             }

@@ -31,10 +31,10 @@ def _dtype(spec) -> torch.dtype:
 
 def build(name: str, device="cuda", bits: int | None = None, n_sink: int = 0, context: int | None = None,
           layers: int | None = None, batch: int | None = None, extra_blocks: int = 0, seed: int | None = None,
-          keep_inputs: bool = False, best_iter: bool = False):
+          keep_inputs: bool = False, best_iter: bool = False, n_q: int | None = None, n_kv: int | None = None):
     """Create and fill the cache of workload `name` (see datagen.WORKLOADS).
 
-    Overrides (bits, context, layers, batch, n_sink) make smaller variants of the same shape.
+    Overrides (bits, context, layers, batch, n_sink, n_q, n_kv) make variants of the same shape.
     Returns (Built, inputs) where inputs holds the K/V/best-iteration tensors if keep_inputs.
     """
     spec = dict(datagen.WORKLOADS[name])
@@ -46,6 +46,10 @@ def build(name: str, device="cuda", bits: int | None = None, n_sink: int = 0, co
         spec["layers"] = layers
     if batch is not None:
         spec["batch"] = batch
+    if n_q is not None:
+        spec["n_q"] = n_q
+    if n_kv is not None:
+        spec["n_kv"] = n_kv
     seed = datagen.SEEDS[name] if seed is None else seed
     dt = _dtype(spec)
     p = K.kvarn_params_init(spec["bits"])

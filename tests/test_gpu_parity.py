@@ -160,6 +160,17 @@ def test_decode_variants(K, bits, n_sink, name):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
+@pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (12, 2), (32, 2)])
+def test_decode_group_sizes(K, n_q, n_kv):
+    """Every query-group size class (1 .. 4 share one kernel, 5 .. 8 and 9 .. 16 the others),
+    with a residual and several body tiles."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", context=3 * 128 + 45, batch=2, n_q=n_q, n_kv=n_kv)
+    q = workloads.decode_queries(built, seed=6)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
 def test_decode_length_above_hint(K):
     """A max_len_hint below the true length still attends every token (last split extends)."""
     from paper_2606_03458_amd import workloads
