@@ -111,6 +111,8 @@ def main():
             alg_bytes.append(decode_bytes(length))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    if not bool(torch.isfinite(out).all()):
+        raise RuntimeError("decode output has non-finite values")
     dec_ms = [a.elapsed_time(b) for a, b in ev]
     dec_avg_s = sum(dec_ms) / len(dec_ms) / 1e3
     bytes_avg = sum(alg_bytes) / len(alg_bytes)
@@ -160,7 +162,7 @@ def main():
                                f"append + decode per step",
                    "layers": spec["layers"], "batch": spec["batch"], "context": spec["context"], "bits": p.bits},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                     "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(name),
                      "kernel": "kvarn_decode_attention", "alg_bytes_per_launch": int(bytes_avg),
                      "avg_launch_ms": round(dec_avg_s * 1e3, 4)},
         "cpu_baseline": cpu,
@@ -176,6 +178,42 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         print(f"[bench] calibration copy: {nbytes} bytes read + {nbytes} bytes written", file=sys.stderr, flush=True)
+
+
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "k_decode4_throughput_hbm_counters.md")
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2606_03458_amd", "csrc", f) for f in ("decode.hip", "common.hpp")]
+
+
+def decode_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in DECODE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per decode launch (FETCH_SIZE + WRITE_SIZE, calibrated) from the committed
+    rocprofv3 counter summary; None unless it covers this workload and was taken on the
+    current decode sources."""
+    try:
+        with open(COUNTER_SUMMARY) as fh:
+            text = fh.read()
+    except OSError:
+        return None
+    fields = {}
+    for line in text.splitlines():
+        line = line.strip().strip("`")
+        if ":" in line and line.split(":", 1)[0] in ("workload", "source_sha256", "hbm_bytes_per_launch"):
+            k, v = line.split(":", 1)
+            fields[k] = v.strip()
+    if fields.get("workload") != workload or fields.get("source_sha256") != decode_source_hash():
+        return None
+    try:
+        return int(fields["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(built, q, length, scale, target_s):

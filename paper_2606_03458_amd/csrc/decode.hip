@@ -38,6 +38,13 @@ typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 
 constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
 
+// A fixed-point grid is only formed for a maximum above this; below it the values are taken
+// as zero.  For p~ this drops a tile whose probabilities are all below 1e-30 relative to the
+// running maximum (whose own probability, 1, is already in l): far below fp32 resolution of
+// the sums.  It keeps grid scale = bound / max finite (a denormal or tiny max would make it
+// inf, and 0 * inf a NaN).
+constexpr float kTinyMax = 1e-30f;
+
 struct DecodeArgs {
     const uint8_t* k_body;
     const uint8_t* v_body;
@@ -247,7 +254,7 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                 }
 #pragma unroll
                 for (int m = 1; m < 32; m <<= 1) mx = xor_max(mx, m);
-                const float sc = mx > 0.f ? (float)QMAX / mx : 0.f;
+                const float sc = mx > kTinyMax ? (float)QMAX / mx : 0.f;
                 // beta in q~ grid units: sum over channels of the rounded q~ times b_K / a_K
                 float bs = 0.f;
                 uint32_t y[4];
@@ -322,7 +329,7 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                     pmx = fmaxf(pmx, fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])));
                 }
             pmx = xor_max(xor_max(pmx, 16), 32);
-            const float psc = pmx > 0.f ? PMAX / pmx : 0.f;
+            const float psc = pmx > kTinyMax ? PMAX / pmx : 0.f;
             float gam = 0.f;  // gamma in p~ grid units: sum of rounded p~ times b_V / a_V
             v4i bp[2][2];
 #pragma unroll
@@ -700,7 +707,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                     mx = fmaxf(mx, fabsf(qt[k]));
                 }
                 mx = row_max(mx);
-                const float sc = mx > 0.f ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
+                const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
                 float bs = 0.f;
                 uint32_t y[8];
 #pragma unroll
@@ -755,7 +762,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                 pmx = fmaxf(pmx, lg[k]);
             }
             pmx = row_max(pmx);
-            const float psc = pmx > 0.f ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
+            const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
             float gam = 0.f;
             v4i ap[2];
 #pragma unroll

@@ -1,0 +1,100 @@
+"""Parity at the full sizes of the benchmark workloads.
+
+The whole cache is built, extended through the append path (one flush included) and decoded
+on the GPU in the launch configuration the benchmark times.  The oracle then recomputes a
+seeded sample of (sequence, kv head) streams one by one, and re-quantizes a sample of body
+tiles from inputs regenerated with the same seeds.  Tolerances are those of gpu_util."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from gpu_util import check_output, compare_tiles, host_streams, q_to_host, tiles_to_host
+
+pytestmark = pytest.mark.gpu
+
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+@pytest.fixture(scope="module")
+def K():
+    from paper_2606_03458_amd import kvarn
+    kvarn.lib()
+    torch.cuda.set_device(0)
+    return kvarn
+
+
+def _run(K, name, n_append, n_streams, n_tiles, out_dtype):
+    from paper_2606_03458_amd import datagen, workloads
+    spec = datagen.WORKLOADS[name]
+    seed = datagen.SEEDS[name]
+    built, inputs = workloads.build(name, extra_blocks=(n_append + 127) // 128 + 1, best_iter=True)
+    p, cache = built.params, built.cache
+    T0 = built.length
+    appended = []
+    for s in range(n_append):
+        kt, vt = workloads.step_tokens(built, seed, s)
+        assert K.kvarn_append_token(p, cache, kt, vt, K.KVARN_BF16, built.length) is None
+        built.length += 1
+        if s < 128:
+            appended.append((kt, vt))
+    assert int(cache.err_word.item()) == 0
+    q = workloads.decode_queries(built, seed, 0)
+    max_len = built.length + 1
+    ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, built.n_q, max_len)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    out = torch.empty(q.shape, dtype=out_dtype, device="cuda")
+    K.kvarn_decode_attention(p, cache, built.n_q, q, K.KVARN_BF16, out,
+                             K.KVARN_BF16 if out_dtype == torch.bfloat16 else K.KVARN_F32, SCALE, max_len, ws,
+                             ws_bytes)
+    torch.cuda.synchronize()
+
+    # decode: sampled streams, the first and the last included
+    rng = np.random.default_rng(seed)
+    n_kv, g = cache.n_kv, built.n_q // cache.n_kv
+    total = cache.batch * n_kv
+    pick = np.unique(np.concatenate([[0, total - 1], rng.choice(total, n_streams, replace=False)]))
+    streams = [divmod(int(s), n_kv) for s in pick]
+    hc = host_streams(cache, streams)
+    qh = q_to_host(q)
+    qs = np.stack([qh[b, kh * g:(kh + 1) * g] for b, kh in streams])
+    ref = oracle.decode(hc, qs.reshape(len(streams), g, 128), SCALE)
+    got = np.stack([out[b, kh * g:(kh + 1) * g].float().cpu().numpy() for b, kh in streams])
+    worst = check_output(got, ref, bf16_out=out_dtype == torch.bfloat16)
+
+    # quantize: body tiles of two layers from regenerated inputs, and the flushed tile
+    L, B = spec["layers"], spec["batch"]
+    nb = T0 // 128
+    stats = []
+    for layer in sorted({0, L - 1}):
+        lseed = seed * 1000 + layer
+        sig = datagen.channel_log_scales(lseed, n_kv, spec["dist"], device="cuda")
+        Kx, Vx = datagen.kv_tokens(lseed, 0, B, n_kv, T0, spec["dist"], dtype=torch.bfloat16, device="cuda",
+                                   sigma_c=sig)
+        sel = [(int(rng.integers(B)), int(rng.integers(n_kv)), int(rng.integers(nb))) for _ in range(n_tiles)]
+        for kind, X, body, best in ((K.KVARN_KEYS, Kx, cache.k_body, inputs["best_k"][layer]),
+                                    (K.KVARN_VALUES, Vx, cache.v_body, inputs["best_v"][layer])):
+            xs = torch.stack([X[b, kh, t * 128:(t + 1) * 128] for b, kh, t in sel])
+            tiles = torch.stack([body[layer * B + b, kh, t] for b, kh, t in sel]).cpu().numpy()
+            bi = np.array([int(best[(b * n_kv + kh) * nb + t]) for b, kh, t in sel])
+            stats.append(compare_tiles(tiles, tiles_to_host(xs), kind, p.bits, gpu_best=bi))
+        del Kx, Vx
+    if n_append >= 128:
+        kst = torch.stack([k for k, _ in appended])  # [128, L*B, n_kv, 128]
+        vst = torch.stack([v for _, v in appended])
+        for kind, X, body in ((K.KVARN_KEYS, kst, cache.k_body), (K.KVARN_VALUES, vst, cache.v_body)):
+            xs = torch.stack([X[:, b, kh] for b, kh in streams[:n_tiles]])
+            tiles = torch.stack([body[b, kh, nb] for b, kh in streams[:n_tiles]]).cpu().numpy()
+            stats.append(compare_tiles(tiles, tiles_to_host(xs), kind, p.bits))
+    return worst, stats
+
+
+def test_full_size_throughput(K):
+    """32 layers x batch 32 (1024 sequences), 32 q / 8 kv heads, 32768-token 2-bit cache plus
+    132 appended tokens (one flush), bf16 q and output, a single split per stream."""
+    _run(K, "throughput", n_append=132, n_streams=40, n_tiles=12, out_dtype=torch.bfloat16)
+
+
+def test_full_size_stress(K):
+    """Heavy-tailed keys, 40 q / 8 kv heads (GQA 5), batch 128, 16384-token 2-bit cache."""
+    _run(K, "stress", n_append=130, n_streams=40, n_tiles=12, out_dtype=torch.float32)

@@ -171,6 +171,26 @@ def test_decode_group_sizes(K, n_q, n_kv):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
+@pytest.mark.parametrize("mult", [4.0, 16.0])
+def test_decode_peaked_softmax(K, mult):
+    """Logits scaled up so that most tiles' probabilities sit near or below fp32 underflow
+    relative to the running maximum: the output stays finite and matches the oracle."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", context=64 * 128 + 3, batch=2)
+    q = workloads.decode_queries(built, seed=7)
+    p, cache = built.params, built.cache
+    out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    max_len = built.length + 1
+    ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, built.n_q, max_len)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    K.kvarn_decode_attention(p, cache, built.n_q, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE * mult, max_len, ws,
+                             ws_bytes)
+    torch.cuda.synchronize()
+    assert bool(torch.isfinite(out).all())
+    ref = oracle.decode(host_cache(cache), q_to_host(q), SCALE * mult)
+    check_output(out.cpu().numpy(), ref, bf16_out=False)
+
+
 def test_decode_length_above_hint(K):
     """A max_len_hint below the true length still attends every token (last split extends)."""
     from paper_2606_03458_amd import workloads
