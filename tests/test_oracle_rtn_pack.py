@@ -47,14 +47,20 @@ def test_tile_bytes_and_bits_per_element(orc):
 #   keys:   unit = (sigma*64 + 16*((c%64)//16) + t%16)*8 + 2*((t%64)//16) + c//64, e = c%16
 #   values: unit = (sigma*64 + 16*((t%16)//4) + c%16)*8 + c//16,  e = 4*((t%64)//16) + t%4
 #   code e = 4s + q sits in word unit at bit 8q + 2s.
-HAND_2BIT = {
-    0: [((0, 0), 0, 0), ((0, 1), 0, 8), ((0, 4), 0, 2), ((0, 15), 0, 30), ((1, 0), 8, 0),
-        ((16, 0), 2, 0), ((0, 64), 1, 0), ((0, 16), 128, 0), ((64, 0), 512, 0),
-        ((127, 127), (64 + 48 + 15) * 8 + 6 + 1, 30)],
-    1: [((0, 0), 0, 0), ((1, 0), 0, 8), ((3, 0), 0, 24), ((4, 0), 128, 0), ((16, 0), 0, 2),
-        ((48, 0), 0, 6), ((0, 1), 8, 0), ((0, 16), 1, 0), ((64, 0), 512, 0),
-        ((127, 127), (64 + 48 + 15) * 8 + 7, 30)],
-}
+def _hand_positions():
+    """Hand-derived 2-bit positions, tests/golden/format_2bit_positions.txt."""
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "format_2bit_positions.txt")
+    table = {0: [], 1: []}
+    with open(path) as fh:
+        for line in fh:
+            if line.strip() and not line.startswith("#"):
+                k, t, c, w, bit = (int(v) for v in line.split())
+                table[k].append(((t, c), w, bit))
+    return table
+
+
+HAND_2BIT = _hand_positions()
 
 
 @pytest.mark.parametrize("kind", [0, 1])
