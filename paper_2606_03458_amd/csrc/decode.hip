@@ -566,25 +566,29 @@ __device__ __forceinline__ uint32_t quad_transpose_bytes(uint32_t y, int j) {
     return perm((uint32_t)dpp_x1((int)t), t, selB);
 }
 
+// Query heads are taken in groups of four (NH groups, g <= 4 * NH): every group repeats the
+// per-head work on the same code operands, which are extracted once per tile.
+template <int NH>
 struct Smem4 {
-    float q[4][kD];        // rotated q (rows >= g zero); reused for the inverse rotation of the output
-    float aux[6][kD];      // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
-    uint4 qp[4][2][4][4];  // q~ digit planes [digit slot][kappa][G][head]; slot 3 stays zero
-    float hv[4][4];        // per head: beta, q~ step, alpha, l
-    float p[4][kG];        // probabilities of a bf16 chunk (sink / residual)
+    float q[4 * NH][kD];       // rotated q (rows >= g zero); reused for the inverse rotation of the output
+    float aux[6][kD];          // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
+    uint4 qp[NH][4][2][4][4];  // q~ digit planes [group][digit slot][kappa][G][head]; slot 3 stays zero
+    float hv[4 * NH][4];       // per head: beta, q~ step, alpha, l
+    float p[4 * NH][kG];       // probabilities of a bf16 chunk (sink / residual)
 };
 
-template <int BITS>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 3 : 2, 8))) void k_decode4(DecodeArgs a) {
-    __shared__ Smem4 sm;
+template <int BITS, int NH>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 ? 3 : 2, 8)))
+void k_decode4(DecodeArgs a) {
+    __shared__ Smem4<NH> sm;
     constexpr int WPU = BITS / 2;
+    constexpr int NHD = 4 * NH;                          // head slots
     constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // fixed-point bound of q~ and p~
     constexpr float MAGIC = 12582912.f;                  // 1.5 * 2^23: x + MAGIC rounds x to an integer
     constexpr uint32_t MAGIC_BITS = 0x4B400000u;
-    // output role: head G, column n; A-operand role: row 4*h + j (digit j of head h)
+    // output role: head 4*hg + G, column n; A-operand role: row 4*h + j (digit j of head 4*hg + h)
     const int l = threadIdx.x, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
     const int g = a.g;
-    const bool head_ok = G < g;
     const int split = blockIdx.x % a.n_split;
     const int stream = blockIdx.x / a.n_split;
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
@@ -598,25 +602,28 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
     const size_t tb = tile_bytes(BITS), cb = code_bytes(BITS);
 
-    float m_run = -INFINITY, l_run = 0.f;  // head G; l_run is this lane's partial sum
-    float orot[8];                         // head G, channel 16*mt + n (rotated domain)
-    float oplain[4][2];                    // head hh, channel 2*l + jj (unrotated)
+    float m_run[NH], l_run[NH];  // head 4*hg + G; l_run is this lane's partial sum
+    float orot[NH][8];           // head 4*hg + G, channel 16*mt + n (rotated domain)
 #pragma unroll
-    for (int mt = 0; mt < 8; ++mt) orot[mt] = 0.f;
+    for (int hg = 0; hg < NH; ++hg) {
+        m_run[hg] = -INFINITY;
+        l_run[hg] = 0.f;
 #pragma unroll
-    for (int hh = 0; hh < 4; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
+        for (int mt = 0; mt < 8; ++mt) orot[hg][mt] = 0.f;
+    }
 
     auto load_q = [&](size_t idx) -> float {
         return a.q_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.q)[idx]) : static_cast<const float*>(a.q)[idx];
     };
-    // online softmax over this lane's 8 logits (log2 units; -inf = absent) -> p, returns alpha
-    auto softmax_update = [&](float (&lg)[8], bool maybe_absent) -> float {
+    // online softmax of group hg over this lane's 8 logits (log2 units; -inf = absent) -> p,
+    // returns alpha
+    auto softmax_update = [](float (&lg)[8], bool maybe_absent, float& m, float& lsum) -> float {
         float mx = lg[0];
 #pragma unroll
         for (int k = 1; k < 8; ++k) mx = fmaxf(mx, lg[k]);
         mx = row_max(mx);
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+        const float m_new = fmaxf(m, mx);
+        const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
         float s = 0.f;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
@@ -625,21 +632,24 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
             lg[k] = p;
             s += p;
         }
-        l_run = l_run * alpha + s;
-        m_run = m_new;
+        lsum = lsum * alpha + s;
+        m = m_new;
         return alpha;
     };
 
     if (blk0 < blk1) {
-        for (int idx = l; idx < 4 * kD; idx += 64)
+        for (int idx = l; idx < NHD * kD; idx += 64)
             sm.q[idx >> 7][idx & 127] = idx < g * kD ? load_q(qrow * kD + idx) : 0.f;
-        if (l < 32) sm.qp[3][l >> 4][(l >> 2) & 3][l & 3] = make_uint4(0u, 0u, 0u, 0u);
+        for (int idx = l; idx < NH * 32; idx += 64)
+            sm.qp[idx >> 5][3][(idx >> 4) & 1][(idx >> 2) & 3][idx & 3] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
-        lds_hadamard<4>(sm.q, g);
-        // q~ role: head G, channels 8n .. 8n + 7 (rotated, normalized)
-        float qr[8];
+        lds_hadamard<NHD>(sm.q, g);
+        // q~ role: head 4*hg + G, channels 8n .. 8n + 7 (rotated, normalized)
+        float qr[NH][8];
 #pragma unroll
-        for (int k = 0; k < 8; ++k) qr[k] = sm.q[G][8 * n + k] * kInvSqrt128;
+        for (int hg = 0; hg < NH; ++hg)
+#pragma unroll
+            for (int k = 0; k < 8; ++k) qr[hg][k] = sm.q[4 * hg + G][8 * n + k] * kInvSqrt128;
         // source lane of the PV operand permutation (see above), as a byte address
         const int perm_addr = (16 * h + 4 * G + j) * 4;
 
@@ -700,118 +710,143 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                 const float4 r1 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n + 4]);
                 const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
                 const float rk[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
-                float qt[8], mx = 0.f;
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    qt[k] = qr[k] * av[k];
-                    mx = fmaxf(mx, fabsf(qt[k]));
-                }
-                mx = row_max(mx);
-                const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
-                float bs = 0.f;
-                uint32_t y[8];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const float yf = fmaf(qt[k], sc, MAGIC);
-                    bs = fmaf(yf - MAGIC, rk[k], bs);
-                    y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
-                }
-                bs = row_sum(bs);
-                uint32_t d0, d1, d2, e0, e1, e2;
-                digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
-                digits4(y[4], y[5], y[6], y[7], e0, e1, e2);
                 // channels 8n .. 8n + 7 = kappa n / 8, group (n % 8) / 2, components 2 (n % 2) + {0, 1}
                 const int kap = n >> 3, Gq = (n >> 1) & 3, half = n & 1;
-                reinterpret_cast<uint2*>(&sm.qp[0][kap][Gq][G])[half] = make_uint2(d0, e0);
-                reinterpret_cast<uint2*>(&sm.qp[1][kap][Gq][G])[half] = make_uint2(d1, e1);
-                reinterpret_cast<uint2*>(&sm.qp[2][kap][Gq][G])[half] = make_uint2(d2, e2);
-                if (n == 0) {
-                    sm.hv[G][0] = bs;
-                    sm.hv[G][1] = mx * (1.0f / (float)QMAX);
+#pragma unroll
+                for (int hg = 0; hg < NH; ++hg) {
+                    float qt[8], mx = 0.f;
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        qt[k] = qr[hg][k] * av[k];
+                        mx = fmaxf(mx, fabsf(qt[k]));
+                    }
+                    mx = row_max(mx);
+                    const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
+                    float bs = 0.f;
+                    uint32_t y[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const float yf = fmaf(qt[k], sc, MAGIC);
+                        bs = fmaf(yf - MAGIC, rk[k], bs);
+                        y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
+                    }
+                    bs = row_sum(bs);
+                    uint32_t d0, d1, d2, e0, e1, e2;
+                    digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
+                    digits4(y[4], y[5], y[6], y[7], e0, e1, e2);
+                    reinterpret_cast<uint2*>(&sm.qp[hg][0][kap][Gq][G])[half] = make_uint2(d0, e0);
+                    reinterpret_cast<uint2*>(&sm.qp[hg][1][kap][Gq][G])[half] = make_uint2(d1, e1);
+                    reinterpret_cast<uint2*>(&sm.qp[hg][2][kap][Gq][G])[half] = make_uint2(d2, e2);
+                    if (n == 0) {
+                        sm.hv[4 * hg + G][0] = bs;
+                        sm.hv[4 * hg + G][1] = mx * (1.0f / (float)QMAX);
+                    }
                 }
             }
             __syncthreads();
-            v4i aq[2];
-#pragma unroll
-            for (int kap = 0; kap < 2; ++kap) {
-                const uint4 u = sm.qp[j][kap][G][h];
-                aq[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
-            }
-            const float beta = sm.hv[G][0];                  // q~ grid units
-            const float fqs = sm.hv[G][1] * a.scale_log2;   // grid step * scale
 
-            // logits of head G, token 64*sg + 16*tau + n
-            float lg[8];
+            // logits of head 4*hg + G, token 64*sg + 16*tau + n
+            float lg[NH][8];
 #pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
+            for (int hg = 0; hg < NH; ++hg) {
+                v4i aq[2];
 #pragma unroll
-                for (int tau = 0; tau < 4; ++tau) {
-                    v4i c = {0, 0, 0, 0};
-#pragma unroll
-                    for (int kap = 0; kap < 2; ++kap) c = mfma_i8(aq[kap], unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]), c);
-                    lg[4 * sg + tau] = ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
+                for (int kap = 0; kap < 2; ++kap) {
+                    const uint4 u = sm.qp[hg][j][kap][G][h];
+                    aq[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
+                const float beta = sm.hv[4 * hg + G][0];                 // q~ grid units
+                const float fqs = sm.hv[4 * hg + G][1] * a.scale_log2;  // grid step * scale
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                    for (int tau = 0; tau < 4; ++tau) {
+                        v4i c = {0, 0, 0, 0};
+#pragma unroll
+                        for (int kap = 0; kap < 2; ++kap)
+                            c = mfma_i8(aq[kap], unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]), c);
+                        lg[hg][4 * sg + tau] =
+                            ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
+                    }
+            }
             if (more) load_codes(tile_k(blk + 1), kc);
-            const float alpha = softmax_update(lg, false);
 
-            // p~ = p * a_V as fixed point on a per-head grid; gamma from the same rounded integers
-            float pmx = 0.f;
 #pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                lg[k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + n];
-                pmx = fmaxf(pmx, lg[k]);
-            }
-            pmx = row_max(pmx);
-            const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
-            float gam = 0.f;
-            v4i ap[2];
+            for (int hg = 0; hg < NH; ++hg) {
+                const float alpha = softmax_update(lg[hg], false, m_run[hg], l_run[hg]);
+
+                // p~ = p * a_V as fixed point on a per-head grid; gamma from the same rounded
+                // integers
+                float pmx = 0.f;
 #pragma unroll
-            for (int sg = 0; sg < 2; ++sg) {
-                uint32_t D[4];
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau) {
-                    const float yf = fmaf(lg[4 * sg + tau], psc, MAGIC);
-                    gam = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam);
-                    // bytes of y: the three digits plus 128 each, and 0x80 on top (digit slot 3
-                    // becomes zero); after the transpose lane (head, 4m + i) holds digit i of
-                    // tokens 16 tau + 4m + {0..3}, which lane (m, 4 head + i) takes as A operand
-                    const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
-                    const uint32_t t = quad_transpose_bytes(y, j);
-                    D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t) ^ 0x80808080u;
+                for (int k = 0; k < 8; ++k) {
+                    lg[hg][k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + n];
+                    pmx = fmaxf(pmx, lg[hg][k]);
                 }
-                ap[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
-            }
-            gam = row_sum(gam);
+                pmx = row_max(pmx);
+                const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
+                float gam = 0.f;
+                v4i ap[2];
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg) {
+                    uint32_t D[4];
+#pragma unroll
+                    for (int tau = 0; tau < 4; ++tau) {
+                        const float yf = fmaf(lg[hg][4 * sg + tau], psc, MAGIC);
+                        gam = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam);
+                        // bytes of y: the three digits plus 128 each, and 0x80 on top (digit
+                        // slot 3 becomes zero); after the transpose lane (head, 4m + i) holds
+                        // digit i of tokens 16 tau + 4m + {0..3}, which lane (m, 4 head + i)
+                        // takes as A operand
+                        const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
+                        const uint32_t t = quad_transpose_bytes(y, j);
+                        D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t) ^ 0x80808080u;
+                    }
+                    ap[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
+                }
+                gam = row_sum(gam);
 
-            // PV: head G, channel 16*mt + n
-            v4i acc[8];
+                // PV: head 4*hg + G, channel 16*mt + n
+                v4i acc[8];
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) acc[mt] = v4i{0, 0, 0, 0};
+                for (int mt = 0; mt < 8; ++mt) acc[mt] = v4i{0, 0, 0, 0};
 #pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
+                for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                    for (int mt = 0; mt < 8; ++mt)
+                        acc[mt] = mfma_i8(ap[sg], unit_i8<BITS>(&vw[sg][mt * WPU]), acc[mt]);
+                if (hg == NH - 1 && more) load_codes(tile_v(blk + 1), vc);
+                const float fp = pmx * (1.0f / (float)QMAX);
 #pragma unroll
                 for (int mt = 0; mt < 8; ++mt)
-                    acc[mt] = mfma_i8(ap[sg], unit_i8<BITS>(&vw[sg][mt * WPU]), acc[mt]);
-            if (more) load_codes(tile_v(blk + 1), vc);
-            const float fp = pmx * (1.0f / (float)QMAX);
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt)
-                orot[mt] = fmaf((float)digit_sum(acc[mt]) + gam, fp * sm.aux[5][16 * mt + n], orot[mt] * alpha);
+                    orot[hg][mt] = fmaf((float)digit_sum(acc[mt]) + gam, fp * sm.aux[5][16 * mt + n],
+                                        orot[hg][mt] * alpha);
+            }
         }
     }
 
     // ---- sink and residual (bf16, unrotated): last split only ------------------------------
+    float oplain[NHD][2];  // head hh, channel 2*l + jj (unrotated)
+#pragma unroll
+    for (int hh = 0; hh < NHD; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
     if (last && ns + nr > 0) {
-        // A operand: row 4h holds q of head h rounded to bf16, row 4h + 1 the remainder (zero
-        // for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds q[h][32k + 8G ..]
-        v8bf aq[4];
+        // A operand of group hg: row 4h holds q of head 4*hg + h rounded to bf16, row 4h + 1 the
+        // remainder (zero for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds
+        // q[.][32k + 8G ..].  Loads are clamped to a valid head, then masked.
+        v8bf aqs[NH][4];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+        for (int hg = 0; hg < NH; ++hg) {
+            const int qh = 4 * hg + h;
+            const bool use = qh < g && j < 2;
+            const size_t base = (qrow + min(qh, g - 1)) * kD + 8 * G;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float v = (h < g && j < 2) ? load_q((qrow + h) * kD + 32 * k + 8 * G + e) : 0.f;
-                const __bf16 hi = (__bf16)v;
-                aq[k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
+            for (int k = 0; k < 4; ++k) {
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float v = use ? load_q(base + 32 * k + e) : 0.f;
+                    const __bf16 hi = (__bf16)v;
+                    aqs[hg][k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
+                }
             }
         }
         const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
@@ -824,34 +859,37 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                                          : a.k_resid + (size_t)stream * kG * kD;
             const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
                                          : a.v_resid + (size_t)stream * kG * kD;
-            // logits of head G, token 16*tau + n
-            float lg[8];
-#pragma unroll
-            for (int tau = 0; tau < 8; ++tau) {
-                v4f acc = {0.f, 0.f, 0.f, 0.f};
-                const int trow = 16 * tau + n;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    uint4 u = {0u, 0u, 0u, 0u};
-                    if (trow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)trow * kD + 32 * k + 8 * G);
-                    v8bf B;
-                    __builtin_memcpy(&B, &u, 16);
-                    acc = mfma_bf16(aq[k], B, acc);
-                }
-                lg[tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
-            }
-            const float alpha = softmax_update(lg, true);
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) orot[mt] *= alpha;
             __syncthreads();  // the previous chunk is done with sm.p / sm.hv
-            if (head_ok) {
 #pragma unroll
-                for (int tau = 0; tau < 8; ++tau) sm.p[G][16 * tau + n] = lg[tau];
-                if (n == 0) sm.hv[G][2] = alpha;
+            for (int hg = 0; hg < NH; ++hg) {
+                // logits of head 4*hg + G, token 16*tau + n
+                float lg[8];
+#pragma unroll
+                for (int tau = 0; tau < 8; ++tau) {
+                    v4f acc = {0.f, 0.f, 0.f, 0.f};
+                    const int trow = 16 * tau + n;
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        uint4 u = {0u, 0u, 0u, 0u};
+                        if (trow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)trow * kD + 32 * k + 8 * G);
+                        v8bf B;
+                        __builtin_memcpy(&B, &u, 16);
+                        acc = mfma_bf16(aqs[hg][k], B, acc);
+                    }
+                    lg[tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
+                }
+                const float alpha = softmax_update(lg, true, m_run[hg], l_run[hg]);
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) orot[hg][mt] *= alpha;
+                if (4 * hg + G < g) {
+#pragma unroll
+                    for (int tau = 0; tau < 8; ++tau) sm.p[4 * hg + G][16 * tau + n] = lg[tau];
+                    if (n == 0) sm.hv[4 * hg + G][2] = alpha;
+                }
             }
             __syncthreads();
 #pragma unroll
-            for (int hh = 0; hh < 4; ++hh) {
+            for (int hh = 0; hh < NHD; ++hh) {
                 if (hh < g) {
                     const float al = sm.hv[hh][2];
                     oplain[hh][0] *= al;
@@ -862,7 +900,7 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
                 const uint32_t v2 = reinterpret_cast<const uint32_t*>(Vp + (size_t)t * kD)[l];
                 const float v0 = __uint_as_float(v2 << 16), v1 = __uint_as_float(v2 & 0xFFFF0000u);
 #pragma unroll
-                for (int hh = 0; hh < 4; ++hh) {
+                for (int hh = 0; hh < NHD; ++hh) {
                     if (hh < g) {
                         const float ph = sm.p[hh][t];
                         oplain[hh][0] = fmaf(ph, v0, oplain[hh][0]);
@@ -874,18 +912,23 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
     }
 
     // ---- finish ------------------------------------------------------------------------------
-    const float lt = row_sum(l_run);
+    float lt[NH];
+#pragma unroll
+    for (int hg = 0; hg < NH; ++hg) lt[hg] = row_sum(l_run[hg]);
     if (a.n_split == 1) {
         __syncthreads();
-        if (head_ok) {
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) sm.q[G][16 * mt + n] = orot[mt];
-            if (n == 0) sm.hv[G][3] = lt;
+        for (int hg = 0; hg < NH; ++hg) {
+            if (4 * hg + G < g) {
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) sm.q[4 * hg + G][16 * mt + n] = orot[hg][mt];
+                if (n == 0) sm.hv[4 * hg + G][3] = lt[hg];
+            }
         }
         __syncthreads();
-        lds_hadamard<4>(sm.q, g);
+        lds_hadamard<NHD>(sm.q, g);
 #pragma unroll
-        for (int hh = 0; hh < 4; ++hh) {
+        for (int hh = 0; hh < NHD; ++hh) {
             if (hh < g) {
                 const float L = sm.hv[hh][3];
                 float o0 = sm.q[hh][2 * l] * kInvSqrt128 + oplain[hh][0];
@@ -901,17 +944,20 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 ? 
             }
         }
     } else {
-        if (head_ok) {
-            float* P = a.ws + ((qrow + G) * a.n_split + split) * kPart;
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) P[4 + 16 * mt + n] = orot[mt];
-            if (n == 0) {
-                P[0] = m_run;
-                P[1] = lt;
+        for (int hg = 0; hg < NH; ++hg) {
+            if (4 * hg + G < g) {
+                float* P = a.ws + ((qrow + 4 * hg + G) * a.n_split + split) * kPart;
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) P[4 + 16 * mt + n] = orot[hg][mt];
+                if (n == 0) {
+                    P[0] = m_run[hg];
+                    P[1] = lt[hg];
+                }
             }
         }
 #pragma unroll
-        for (int hh = 0; hh < 4; ++hh) {
+        for (int hh = 0; hh < NHD; ++hh) {
             if (hh < g) {
                 float* P = a.ws + ((qrow + hh) * a.n_split + split) * kPart;
                 *reinterpret_cast<float2*>(P + 132 + 2 * l) = make_float2(oplain[hh][0], oplain[hh][1]);
@@ -970,7 +1016,9 @@ template <int BITS, int GQ>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
     if constexpr (GQ == 4)
-        hipLaunchKernelGGL((k_decode4<BITS>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+        hipLaunchKernelGGL((k_decode4<BITS, 1>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+    else if constexpr (GQ == 8)
+        hipLaunchKernelGGL((k_decode4<BITS, 2>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     else
         hipLaunchKernelGGL((k_decode<BITS, GQ>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     hipError_t e = hipGetLastError();
