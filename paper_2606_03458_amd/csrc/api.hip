@@ -132,7 +132,7 @@ int kvarn_append_token(const kvarn_params* p, const kvarn_cache* cache, const vo
 size_t kvarn_decode_workspace_bytes(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q,
                                     int32_t max_len_hint) {
     if (check_params(p) || !cache || cache->batch <= 0 || cache->n_kv <= 0 || n_q <= 0 || max_len_hint < 0) return 0;
-    const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, max_len_hint, p->n_sink, cache->max_blocks);
+    const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
     return decode_workspace_bytes(cache->batch, n_q, plan);
 }
 
@@ -147,7 +147,7 @@ int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int3
     if (check_dtype(q_dtype) || check_dtype(out_dtype)) return KVARN_EINVAL;
     if (!q || !out || !std::isfinite(sm_scale) || max_len_hint < 0) return KVARN_EINVAL;
     if (!aligned(q, 4) || !aligned(out, 8)) return KVARN_EINVAL;
-    const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, max_len_hint, p->n_sink, cache->max_blocks);
+    const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
     const size_t need = decode_workspace_bytes(cache->batch, n_q, plan);
     if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return KVARN_EWORKSPACE;
     hipError_t e = launch_decode(*cache, p->bits, p->n_sink, n_q, q, q_dtype == KVARN_BF16, out,

@@ -51,7 +51,7 @@ struct DecodePlan {
     int max_blocks_used;   // upper bound of body tiles over the batch
 };
 
-DecodePlan plan_decode(int batch, int n_kv, int max_len, int n_sink, int max_blocks);
+DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int n_sink, int max_blocks);
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan);
 
 hipError_t launch_decode(const kvarn_cache& c, int bits, int n_sink, int n_q, const void* q, bool q_bf16, void* out,

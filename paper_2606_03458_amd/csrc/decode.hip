@@ -1036,15 +1036,19 @@ hipError_t launch_bits(const DecodeArgs& a, int batch, hipStream_t stream) {
 
 }  // namespace
 
-DecodePlan plan_decode(int batch, int n_kv, int max_len, int n_sink, int max_blocks) {
+DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int n_sink, int max_blocks) {
     DecodePlan p;
     int nb = max_len > n_sink ? (max_len - n_sink) / kG : 0;
     if (nb > max_blocks) nb = max_blocks;
     p.max_blocks_used = nb;
     const int streams = batch * n_kv;
-    // one wave per (split, stream): aim for about 4096 waves (4 per SIMD), at least one tile each
-    int want = (4096 + streams - 1) / streams;
-    if (want > nb) want = nb;
+    const int g = n_kv > 0 ? n_q / n_kv : 1;
+    // one wave per (split, stream).  Aim for one round of resident waves (the kernels'
+    // occupancy on 1024 SIMDs), with at least 4 body tiles per split so that the per-wave
+    // setup and the merge stay small against the streaming.
+    const int per_simd = g <= 4 ? (bits == 2 ? 3 : 2) : (g <= 8 ? 2 : 1);
+    int want = (1024 * per_simd + streams - 1) / streams;
+    if (want > nb / 4) want = nb / 4;
     if (want <= 1) {
         p.n_split = 1;
         p.blocks_per_split = nb > 0 ? nb : 1;

@@ -152,7 +152,7 @@ def test_decode_variants(K, bits, n_sink, name):
     """Sink region, 4-bit codes, GQA 5, ragged lengths (including 0 and sink-only) and a
     residual, on a small batch that the split-K plan divides into many splits."""
     from paper_2606_03458_amd import workloads
-    built, _ = workloads.build(name, bits=bits, n_sink=n_sink, context=n_sink + 3 * 128 + 77, batch=5)
+    built, _ = workloads.build(name, bits=bits, n_sink=n_sink, context=n_sink + 20 * 128 + 77, batch=5)
     lens = [built.length, n_sink + 2 * 128, n_sink + 131, n_sink // 2 if n_sink else 0, 0]
     built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
     q = workloads.decode_queries(built, seed=3)
@@ -162,10 +162,10 @@ def test_decode_variants(K, bits, n_sink, name):
 
 @pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (12, 2), (32, 2)])
 def test_decode_group_sizes(K, n_q, n_kv):
-    """Every query-group size class (1 .. 4 share one kernel, 5 .. 8 and 9 .. 16 the others),
-    with a residual and several body tiles."""
+    """Every query-group size class (1 .. 4, 5 .. 8, 9 .. 16 take different kernels), with a
+    residual and enough body tiles for the plan to split every stream."""
     from paper_2606_03458_amd import workloads
-    built, _ = workloads.build("llama", context=3 * 128 + 45, batch=2, n_q=n_q, n_kv=n_kv)
+    built, _ = workloads.build("llama", context=12 * 128 + 45, batch=2, n_q=n_q, n_kv=n_kv)
     q = workloads.decode_queries(built, seed=6)
     out = _decode(K, built, q)
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
