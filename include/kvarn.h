@@ -80,6 +80,9 @@ typedef struct {
     float log_lo;       /* clamp of the cumulative log-scales: -0.3 (Algorithm 1)       */
     float log_hi;       /* 10.0 (Algorithm 1)                                           */
 } kvarn_params;
+/* Accepted ranges (else KVARN_EINVAL): 1e-30 <= var_min <= var_max <= 1e30 and
+ * -40 <= log_lo <= log_hi <= 40, which keeps every scale exp(+-L) and every log of a clamped
+ * variance inside the normal fp32 range. */
 
 /* The cache of `batch` sequences with n_kv kv heads each (a model's layers may be folded
  * into batch).  Device buffers, all caller-allocated (sizes from kvarn_cache_sizes):

@@ -16,9 +16,9 @@ int check_params(const kvarn_params* p) {
     if (p->bits != 2 && p->bits != 4) return KVARN_EUNSUPPORTED;
     if (p->varn_iters < 0 || p->varn_iters > 64) return KVARN_EINVAL;
     if (p->n_sink < 0 || p->n_sink > 1024) return KVARN_EINVAL;
-    if (!std::isfinite(p->var_min) || !std::isfinite(p->var_max) || !(p->var_min > 0.f) || p->var_min > p->var_max)
-        return KVARN_EINVAL;
-    if (std::isnan(p->log_lo) || std::isnan(p->log_hi) || p->log_lo > p->log_hi) return KVARN_EINVAL;
+    // ranges that keep exp(+-L) and log(v) of the quantizer inside the normal fp32 range
+    if (!(p->var_min >= 1e-30f) || !(p->var_max <= 1e30f) || p->var_min > p->var_max) return KVARN_EINVAL;
+    if (!(p->log_lo >= -40.f) || !(p->log_hi <= 40.f) || p->log_lo > p->log_hi) return KVARN_EINVAL;
     return KVARN_OK;
 }
 

@@ -41,15 +41,40 @@ struct OpMin {
     __device__ static float f(float a, float b) { return fminf(a, b); }
 };
 
-// Across the 16 threads that share a channel block (all token blocks): lanes ^16, ^32, then
-// the four waves through LDS.  Every thread of a channel block ends with the same values.
+template <int CTRL>
+__device__ __forceinline__ float dppf(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+
+// Op over the 16 lanes of a DPP row: quad partners ^1 and ^2, then the other quad of the half
+// (mirror within 8 lanes) and the other half (mirror within 16).  Each step combines two
+// equal partial results, so every lane of the row ends with the same value.
+template <class Op>
+__device__ __forceinline__ float row16(float v) {
+    v = Op::f(v, dppf<0xB1>(v));
+    v = Op::f(v, dppf<0x4E>(v));
+    v = Op::f(v, dppf<0x141>(v));
+    return Op::f(v, dppf<0x140>(v));
+}
+
+// Op over lanes l, l ^ 16, l ^ 32, l ^ 48 (the four rows of a wave).  With both operands equal,
+// a row-pair swap returns (value of the even row, value of the odd row) in every lane of the
+// pair, so all four lanes end with the same value.
+template <class Op>
+__device__ __forceinline__ float across_rows(float v) {
+    const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = Op::f(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return Op::f(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+// Across the 16 threads that share a channel block (all token blocks): the four rows of the
+// wave, then the four waves through LDS.  Every thread of a channel block ends with the same
+// values.
 template <class Op>
 __device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& buf, const Lane& L) {
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        s[j] = Op::f(s[j], __shfl_xor(s[j], 16));
-        s[j] = Op::f(s[j], __shfl_xor(s[j], 32));
-    }
+    for (int j = 0; j < 8; ++j) s[j] = across_rows<Op>(s[j]);
     if (L.lane < 16) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) sm.red[buf][L.wave][8 * L.tc + j] = s[j];
@@ -63,25 +88,23 @@ __device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& b
     buf ^= 1;
 }
 
-// Across the 16 channel-block threads of a token row (lanes ^1, ^2, ^4, ^8 of a DPP row).
+// Across the 16 channel-block threads of a token row (one DPP row).
 template <class Op>
 __device__ __forceinline__ void reduce_rows(float (&s)[8]) {
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-#pragma unroll
-        for (int m = 1; m < 16; m <<= 1) s[i] = Op::f(s[i], __shfl_xor(s[i], m));
-    }
+    for (int i = 0; i < 8; ++i) s[i] = row16<Op>(s[i]);
 }
 
 // Variance over tokens of every column of T*w (two-pass, ddof = 1).
 __device__ __forceinline__ void column_var(const float (&x)[8][8], const float (&w)[8], float (&var)[8],
                                            QuantSmem& sm, int& buf, const Lane& L) {
+    // (explicit fmas: each pass forms x * w inside its own fma)
     float s[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         float acc = 0.f;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) acc += x[i][j] * w[i];
+        for (int i = 0; i < 8; ++i) acc = fmaf(x[i][j], w[i], acc);
         s[j] = acc;
     }
     reduce_cols<OpSum>(s, sm, buf, L);
@@ -93,8 +116,8 @@ __device__ __forceinline__ void column_var(const float (&x)[8][8], const float (
         float acc = 0.f;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
-            const float d = x[i][j] * w[i] - mean[j];
-            acc += d * d;
+            const float d = fmaf(x[i][j], w[i], -mean[j]);
+            acc = fmaf(d, d, acc);
         }
         s[j] = acc;
     }
@@ -110,7 +133,7 @@ __device__ __forceinline__ void row_var(const float (&x)[8][8], const float (&u)
     for (int i = 0; i < 8; ++i) {
         float acc = 0.f;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) acc += x[i][j] * u[j];
+        for (int j = 0; j < 8; ++j) acc = fmaf(x[i][j], u[j], acc);
         s[i] = acc;
     }
     reduce_rows<OpSum>(s);
@@ -122,8 +145,8 @@ __device__ __forceinline__ void row_var(const float (&x)[8][8], const float (&u)
         float acc = 0.f;
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-            const float d = x[i][j] * u[j] - mean[i];
-            acc += d * d;
+            const float d = fmaf(x[i][j], u[j], -mean[i]);
+            acc = fmaf(d, d, acc);
         }
         s[i] = acc;
     }
@@ -145,16 +168,11 @@ __device__ __forceinline__ float imbalance(const float (&vr)[8], const float (&v
         cmin = fminf(cmin, vc[k]);
     }
     // columns: all 128 channels live in one 16-lane row
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) {
-        cmax = fmaxf(cmax, __shfl_xor(cmax, m));
-        cmin = fminf(cmin, __shfl_xor(cmin, m));
-    }
+    cmax = row16<OpMax>(cmax);
+    cmin = row16<OpMin>(cmin);
     // rows: token blocks span the four lane groups and the four waves
-    rmax = fmaxf(rmax, __shfl_xor(rmax, 16));
-    rmin = fminf(rmin, __shfl_xor(rmin, 16));
-    rmax = fmaxf(rmax, __shfl_xor(rmax, 32));
-    rmin = fminf(rmin, __shfl_xor(rmin, 32));
+    rmax = across_rows<OpMax>(rmax);
+    rmin = across_rows<OpMin>(rmin);
     if (L.lane == 0) {
         sm.rstat[buf][L.wave][0] = rmax;
         sm.rstat[buf][L.wave][1] = rmin;
@@ -167,6 +185,12 @@ __device__ __forceinline__ float imbalance(const float (&vr)[8], const float (&v
 }
 
 __device__ __forceinline__ float clampf(float v, float lo, float hi) { return fminf(fmaxf(v, lo), hi); }
+
+// Natural log and exp on the hardware log2 / exp2.  Their arguments stay far from the denormal
+// range (variances clamped to [var_min, var_max] >= 1e-30, log-scales to [log_lo, log_hi]
+// within +-40), so no range fix-up is needed.
+__device__ __forceinline__ float ln_hw(float v) { return __builtin_amdgcn_logf(v) * 0.6931471805599453f; }
+__device__ __forceinline__ float exp_hw(float v) { return __builtin_amdgcn_exp2f(v * kLog2e); }
 
 // Quantize one tile.  src: token t at src + t*tstride elements, channels contiguous (16-byte
 // aligned rows).  dst: the packed tile (16-byte aligned).
@@ -218,7 +242,8 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         for (int i = 0; i < 8; ++i) {
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const float p = __shfl_xor(x[i][j], m);
+                // partners ^1 and ^2 by DPP quad permutes, ^4 and ^8 through the LDS crossbar
+                const float p = m == 1 ? dppf<0xB1>(x[i][j]) : (m == 2 ? dppf<0x4E>(x[i][j]) : __shfl_xor(x[i][j], m));
                 x[i][j] = upper ? (p - x[i][j]) : (x[i][j] + p);
             }
         }
@@ -245,16 +270,16 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
             const float v = clampf(u[j] * u[j] * cv[j], P.var_min, P.var_max);
-            Lc[j] = clampf(Lc[j] + 0.5f * __logf(v), P.log_lo, P.log_hi);
-            u[j] = __expf(-Lc[j]);
+            Lc[j] = clampf(Lc[j] + 0.5f * ln_hw(v), P.log_lo, P.log_hi);
+            u[j] = exp_hw(-Lc[j]);
         }
         // row update from the row variances w^2 * var_c(T u)
         row_var(x, u, rv);
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const float v = clampf(w[i] * w[i] * rv[i], P.var_min, P.var_max);
-            Lr[i] = clampf(Lr[i] + 0.5f * __logf(v), P.log_lo, P.log_hi);
-            w[i] = __expf(-Lr[i]);
+            Lr[i] = clampf(Lr[i] + 0.5f * ln_hw(v), P.log_lo, P.log_hi);
+            w[i] = exp_hw(-Lr[i]);
         }
         // imbalance of the new Cur; its column statistics seed the next column update
         column_var(x, w, cv, sm, buf, L);
@@ -280,10 +305,10 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
     float Sc[8], Sr[8];
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
-        Sc[m] = __expf(bLc[m]);
-        Sr[m] = __expf(bLr[m]);
-        u[m] = __expf(-bLc[m]);
-        w[m] = __expf(-bLr[m]);
+        Sc[m] = exp_hw(bLc[m]);
+        Sr[m] = exp_hw(bLr[m]);
+        u[m] = exp_hw(-bLc[m]);
+        w[m] = exp_hw(-bLr[m]);
     }
 #pragma unroll
     for (int i = 0; i < 8; ++i) {

@@ -75,7 +75,9 @@ def test_quantize_validation(K):
     call(n_outer=0, x=None, out=None)
     call(n_inner=0)
     for field, val, code in [("bits", 3, -2), ("varn_iters", -1, -1), ("varn_iters", 65, -1), ("var_min", 0.0, -1),
-                             ("var_min", float("nan"), -1), ("log_lo", 11.0, -1), ("n_sink", -5, -1)]:
+                             ("var_min", float("nan"), -1), ("var_min", 1e-31, -1), ("var_max", 1e31, -1),
+                             ("var_max", float("inf"), -1), ("log_lo", 11.0, -1), ("log_lo", -41.0, -1),
+                             ("log_hi", 41.0, -1), ("log_hi", float("nan"), -1), ("n_sink", -5, -1)]:
         q = K.kvarn_params_init(2)
         setattr(q, field, val)
         with pytest.raises(K.KVarNError) as e:
@@ -126,11 +128,12 @@ def test_append_validation(K):
 
 def test_decode_validation(K):
     p = K.kvarn_params_init(2)
-    c = _HostCache(K, batch=2, n_kv=2, max_blocks=4)
+    c = _HostCache(K, batch=2, n_kv=2, max_blocks=32)
     keep, buf = _fake(1 << 20)
-    need = K.kvarn_decode_workspace_bytes(p, c, 8, 512)
+    need = K.kvarn_decode_workspace_bytes(p, c, 8, 4096)  # 4 streams x 32 tiles: split
     assert need > 0
-    good = dict(n_q=8, q=buf, q_dtype=1, out=buf, out_dtype=1, sm_scale=0.088, max_len_hint=512, workspace=buf,
+    assert K.kvarn_decode_workspace_bytes(p, c, 8, 512) == 0  # 4 tiles: one split, no partials
+    good = dict(n_q=8, q=buf, q_dtype=1, out=buf, out_dtype=1, sm_scale=0.088, max_len_hint=4096, workspace=buf,
                 workspace_bytes=need)
 
     def call(**kw):
@@ -145,7 +148,7 @@ def test_decode_validation(K):
             call(**kw)
         assert e.value.status == code, kw
     # the workspace grows with the split plan and the number of query heads
-    assert K.kvarn_decode_workspace_bytes(p, c, 16, 512) == 2 * need
+    assert K.kvarn_decode_workspace_bytes(p, c, 16, 4096) == 2 * need
     assert K.kvarn_decode_workspace_bytes(p, c, 8, -1) == 0
 
 
