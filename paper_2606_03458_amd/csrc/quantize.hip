@@ -454,7 +454,7 @@ struct TileArgs {
     int32_t* best_iter;
 };
 
-__global__ __launch_bounds__(kThreads) void k_quantize_tiles(TileArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_quantize_tiles(TileArgs a) {
     __shared__ QuantSmem sm;
     const int64_t tile = a.tile0 + blockIdx.x;
     const int64_t i = tile / a.n_inner, j = tile % a.n_inner;
@@ -473,7 +473,7 @@ struct FlushArgs {
 // One workgroup per (sequence, kv head, K|V).  Runs after the append kernel has incremented
 // seq_len: a sequence whose residual just reached 128 tokens quantizes it into body tile
 // (len - n_sink)/128 - 1; every other workgroup exits at once.
-__global__ __launch_bounds__(kThreads) void k_flush(FlushArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_flush(FlushArgs a) {
     __shared__ QuantSmem sm;
     const int kind = blockIdx.x & 1;
     const int64_t stream = blockIdx.x >> 1;
