@@ -71,15 +71,26 @@ __device__ __forceinline__ float across_rows(float v) {
 // Across the 16 threads that share a channel block (all token blocks): the four rows of the
 // wave, then the four waves through LDS.  Every thread of a channel block ends with the same
 // values.
-template <class Op>
-__device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& buf, const Lane& L) {
+// With STAT, the same LDS round also carries one (max, min) pair per wave (xmax, xmin: the
+// wave's values in, the workgroup's out).
+template <class Op, bool STAT = false>
+__device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& buf, const Lane& L,
+                                            float* xmax = nullptr, float* xmin = nullptr) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) s[j] = across_rows<Op>(s[j]);
     if (L.lane < 16) {
 #pragma unroll
         for (int j = 0; j < 8; ++j) sm.red[buf][L.wave][8 * L.tc + j] = s[j];
     }
+    if (STAT && L.lane == 0) {
+        sm.rstat[buf][L.wave][0] = *xmax;
+        sm.rstat[buf][L.wave][1] = *xmin;
+    }
     __syncthreads();
+    if (STAT) {
+        *xmax = fmaxf(fmaxf(sm.rstat[buf][0][0], sm.rstat[buf][1][0]), fmaxf(sm.rstat[buf][2][0], sm.rstat[buf][3][0]));
+        *xmin = fminf(fminf(sm.rstat[buf][0][1], sm.rstat[buf][1][1]), fminf(sm.rstat[buf][2][1], sm.rstat[buf][3][1]));
+    }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
         const int c = 8 * L.tc + j;
@@ -95,9 +106,10 @@ __device__ __forceinline__ void reduce_rows(float (&s)[8]) {
     for (int i = 0; i < 8; ++i) s[i] = row16<Op>(s[i]);
 }
 
-// Variance over tokens of every column of T*w (two-pass, ddof = 1).
+// Variance over tokens of every column of T*w (two-pass, ddof = 1).  The first LDS round also
+// reduces the wave's (rmax, rmin) of the row variances to the workgroup's.
 __device__ __forceinline__ void column_var(const float (&x)[8][8], const float (&w)[8], float (&var)[8],
-                                           QuantSmem& sm, int& buf, const Lane& L) {
+                                           QuantSmem& sm, int& buf, const Lane& L, float& rmax, float& rmin) {
     // (explicit fmas: each pass forms x * w inside its own fma)
     float s[8];
 #pragma unroll
@@ -107,7 +119,7 @@ __device__ __forceinline__ void column_var(const float (&x)[8][8], const float (
         for (int i = 0; i < 8; ++i) acc = fmaf(x[i][j], w[i], acc);
         s[j] = acc;
     }
-    reduce_cols<OpSum>(s, sm, buf, L);
+    reduce_cols<OpSum, true>(s, sm, buf, L, &rmax, &rmin);
     float mean[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) mean[j] = s[j] * (1.0f / kG);
@@ -156,31 +168,28 @@ __device__ __forceinline__ void row_var(const float (&x)[8][8], const float (&u)
 }
 
 // Imb of Algorithm 1 from the row variances (per token, replicated over tc) and the column
-// variances (per channel, replicated over tr).  Uniform over the workgroup.
-__device__ __forceinline__ float imbalance(const float (&vr)[8], const float (&vc)[8], QuantSmem& sm, int& buf,
-                                           const Lane& L) {
-    float rmax = vr[0], rmin = vr[0], cmax = vc[0], cmin = vc[0];
+// variances (per channel, replicated over tr), in two parts: the wave's max / min of the row
+// variances (reduced over the workgroup by column_var's first LDS round), then the value.
+__device__ __forceinline__ void row_stat(const float (&vr)[8], float& rmax, float& rmin) {
+    rmax = rmin = vr[0];
 #pragma unroll
     for (int k = 1; k < 8; ++k) {
         rmax = fmaxf(rmax, vr[k]);
         rmin = fminf(rmin, vr[k]);
+    }
+    rmax = across_rows<OpMax>(rmax);
+    rmin = across_rows<OpMin>(rmin);
+}
+__device__ __forceinline__ float imbalance(float rmax, float rmin, const float (&vc)[8]) {
+    float cmax = vc[0], cmin = vc[0];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) {
         cmax = fmaxf(cmax, vc[k]);
         cmin = fminf(cmin, vc[k]);
     }
-    // columns: all 128 channels live in one 16-lane row
+    // all 128 channels live in one 16-lane row
     cmax = row16<OpMax>(cmax);
     cmin = row16<OpMin>(cmin);
-    // rows: token blocks span the four lane groups and the four waves
-    rmax = across_rows<OpMax>(rmax);
-    rmin = across_rows<OpMin>(rmin);
-    if (L.lane == 0) {
-        sm.rstat[buf][L.wave][0] = rmax;
-        sm.rstat[buf][L.wave][1] = rmin;
-    }
-    __syncthreads();
-    rmax = fmaxf(fmaxf(sm.rstat[buf][0][0], sm.rstat[buf][1][0]), fmaxf(sm.rstat[buf][2][0], sm.rstat[buf][3][0]));
-    rmin = fminf(fminf(sm.rstat[buf][0][1], sm.rstat[buf][1][1]), fminf(sm.rstat[buf][2][1], sm.rstat[buf][3][1]));
-    buf ^= 1;
     return rmax / fmaxf(rmin, 1e-8f) + cmax / fmaxf(cmin, 1e-8f);
 }
 
@@ -261,9 +270,11 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         Lc[k] = Lr[k] = bLc[k] = bLr[k] = 0.f;
         u[k] = w[k] = 1.f;
     }
-    column_var(x, w, cv, sm, buf, L);  // variance over tokens of T's columns
-    row_var(x, u, rv);                 // variance over channels of T's rows
-    float I_best = imbalance(rv, cv, sm, buf, L);
+    float rmax, rmin;
+    row_var(x, u, rv);  // variance over channels of T's rows
+    row_stat(rv, rmax, rmin);
+    column_var(x, w, cv, sm, buf, L, rmax, rmin);  // variance over tokens of T's columns
+    float I_best = imbalance(rmax, rmin, cv);
     int best = 0;
     for (int k = 1; k <= P.iters; ++k) {
         // column update from the current column variances u^2 * var_t(T w)
@@ -282,14 +293,14 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
             w[i] = exp_hw(-Lr[i]);
         }
         // imbalance of the new Cur; its column statistics seed the next column update
-        column_var(x, w, cv, sm, buf, L);
         float vr[8], vc[8];
 #pragma unroll
-        for (int m = 0; m < 8; ++m) {
-            vr[m] = w[m] * w[m] * rv[m];
-            vc[m] = u[m] * u[m] * cv[m];
-        }
-        const float I = imbalance(vr, vc, sm, buf, L);
+        for (int m = 0; m < 8; ++m) vr[m] = w[m] * w[m] * rv[m];
+        row_stat(vr, rmax, rmin);
+        column_var(x, w, cv, sm, buf, L, rmax, rmin);
+#pragma unroll
+        for (int m = 0; m < 8; ++m) vc[m] = u[m] * u[m] * cv[m];
+        const float I = imbalance(rmax, rmin, vc);
         if (I <= I_best) {  // later iteration wins ties
             I_best = I;
             best = k;
