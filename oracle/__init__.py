@@ -14,6 +14,9 @@ Parity status of each function (pins are in ``tests/test_oracle_*.py``):
   quantize_tile    pinned through the above plus the dequantization error bound
   decode / attend  pinned (rotation invariance, special cases, numpy softmax on tiny inputs)
   append           pinned (region bookkeeping against a direct re-quantization)
+  e4m3 / fp16      pinned (all E4M3 values enumerated from the format definition, brute-force
+                   nearest / upward rounding; numpy's binary16 conversion)
+  compact aux      pinned through the conversions, the round trip and the error bound
   c_min, c_max     parity unpinned: the paper does not give their values.
 """
 from __future__ import annotations
@@ -48,12 +51,12 @@ class _Params(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("varn_iters", ctypes.c_int32),
                 ("c_min", ctypes.c_double), ("c_max", ctypes.c_double),
                 ("log_lo", ctypes.c_double), ("log_hi", ctypes.c_double),
-                ("imb_floor", ctypes.c_double), ("ddof", ctypes.c_int32)]
+                ("imb_floor", ctypes.c_double), ("ddof", ctypes.c_int32), ("aux", ctypes.c_int32)]
 
 
 class _Cache(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_kv", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
-                ("n_sink", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("n_sink", ctypes.c_int32), ("bits", ctypes.c_int32), ("aux", ctypes.c_int32),
                 ("k_body", ctypes.c_void_p), ("v_body", ctypes.c_void_p),
                 ("k_resid", ctypes.c_void_p), ("v_resid", ctypes.c_void_p),
                 ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p),
@@ -66,6 +69,8 @@ class Params:
 
     log_lo/log_hi = -0.3/10.0 and imb_floor = 1e-8 are printed in Algorithm 1; K = 8 is the
     iteration count of the runtime experiment (Sec. 4.2); c_min/c_max are unstated (unpinned).
+    aux selects the stored aux format: 0 = fp32 vectors, 1 = compact (App. D: E4M3 scales,
+    binary16 offset).
     """
     bits: int = 2
     varn_iters: int = 8
@@ -75,10 +80,11 @@ class Params:
     log_hi: float = 10.0
     imb_floor: float = 1e-8
     ddof: int = 1
+    aux: int = 0
 
     def c(self) -> _Params:
         return _Params(self.bits, self.varn_iters, self.c_min, self.c_max, self.log_lo, self.log_hi,
-                       self.imb_floor, self.ddof)
+                       self.imb_floor, self.ddof, self.aux)
 
 
 _lib = None
@@ -98,12 +104,20 @@ def lib():
         L.kvo_rtn_group.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp, ctypes.c_int, vp, vp, vp,
                                     ctypes.c_int]
         L.kvo_quantize_tile.argtypes = [vp, ctypes.c_int, ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp, vp, vp,
-                                        vp, vp, vp]
-        L.kvo_tile_bytes.argtypes = [ctypes.c_int]
+                                        vp, vp, vp, vp]
+        L.kvo_tile_bytes.argtypes = [ctypes.c_int, ctypes.c_int]
         L.kvo_tile_bytes.restype = ctypes.c_size_t
-        L.kvo_pack_tile.argtypes = [vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, vp]
-        L.kvo_unpack_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp]
-        L.kvo_dequantize_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, vp]
+        L.kvo_pack_tile.argtypes = [vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp]
+        L.kvo_unpack_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp]
+        L.kvo_dequantize_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp]
+        L.kvo_e4m3_to_double.argtypes = [ctypes.c_uint8]
+        L.kvo_e4m3_to_double.restype = ctypes.c_double
+        L.kvo_e4m3_from_double.argtypes = [ctypes.c_double, ctypes.c_int]
+        L.kvo_e4m3_from_double.restype = ctypes.c_uint8
+        L.kvo_fp16_to_double.argtypes = [ctypes.c_uint16]
+        L.kvo_fp16_to_double.restype = ctypes.c_double
+        L.kvo_fp16_from_double.argtypes = [ctypes.c_double]
+        L.kvo_fp16_from_double.restype = ctypes.c_uint16
         L.kvo_quantize_pack.argtypes = [vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int, ctypes.POINTER(_Params), vp]
         L.kvo_quantize_tiles.argtypes = [vp, ctypes.c_int, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                          ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.POINTER(_Params), vp,
@@ -194,6 +208,7 @@ class TileResult:
     Sr: np.ndarray
     imb: np.ndarray
     best_iter: int
+    pre: np.ndarray    # [3][128]: a, b, s2 before rounding to the stored format
 
 
 def quantize_tile(X, kind: int, params: Params = Params()) -> TileResult:
@@ -205,38 +220,55 @@ def quantize_tile(X, kind: int, params: Params = Params()) -> TileResult:
     T, B, u = np.zeros((G, D)), np.zeros((G, D)), np.zeros((G, D))
     Sc, Sr = np.zeros(D), np.zeros(G)
     imb = np.zeros(params.varn_iters + 1)
+    pre = np.zeros((3, 128))
     best = ctypes.c_int(-1)
     pc = params.c()
     lib().kvo_quantize_tile(_p(X), kind, ctypes.byref(pc), _p(codes), _p(a), _p(b), _p(s2), _p(T), _p(B), _p(u),
-                            _p(Sc), _p(Sr), _p(imb), ctypes.cast(ctypes.byref(best), ctypes.c_void_p))
-    return TileResult(codes, a, b, s2, T, B, u, Sc, Sr, imb, best.value)
+                            _p(Sc), _p(Sr), _p(imb), ctypes.cast(ctypes.byref(best), ctypes.c_void_p), _p(pre))
+    return TileResult(codes, a, b, s2, T, B, u, Sc, Sr, imb, best.value, pre)
 
 
-def tile_bytes(bits: int) -> int:
-    return int(lib().kvo_tile_bytes(bits))
+def tile_bytes(bits: int, aux: int = 0) -> int:
+    return int(lib().kvo_tile_bytes(bits, aux))
 
 
-def pack_tile(codes, a, b, s2, kind: int, bits: int) -> np.ndarray:
+def pack_tile(codes, a, b, s2, kind: int, bits: int, aux: int = 0) -> np.ndarray:
     codes = np.ascontiguousarray(codes, dtype=np.uint8)
     a, b, s2 = (np.ascontiguousarray(v, dtype=np.float32) for v in (a, b, s2))
-    out = np.zeros(tile_bytes(bits), dtype=np.uint8)
-    lib().kvo_pack_tile(_p(codes), _p(a), _p(b), _p(s2), kind, bits, _p(out))
+    out = np.zeros(tile_bytes(bits, aux), dtype=np.uint8)
+    lib().kvo_pack_tile(_p(codes), _p(a), _p(b), _p(s2), kind, bits, aux, _p(out))
     return out
 
 
-def unpack_tile(tile, kind: int, bits: int):
+def unpack_tile(tile, kind: int, bits: int, aux: int = 0):
     tile = np.ascontiguousarray(tile, dtype=np.uint8)
     codes = np.zeros((G, D), dtype=np.uint8)
     a, b, s2 = (np.zeros(128, dtype=np.float32) for _ in range(3))
-    lib().kvo_unpack_tile(_p(tile), kind, bits, _p(codes), _p(a), _p(b), _p(s2))
+    lib().kvo_unpack_tile(_p(tile), kind, bits, aux, _p(codes), _p(a), _p(b), _p(s2))
     return codes, a, b, s2
 
 
-def dequantize_tile(tile, kind: int, bits: int) -> np.ndarray:
+def dequantize_tile(tile, kind: int, bits: int, aux: int = 0) -> np.ndarray:
     tile = np.ascontiguousarray(tile, dtype=np.uint8)
     X = np.zeros((G, D))
-    lib().kvo_dequantize_tile(_p(tile), kind, bits, _p(X))
+    lib().kvo_dequantize_tile(_p(tile), kind, bits, aux, _p(X))
     return X
+
+
+def e4m3_decode(v: int) -> float:
+    return float(lib().kvo_e4m3_to_double(int(v)))
+
+
+def e4m3_encode(x: float, round_up: bool = False) -> int:
+    return int(lib().kvo_e4m3_from_double(float(x), int(round_up)))
+
+
+def fp16_decode(h: int) -> float:
+    return float(lib().kvo_fp16_to_double(int(h)))
+
+
+def fp16_encode(x: float) -> int:
+    return int(lib().kvo_fp16_from_double(float(x)))
 
 
 def quantize_tiles(x: np.ndarray, kind: int, params: Params = Params()) -> np.ndarray:
@@ -252,7 +284,7 @@ def quantize_tiles(x: np.ndarray, kind: int, params: Params = Params()) -> np.nd
     assert T % G == 0 and x.shape[-1] == D
     n_outer = int(np.prod(lead)) if lead else 1
     n_inner = T // G
-    tb = tile_bytes(params.bits)
+    tb = tile_bytes(params.bits, params.aux)
     out = np.zeros(lead + (n_inner, tb), dtype=np.uint8)
     pc = params.c()
     lib().kvo_quantize_tiles(_p(x), dtype, n_outer, n_inner, T * D, G * D, D, kind, ctypes.byref(pc), _p(out),
@@ -267,9 +299,10 @@ def quantize_tiles(x: np.ndarray, kind: int, params: Params = Params()) -> np.nd
 class HostCache:
     """Host copy of the cache in the shared layout (numpy arrays; bf16 held as uint16)."""
 
-    def __init__(self, batch, n_kv, max_blocks, bits=2, n_sink=0):
-        tb = tile_bytes(bits)
+    def __init__(self, batch, n_kv, max_blocks, bits=2, n_sink=0, aux=0):
+        tb = tile_bytes(bits, aux)
         self.batch, self.n_kv, self.max_blocks, self.bits, self.n_sink = batch, n_kv, max_blocks, bits, n_sink
+        self.aux = aux
         self.k_body = np.zeros((batch, n_kv, max_blocks, tb), dtype=np.uint8)
         self.v_body = np.zeros((batch, n_kv, max_blocks, tb), dtype=np.uint8)
         self.k_resid = np.zeros((batch, n_kv, G, D), dtype=np.uint16)
@@ -279,7 +312,7 @@ class HostCache:
         self.seq_len = np.zeros(batch, dtype=np.int32)
 
     def c(self) -> _Cache:
-        return _Cache(self.batch, self.n_kv, self.max_blocks, self.n_sink, self.bits,
+        return _Cache(self.batch, self.n_kv, self.max_blocks, self.n_sink, self.bits, self.aux,
                       self.k_body.ctypes.data, self.v_body.ctypes.data, self.k_resid.ctypes.data,
                       self.v_resid.ctypes.data, self.k_sink.ctypes.data, self.v_sink.ctypes.data,
                       self.seq_len.ctypes.data)
@@ -313,7 +346,7 @@ def decode(cache: HostCache, q: np.ndarray, scale: float) -> np.ndarray:
 
 def append(cache: HostCache, k_new: np.ndarray, v_new: np.ndarray, params: Params = Params()) -> int:
     """Append one bf16 token per (sequence, kv head); flushes full residuals into the body."""
-    assert params.bits == cache.bits
+    assert params.bits == cache.bits and params.aux == cache.aux
     k_new = np.ascontiguousarray(k_new, dtype=np.uint16)
     v_new = np.ascontiguousarray(v_new, dtype=np.uint16)
     cc = cache.c()

@@ -14,7 +14,9 @@
  * tile format is implemented here a second time, from its written description.
  *
  * Every floating-point step runs in double precision.  Values that the format stores in
- * fp32 (the three auxiliary vectors) are rounded once, to nearest-even, when stored.
+ * fp32 (the three auxiliary vectors) are rounded once, to nearest-even, when stored.  The
+ * compact format (App. D "Effective memory overhead": two FP8 scales and one FP16 zero point
+ * per group) rounds them to OCP E4M3 and IEEE binary16 instead, see kvo_quantize_tile.
  *
  * Parity pins for each function live in tests/test_oracle_*.py.  The constants c_min and
  * c_max of Algorithm 1 are not given numerically by the paper (parity unpinned; 1e-8 and
@@ -37,6 +39,8 @@ typedef struct {
     double log_lo, log_hi; /* clamp of the cumulative log-scales: -0.3 and 10.0 in Algorithm 1 */
     double imb_floor;    /* floor on min variance inside Imb(): 1e-8 in Algorithm 1 */
     int32_t ddof;        /* variance estimator: 1 (unbiased) by default */
+    int32_t aux;         /* stored aux format: 0 = three fp32 vectors, 1 = compact (E4M3 a and s2,
+                            binary16 b) */
 } kvo_params;
 
 /* ------------------------------------------------------------------------------------------
@@ -58,6 +62,68 @@ uint16_t kvo_double_to_bf16(double x) {
     uint32_t lsb = (u >> 16) & 1u;
     u += 0x7FFFu + lsb;
     return (uint16_t)(u >> 16);
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Narrow formats of the compact aux (App. D: "two FP8 scales ... and one FP16 zero-point").
+ *   E4M3 (the OCP 8-bit floating-point format E4M3): sign, 4 exponent bits with bias 7, 3
+ *   mantissa bits.  Exponent field 0 holds the subnormals m * 2^-9; there are no infinities and
+ *   the pattern with all exponent and mantissa bits set is NaN, so the largest finite value is
+ *   1.75 * 2^8 = 448.  Only positive values are stored here (scales).
+ *   binary16 (IEEE 754): 5 exponent bits with bias 15, 10 mantissa bits, subnormals
+ *   m * 2^-24, largest finite 65504.
+ * Encoding rounds on the grid of the binade of x (spacing 2^(e - mantissa bits), subnormal
+ * spacing below the smallest normal): to nearest with ties to the even grid point, or upward.
+ * Values beyond the largest finite one saturate to it.
+ * ------------------------------------------------------------------------------------------ */
+double kvo_e4m3_to_double(uint8_t v) {
+    const int e = (v >> 3) & 15, m = v & 7;
+    const double mag = e == 0 ? ldexp((double)m, -9) : ldexp(1.0 + m / 8.0, e - 7);
+    return (v & 0x80) ? -mag : mag;
+}
+
+uint8_t kvo_e4m3_from_double(double x, int round_up) {
+    if (!(x > 0.0)) return 0;
+    if (x >= 448.0) return 0x7E; /* exponent field 15, mantissa 6: 448 */
+    int ex;
+    frexp(x, &ex); /* x = f * 2^ex, f in [0.5, 1): binade [2^(ex-1), 2^ex) */
+    int E = ex - 1;
+    if (E < -6) E = -6; /* subnormal grid spacing 2^-9 */
+    const double step = ldexp(1.0, E - 3);
+    double q = x / step; /* exact: step is a power of two */
+    q = round_up ? ceil(q) : nearbyint(q);
+    const double v = q * step; /* <= 448: 448 is a grid point */
+    if (v < ldexp(1.0, -6)) return (uint8_t)q; /* subnormal (or zero) */
+    int ev;
+    frexp(v, &ev);
+    const int Ev = ev - 1;
+    const int m = (int)((v / ldexp(1.0, Ev) - 1.0) * 8.0);
+    return (uint8_t)(((Ev + 7) << 3) | m);
+}
+
+double kvo_fp16_to_double(uint16_t h) {
+    const int e = (h >> 10) & 31, m = h & 1023;
+    const double mag = e == 0 ? ldexp((double)m, -24) : ldexp(1.0 + m / 1024.0, e - 15);
+    return (h & 0x8000) ? -mag : mag;
+}
+
+uint16_t kvo_fp16_from_double(double x) {
+    const uint16_t sign = x < 0.0 ? 0x8000 : 0;
+    const double ax = fabs(x);
+    if (ax >= 65504.0) return sign | 0x7BFF;
+    if (ax == 0.0) return sign;
+    int ex;
+    frexp(ax, &ex);
+    int E = ex - 1;
+    if (E < -14) E = -14;
+    const double step = ldexp(1.0, E - 10);
+    const double v = nearbyint(ax / step) * step;
+    if (v < ldexp(1.0, -14)) return sign | (uint16_t)(v / ldexp(1.0, -24));
+    int ev;
+    frexp(v, &ev);
+    const int Ev = ev - 1;
+    const int m = (int)((v / ldexp(1.0, Ev) - 1.0) * 1024.0);
+    return sign | (uint16_t)(((Ev + 15) << 10) | m);
 }
 
 /* ------------------------------------------------------------------------------------------
@@ -225,12 +291,66 @@ void kvo_rtn_group(const double *x, int n, int stride, int bits, uint8_t *codes,
  *        values: a[t] = s_t * S_r*[t],  b[t] = mn_t * S_r*[t],  s2[c] = S_c*[c]
  *      so that the dequantized rotated tile is  (code * a + b) * s2.
  * Outputs: codes[128*128] token-major; a, b, s2 rounded to fp32.
+ *
+ * Compact aux (p->aux == 1): the stored values are narrow, so they are rounded first and the
+ * codes are computed against the stored values ("absorb, then round"):
+ *   s2  = E4M3 nearest of the other-axis scale (kept within [2^-6, 448]);
+ *   z   = T / s2 along the other axis (= B times the group-axis Sinkhorn scale: RTN of a group
+ *         does not depend on a common factor, so that scale is absorbed exactly);
+ *   per group: mn, mx of z, step = (mx - mn) / (2^bits - 1) (1 when mx == mn),
+ *   a   = E4M3 of step rounded upward (so [b, b + qmax * a] covers the group), b = binary16
+ *         nearest of mn, u = (z - b) / a, code = clamp(round-half-even(u), 0, qmax).
+ * The dequantized value (code * a + b) * s2 then keeps the RTN error bound a * s2 / 2 (plus the
+ * rounding of b).
  * Optional debug outputs (NULL to skip): T_out[128*128], Bal_out[128*128], u_out[128*128]
- * (token-major unrounded quotients), Sc_out[128], Sr_out[128], imb_hist[K+1], best_iter.
+ * (token-major unrounded quotients), Sc_out[128], Sr_out[128], imb_hist[K+1], best_iter,
+ * pre_out[3*128]: a, b, s2 before their rounding to the stored format.
  * ------------------------------------------------------------------------------------------ */
+static void quantize_compact(const double *T, const double *Sc, const double *Sr, int kind, int bits,
+                             uint8_t *codes, float *a, float *b, float *s2, double *u_out, double *pre_out) {
+    const double qmax = (double)((1 << bits) - 1);
+    const double *So = kind == KVO_KEYS ? Sr : Sc; /* other-axis scale: per token for keys */
+    double s2q[128];
+    for (int i = 0; i < 128; ++i) {
+        const double v = clampd(So[i], ldexp(1.0, -6), 448.0);
+        s2q[i] = kvo_e4m3_to_double(kvo_e4m3_from_double(v, 0));
+        s2[i] = (float)s2q[i];
+        if (pre_out) pre_out[256 + i] = So[i];
+    }
+    double z[128];
+    for (int g = 0; g < 128; ++g) { /* group: channel g (keys) or token g (values) */
+        double mn = INFINITY, mx = -INFINITY;
+        for (int i = 0; i < 128; ++i) { /* i: token (keys) or channel (values) */
+            const double x = kind == KVO_KEYS ? T[(size_t)i * D + g] : T[(size_t)g * D + i];
+            z[i] = x / s2q[i];
+            mn = fmin(mn, z[i]);
+            mx = fmax(mx, z[i]);
+        }
+        double step = (mx - mn) / qmax;
+        if (step == 0.0) step = 1.0;
+        const double aq = kvo_e4m3_to_double(kvo_e4m3_from_double(step, 1));
+        const double bq = kvo_fp16_to_double(kvo_fp16_from_double(mn));
+        a[g] = (float)aq;
+        b[g] = (float)bq;
+        if (pre_out) {
+            pre_out[g] = step;
+            pre_out[128 + g] = mn;
+        }
+        for (int i = 0; i < 128; ++i) {
+            const double u = (z[i] - bq) / aq;
+            double q = nearbyint(u);
+            if (q < 0.0) q = 0.0;
+            if (q > qmax) q = qmax;
+            const size_t at = kind == KVO_KEYS ? (size_t)i * D + g : (size_t)g * D + i;
+            codes[at] = (uint8_t)q;
+            if (u_out) u_out[at] = u;
+        }
+    }
+}
+
 void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *codes, float *a, float *b,
                        float *s2, double *T_out, double *Bal_out, double *u_out, double *Sc_out, double *Sr_out,
-                       double *imb_hist, int *best_iter) {
+                       double *imb_hist, int *best_iter, double *pre_out) {
     double *T = malloc((size_t)G * D * sizeof(double));
     double *Bal = malloc((size_t)G * D * sizeof(double));
     double Sc[D], Sr[G];
@@ -238,7 +358,9 @@ void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *
     for (int t = 0; t < G; ++t) kvo_hadamard128(T + (size_t)t * D);
     kvo_varn(T, G, D, p, Sc, Sr, Bal, imb_hist, NULL, NULL, best_iter);
 
-    if (kind == KVO_KEYS) {
+    if (p->aux == 1) {
+        quantize_compact(T, Sc, Sr, kind, p->bits, codes, a, b, s2, u_out, pre_out);
+    } else if (kind == KVO_KEYS) {
         for (int c = 0; c < D; ++c) {
             double mn, s;
             kvo_rtn_group(Bal + c, G, D, p->bits, codes + c, D, &mn, &s, u_out ? u_out + c : NULL, D);
@@ -268,7 +390,8 @@ void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *
  * Packed tile format (this library's own storage format; the paper fixes only what is
  * stored per group, App. D).  A tile is
  *     codes region: bits * 2048 bytes (128 x 128 codes of `bits` bits)
- *     a[128], b[128], s2[128]: little-endian binary32, in index order (token or channel)
+ *     aux 0: a[128], b[128], s2[128]: little-endian binary32, in index order (token or channel)
+ *     aux 1: b[128] little-endian binary16, then a[128] and s2[128] as E4M3 bytes
  * Codes are grouped in "units" of 16 codes; unit u occupies bits/2 consecutive 32-bit
  * little-endian words starting at word u * bits/2.  Inside a unit, code number e = 4*s + q
  * (s, q in 0..3) sits in word  s / (8/bits)  at bit  8*q + bits*(s % (8/bits)).
@@ -278,7 +401,7 @@ void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *
  *   values: unit = (sigma*64 + 16*((t % 16) / 4) + c % 16) * 8 + c / 16,
  *           e = 4*((t % 64) / 16) + t % 4
  * ------------------------------------------------------------------------------------------ */
-size_t kvo_tile_bytes(int bits) { return (size_t)bits * 2048 + 3 * 128 * sizeof(float); }
+size_t kvo_tile_bytes(int bits, int aux) { return (size_t)bits * 2048 + (aux == 1 ? 512 : 3 * 128 * 4); }
 
 static void code_location(int kind, int bits, int t, int c, size_t *word, int *shift) {
     int sigma = t / 64;
@@ -300,7 +423,7 @@ static void put_f32(uint8_t *dst, float v) { memcpy(dst, &v, 4); } /* host is li
 static float get_f32(const uint8_t *src) { float v; memcpy(&v, src, 4); return v; }
 
 void kvo_pack_tile(const uint8_t *codes, const float *a, const float *b, const float *s2, int kind, int bits,
-                   uint8_t *dst) {
+                   int aux, uint8_t *dst) {
     size_t ncode_bytes = (size_t)bits * 2048;
     uint32_t *words = calloc(ncode_bytes / 4, sizeof(uint32_t));
     for (int t = 0; t < G; ++t)
@@ -317,14 +440,23 @@ void kvo_pack_tile(const uint8_t *codes, const float *a, const float *b, const f
         dst[4 * w + 3] = (uint8_t)(words[w] >> 24);
     }
     for (int i = 0; i < 128; ++i) {
-        put_f32(dst + ncode_bytes + 4 * i, a[i]);
-        put_f32(dst + ncode_bytes + 512 + 4 * i, b[i]);
-        put_f32(dst + ncode_bytes + 1024 + 4 * i, s2[i]);
+        if (aux == 1) { /* the values are already on the narrow grids: exact re-encoding */
+            const uint16_t h = kvo_fp16_from_double((double)b[i]);
+            dst[ncode_bytes + 2 * i] = (uint8_t)h;
+            dst[ncode_bytes + 2 * i + 1] = (uint8_t)(h >> 8);
+            dst[ncode_bytes + 256 + i] = kvo_e4m3_from_double((double)a[i], 0);
+            dst[ncode_bytes + 384 + i] = kvo_e4m3_from_double((double)s2[i], 0);
+        } else {
+            put_f32(dst + ncode_bytes + 4 * i, a[i]);
+            put_f32(dst + ncode_bytes + 512 + 4 * i, b[i]);
+            put_f32(dst + ncode_bytes + 1024 + 4 * i, s2[i]);
+        }
     }
     free(words);
 }
 
-void kvo_unpack_tile(const uint8_t *src, int kind, int bits, uint8_t *codes, float *a, float *b, float *s2) {
+void kvo_unpack_tile(const uint8_t *src, int kind, int bits, int aux, uint8_t *codes, float *a, float *b,
+                     float *s2) {
     size_t ncode_bytes = (size_t)bits * 2048;
     const uint32_t mask = (1u << bits) - 1u;
     for (int t = 0; t < G; ++t)
@@ -337,9 +469,16 @@ void kvo_unpack_tile(const uint8_t *src, int kind, int bits, uint8_t *codes, flo
             codes[(size_t)t * D + c] = (uint8_t)((word >> sh) & mask);
         }
     for (int i = 0; i < 128; ++i) {
-        if (a) a[i] = get_f32(src + ncode_bytes + 4 * i);
-        if (b) b[i] = get_f32(src + ncode_bytes + 512 + 4 * i);
-        if (s2) s2[i] = get_f32(src + ncode_bytes + 1024 + 4 * i);
+        if (aux == 1) {
+            const uint16_t h = (uint16_t)(src[ncode_bytes + 2 * i] | src[ncode_bytes + 2 * i + 1] << 8);
+            if (b) b[i] = (float)kvo_fp16_to_double(h);
+            if (a) a[i] = (float)kvo_e4m3_to_double(src[ncode_bytes + 256 + i]);
+            if (s2) s2[i] = (float)kvo_e4m3_to_double(src[ncode_bytes + 384 + i]);
+        } else {
+            if (a) a[i] = get_f32(src + ncode_bytes + 4 * i);
+            if (b) b[i] = get_f32(src + ncode_bytes + 512 + 4 * i);
+            if (s2) s2[i] = get_f32(src + ncode_bytes + 1024 + 4 * i);
+        }
     }
 }
 
@@ -349,10 +488,10 @@ void kvo_unpack_tile(const uint8_t *src, int kind, int bits, uint8_t *codes, flo
  *            values Xr[t][c] = (code * a[t] + b[t]) * s2[c]
  *   then X[t,:] = H Xr[t,:] (H is its own inverse).  Out: X[128*128] token-major.
  */
-void kvo_dequantize_tile(const uint8_t *src, int kind, int bits, double *X) {
+void kvo_dequantize_tile(const uint8_t *src, int kind, int bits, int aux, double *X) {
     uint8_t *codes = malloc((size_t)G * D);
     float a[128], b[128], s2[128];
-    kvo_unpack_tile(src, kind, bits, codes, a, b, s2);
+    kvo_unpack_tile(src, kind, bits, aux, codes, a, b, s2);
     for (int t = 0; t < G; ++t) {
         for (int c = 0; c < D; ++c) {
             double q = (double)codes[(size_t)t * D + c];
@@ -374,8 +513,8 @@ void kvo_quantize_pack(const void *x, int dtype, int64_t token_stride, int kind,
         for (int c = 0; c < D; ++c)
             X[(size_t)t * D + c] = dtype == 0 ? (double)((const float *)x)[t * token_stride + c]
                                               : kvo_bf16_to_double(((const uint16_t *)x)[t * token_stride + c]);
-    kvo_quantize_tile(X, kind, p, codes, a, b, s2, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
-    kvo_pack_tile(codes, a, b, s2, kind, p->bits, dst);
+    kvo_quantize_tile(X, kind, p, codes, a, b, s2, NULL, NULL, NULL, NULL, NULL, NULL, NULL, NULL);
+    kvo_pack_tile(codes, a, b, s2, kind, p->bits, p->aux, dst);
     free(X);
     free(codes);
 }
@@ -388,7 +527,7 @@ void kvo_quantize_pack(const void *x, int dtype, int64_t token_stride, int kind,
 void kvo_quantize_tiles(const void *x, int dtype, int64_t n_outer, int64_t n_inner, int64_t x_outer, int64_t x_inner,
                         int64_t token_stride, int kind, const kvo_params *p, uint8_t *out, int64_t out_outer,
                         int64_t out_inner) {
-    const size_t tb = kvo_tile_bytes(p->bits);
+    const size_t tb = kvo_tile_bytes(p->bits, p->aux);
     const size_t esz = dtype == 0 ? 4 : 2;
 #pragma omp parallel for collapse(2) schedule(dynamic)
     for (int64_t i = 0; i < n_outer; ++i)
@@ -410,7 +549,7 @@ void kvo_quantize_tiles(const void *x, int dtype, int64_t n_outer, int64_t n_inn
  *   seq_len:          [batch] int32
  * ------------------------------------------------------------------------------------------ */
 typedef struct {
-    int32_t batch, n_kv, max_blocks, n_sink, bits;
+    int32_t batch, n_kv, max_blocks, n_sink, bits, aux;
     uint8_t *k_body, *v_body;
     uint16_t *k_resid, *v_resid, *k_sink, *v_sink;
     int32_t *seq_len;
@@ -438,7 +577,7 @@ void kvo_gather_stream(const kvo_cache *cc, int32_t bi, int32_t kh, double *K, d
     int32_t ns, nb, nr;
     region_sizes(cc, len, &ns, &nb, &nr);
     const size_t stream = (size_t)bi * cc->n_kv + kh;
-    const size_t tb = kvo_tile_bytes(cc->bits);
+    const size_t tb = kvo_tile_bytes(cc->bits, cc->aux);
     int32_t t = 0;
     for (int32_t i = 0; i < ns; ++i, ++t)
         for (int c = 0; c < D; ++c) {
@@ -446,8 +585,10 @@ void kvo_gather_stream(const kvo_cache *cc, int32_t bi, int32_t kh, double *K, d
             V[(size_t)t * D + c] = kvo_bf16_to_double(cc->v_sink[(stream * cc->n_sink + i) * D + c]);
         }
     for (int32_t blk = 0; blk < nb; ++blk, t += G) {
-        kvo_dequantize_tile(cc->k_body + (stream * cc->max_blocks + blk) * tb, KVO_KEYS, cc->bits, K + (size_t)t * D);
-        kvo_dequantize_tile(cc->v_body + (stream * cc->max_blocks + blk) * tb, KVO_VALUES, cc->bits, V + (size_t)t * D);
+        kvo_dequantize_tile(cc->k_body + (stream * cc->max_blocks + blk) * tb, KVO_KEYS, cc->bits, cc->aux,
+                            K + (size_t)t * D);
+        kvo_dequantize_tile(cc->v_body + (stream * cc->max_blocks + blk) * tb, KVO_VALUES, cc->bits, cc->aux,
+                            V + (size_t)t * D);
     }
     for (int32_t i = 0; i < nr; ++i, ++t)
         for (int c = 0; c < D; ++c) {
@@ -513,7 +654,8 @@ void kvo_decode(const kvo_cache *cc, int32_t n_q, const void *q, int dtype, doub
  * emptied.  Returns 0, or -3 if a sequence has no free body slot for the flush.
  */
 int kvo_append(kvo_cache *cc, const uint16_t *k_new, const uint16_t *v_new, const kvo_params *p) {
-    const size_t tb = kvo_tile_bytes(cc->bits);
+    if (p->bits != cc->bits || p->aux != cc->aux) return -1;
+    const size_t tb = kvo_tile_bytes(cc->bits, cc->aux);
     for (int32_t bi = 0; bi < cc->batch; ++bi) {
         int32_t len = cc->seq_len[bi];
         int32_t ns, nb, nr;
