@@ -28,15 +28,27 @@
  *
  * Packed tile (the library's storage format; the paper fixes only what is stored per group):
  *   bytes [0, bits*2048)          128 x 128 codes of `bits` bits (layout below)
- *   next 512 bytes                a[128]  fp32   keys: RTN scale of channel c times its
- *                                                 Sinkhorn channel scale; values: of token t
- *   next 512 bytes                b[128]  fp32   the matching offset (group minimum times
- *                                                 the same Sinkhorn scale)
- *   next 512 bytes                s2[128] fp32   second scale: keys per token, values per
- *                                                 channel (the other Sinkhorn scale)
- *   Dequantized rotated tile: keys (code[t][c]*a[c] + b[c]) * s2[t]; values
+ *   then the aux, in one of two formats (kvarn_params.aux_format):
+ *   KVARN_AUX_F32:
+ *     512 bytes   a[128]  fp32   keys: RTN scale of channel c times its Sinkhorn channel
+ *                                scale; values: of token t
+ *     512 bytes   b[128]  fp32   the matching offset (group minimum times the same scale)
+ *     512 bytes   s2[128] fp32   second scale: keys per token, values per channel (the other
+ *                                Sinkhorn scale)
+ *     Tile size 5632 bytes at 2 bits (2.75 bits/element), 9728 at 4 bits.
+ *   KVARN_AUX_COMPACT (App. D, "Effective memory overhead": two FP8 scales and one FP16 zero
+ *   point per group of 128 elements):
+ *     256 bytes   b[128]  IEEE binary16, little-endian
+ *     128 bytes   a[128]  OCP E4M3 (4-bit exponent, bias 7, 3-bit mantissa, largest 448)
+ *     128 bytes   s2[128] OCP E4M3
+ *     s2 is rounded to nearest first and the tile is quantized against the stored s2; a is the
+ *     RTN step rounded upward (the stored range covers the group), b the nearest binary16 of
+ *     the group minimum, and codes are chosen for the stored a and b.  Scales are kept within
+ *     [2^-6, 448] and b within +-65504.  Tile size 4608 bytes at 2 bits (2.25 bits/element),
+ *     8704 at 4 bits.
+ *   Dequantized rotated tile, both formats: keys (code[t][c]*a[c] + b[c]) * s2[t]; values
  *   (code[t][c]*a[t] + b[t]) * s2[c]; un-rotate each token with the orthonormal Hadamard
- *   matrix.  Tile size: 5632 bytes at 2 bits (2.75 bits/element), 9728 at 4 bits.
+ *   matrix.
  *   Code layout: codes form units of 16; unit u is bits/2 little-endian 32-bit words starting
  *   at word u*bits/2.  Code e = 4*s + q (s, q in 0..3) of a unit sits in word s/(8/bits) of
  *   the unit, at bit 8*q + bits*(s % (8/bits)).  For token t, channel c, sigma = t/64:
@@ -79,14 +91,16 @@ typedef struct {
     float var_max;      /* c_max: 1e8 (the paper gives no values for c_min, c_max)      */
     float log_lo;       /* clamp of the cumulative log-scales: -0.3 (Algorithm 1)       */
     float log_hi;       /* 10.0 (Algorithm 1)                                           */
+    int32_t aux_format; /* KVARN_AUX_F32 (default) or KVARN_AUX_COMPACT                  */
 } kvarn_params;
+typedef enum { KVARN_AUX_F32 = 0, KVARN_AUX_COMPACT = 1 } kvarn_aux_format;
 /* Accepted ranges (else KVARN_EINVAL): 1e-30 <= var_min <= var_max <= 1e30 and
  * -40 <= log_lo <= log_hi <= 40, which keeps every scale exp(+-L) and every log of a clamped
  * variance inside the normal fp32 range. */
 
 /* The cache of `batch` sequences with n_kv kv heads each (a model's layers may be folded
  * into batch).  Device buffers, all caller-allocated (sizes from kvarn_cache_sizes):
- *   k_body, v_body   [batch][n_kv][max_blocks] packed tiles of kvarn_tile_bytes(bits)
+ *   k_body, v_body   [batch][n_kv][max_blocks] packed tiles of kvarn_tile_bytes(p)
  *   k_resid, v_resid [batch][n_kv][128][128]    bf16, tokens as given (unrotated)
  *   k_sink, v_sink   [batch][n_kv][n_sink][128] bf16, or NULL when n_sink == 0
  *   seq_len          [batch] int32: tokens held by each sequence (all regions)
@@ -104,12 +118,13 @@ typedef struct {
     uint32_t *err_word;
 } kvarn_cache;
 
-/* Fill `p` with the defaults for `bits` (2 or 4).  Returns KVARN_EINVAL for a null `p`,
- * KVARN_EUNSUPPORTED for other bit widths. */
+/* Fill `p` with the defaults for `bits` (2 or 4; fp32 aux).  Returns KVARN_EINVAL for a null
+ * `p`, KVARN_EUNSUPPORTED for other bit widths. */
 KVARN_API int kvarn_params_init(kvarn_params *p, int32_t bits);
 
-/* Bytes of one packed tile: 5632 for bits = 2, 9728 for bits = 4, 0 otherwise. */
-KVARN_API size_t kvarn_tile_bytes(int32_t bits);
+/* Bytes of one packed tile for p's bits and aux format (5632 / 9728 with fp32 aux, 4608 / 8704
+ * compact); 0 for invalid parameters. */
+KVARN_API size_t kvarn_tile_bytes(const kvarn_params *p);
 
 /* Byte sizes of the seven cache buffers, in the order k_body, v_body, k_resid, v_resid,
  * k_sink, v_sink, seq_len.  Returns KVARN_EINVAL for null pointers or non-positive sizes. */
@@ -122,7 +137,7 @@ KVARN_API int kvarn_cache_sizes(const kvarn_params *p, int32_t batch, int32_t n_
  *           it at + t*x_token_stride; its 128 channels are contiguous.  dtype fp32 or bf16.
  *           The input is unrotated: the library applies the Hadamard rotation.
  *   out     tile (i, j) is written at byte out + (i*out_outer_stride + j*out_inner_stride) *
- *           kvarn_tile_bytes(bits) (strides counted in tiles).
+ *           kvarn_tile_bytes(p) (strides counted in tiles).
  *   best_iter  optional [n_outer*n_inner] int32 (row-major over (i, j)): the VarN iteration
  *           whose scales were kept (0 = the initial unit scales); NULL to skip.
  * Strides must be non-negative, x_token_stride >= 128; x, and every x stride times the

@@ -51,7 +51,8 @@ class _Params(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("varn_iters", ctypes.c_int32),
                 ("c_min", ctypes.c_double), ("c_max", ctypes.c_double),
                 ("log_lo", ctypes.c_double), ("log_hi", ctypes.c_double),
-                ("imb_floor", ctypes.c_double), ("ddof", ctypes.c_int32), ("aux", ctypes.c_int32)]
+                ("imb_floor", ctypes.c_double), ("ddof", ctypes.c_int32), ("aux", ctypes.c_int32),
+                ("force_best", ctypes.c_int32)]
 
 
 class _Cache(ctypes.Structure):
@@ -70,7 +71,8 @@ class Params:
     log_lo/log_hi = -0.3/10.0 and imb_floor = 1e-8 are printed in Algorithm 1; K = 8 is the
     iteration count of the runtime experiment (Sec. 4.2); c_min/c_max are unstated (unpinned).
     aux selects the stored aux format: 0 = fp32 vectors, 1 = compact (App. D: E4M3 scales,
-    binary16 offset).
+    binary16 offset).  force_best (test use) keeps iteration k's scales instead of Algorithm 1's
+    selection: the outcome had k won a near-tie of Imb.
     """
     bits: int = 2
     varn_iters: int = 8
@@ -81,10 +83,11 @@ class Params:
     imb_floor: float = 1e-8
     ddof: int = 1
     aux: int = 0
+    force_best: int = -1
 
     def c(self) -> _Params:
         return _Params(self.bits, self.varn_iters, self.c_min, self.c_max, self.log_lo, self.log_hi,
-                       self.imb_floor, self.ddof, self.aux)
+                       self.imb_floor, self.ddof, self.aux, self.force_best)
 
 
 _lib = None

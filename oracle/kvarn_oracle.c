@@ -41,6 +41,8 @@ typedef struct {
     int32_t ddof;        /* variance estimator: 1 (unbiased) by default */
     int32_t aux;         /* stored aux format: 0 = three fp32 vectors, 1 = compact (E4M3 a and s2,
                             binary16 b) */
+    int32_t force_best;  /* -1: Algorithm 1's selection.  k in 0..K: keep iteration k's scales
+                            instead (test use: the outcome had iteration k won a near-tie) */
 } kvo_params;
 
 /* ------------------------------------------------------------------------------------------
@@ -231,7 +233,8 @@ void kvo_varn(const double *T, int R, int C, const kvo_params *p, double *Sc, do
         current_tile(T, R, C, Lc, Lr, Cur);
 
         double I_curr = kvo_imbalance(Cur, R, C, p->ddof, p->imb_floor);
-        if (I_curr <= I_best) { /* "<=": a later iteration wins a tie */
+        const int take = p->force_best >= 0 ? k == p->force_best : I_curr <= I_best;
+        if (take) { /* "<=": a later iteration wins a tie */
             I_best = I_curr;
             for (int c = 0; c < C; ++c) Sc[c] = exp(Lc[c]);
             for (int r = 0; r < R; ++r) Sr[r] = exp(Lr[r]);

@@ -14,6 +14,7 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 int check_params(const kvarn_params* p) {
     if (!p) return KVARN_EINVAL;
     if (p->bits != 2 && p->bits != 4) return KVARN_EUNSUPPORTED;
+    if (p->aux_format != KVARN_AUX_F32 && p->aux_format != KVARN_AUX_COMPACT) return KVARN_EUNSUPPORTED;
     if (p->varn_iters < 0 || p->varn_iters > 64) return KVARN_EINVAL;
     if (p->n_sink < 0 || p->n_sink > 1024) return KVARN_EINVAL;
     // ranges that keep exp(+-L) and log(v) of the quantizer inside the normal fp32 range
@@ -23,7 +24,8 @@ int check_params(const kvarn_params* p) {
 }
 
 QParams qparams(const kvarn_params* p) {
-    return QParams{p->bits, p->varn_iters, p->var_min, p->var_max, p->log_lo, p->log_hi};
+    return QParams{p->bits, p->varn_iters, p->var_min, p->var_max, p->log_lo, p->log_hi,
+                   p->aux_format == KVARN_AUX_COMPACT ? 1 : 0};
 }
 
 int check_cache(const kvarn_params* p, const kvarn_cache* c) {
@@ -54,17 +56,20 @@ int kvarn_params_init(kvarn_params* p, int32_t bits) {
     p->var_max = 1e8f;
     p->log_lo = -0.3f;
     p->log_hi = 10.0f;
+    p->aux_format = KVARN_AUX_F32;
     return KVARN_OK;
 }
 
-size_t kvarn_tile_bytes(int32_t bits) { return (bits == 2 || bits == 4) ? tile_bytes(bits) : 0; }
+size_t kvarn_tile_bytes(const kvarn_params* p) {
+    return check_params(p) ? 0 : tile_bytes(p->bits, p->aux_format == KVARN_AUX_COMPACT);
+}
 
 int kvarn_cache_sizes(const kvarn_params* p, int32_t batch, int32_t n_kv, int32_t max_blocks, size_t sizes[7]) {
     int st = check_params(p);
     if (st) return st;
     if (!sizes || batch <= 0 || n_kv <= 0 || max_blocks < 0) return KVARN_EINVAL;
     const size_t streams = (size_t)batch * n_kv;
-    sizes[0] = sizes[1] = streams * max_blocks * tile_bytes(p->bits);
+    sizes[0] = sizes[1] = streams * max_blocks * tile_bytes(p->bits, p->aux_format == KVARN_AUX_COMPACT);
     sizes[2] = sizes[3] = streams * kG * kD * sizeof(uint16_t);
     sizes[4] = sizes[5] = streams * (size_t)p->n_sink * kD * sizeof(uint16_t);
     sizes[6] = (size_t)batch * sizeof(int32_t);
@@ -150,8 +155,9 @@ int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int3
     const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
     const size_t need = decode_workspace_bytes(cache->batch, n_q, plan);
     if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return KVARN_EWORKSPACE;
-    hipError_t e = launch_decode(*cache, p->bits, p->n_sink, n_q, q, q_dtype == KVARN_BF16, out,
-                                 out_dtype == KVARN_BF16, sm_scale, plan, static_cast<float*>(workspace), stream);
+    hipError_t e = launch_decode(*cache, p->bits, p->aux_format == KVARN_AUX_COMPACT, p->n_sink, n_q, q,
+                                 q_dtype == KVARN_BF16, out, out_dtype == KVARN_BF16, sm_scale, plan,
+                                 static_cast<float*>(workspace), stream);
     return e == hipSuccess ? KVARN_OK : KVARN_EHIP;
 }
 

@@ -15,8 +15,10 @@ constexpr int kG = 128;  // tokens per quantization group / body tile
 constexpr float kInvSqrt128 = 0.08838834764831845f;
 constexpr float kLog2e = 1.4426950408889634f;
 
-__host__ __device__ inline size_t tile_bytes(int bits) { return (size_t)bits * 2048 + 3 * 128 * sizeof(float); }
+// aux bytes per tile: three fp32 vectors, or the compact binary16 b + E4M3 a + E4M3 s2
+__host__ __device__ inline size_t aux_bytes(int compact) { return compact ? 512 : 3 * 128 * sizeof(float); }
 __host__ __device__ inline size_t code_bytes(int bits) { return (size_t)bits * 2048; }
+__host__ __device__ inline size_t tile_bytes(int bits, int compact) { return code_bytes(bits) + aux_bytes(compact); }
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
@@ -33,6 +35,7 @@ struct QParams {
     int bits;
     int iters;
     float var_min, var_max, log_lo, log_hi;
+    int compact;  // aux format: 0 fp32, 1 compact
 };
 
 // Kernel launchers (defined in the .hip files; called by the host API).
@@ -54,7 +57,8 @@ struct DecodePlan {
 DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int n_sink, int max_blocks);
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan);
 
-hipError_t launch_decode(const kvarn_cache& c, int bits, int n_sink, int n_q, const void* q, bool q_bf16, void* out,
-                         bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws, hipStream_t stream);
+hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int n_sink, int n_q, const void* q, bool q_bf16,
+                         void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
+                         hipStream_t stream);
 
 }  // namespace kvarn

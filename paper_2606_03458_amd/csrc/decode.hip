@@ -58,6 +58,7 @@ struct DecodeArgs {
     void* out;
     int out_bf16;
     int n_kv, n_q, g, max_blocks, n_sink;
+    int compact;       // aux format of the body tiles: 0 fp32, 1 compact (binary16 b, E4M3 a and s2)
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
     int n_split, bps;  // body splits per stream and body tiles per split
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
@@ -104,6 +105,55 @@ __device__ __forceinline__ void digits4_2(uint32_t y0, uint32_t y1, uint32_t y2,
     const uint32_t t01 = perm(y1, y0, 0x05010400u), t23 = perm(y3, y2, 0x05010400u);
     d0 = perm(t23, t01, 0x05040100u) ^ 0x80808080u;
     d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
+}
+
+// The aux of one K tile and one V tile, as loaded by a wave: fp32 aux is 3 KB, three 16-byte
+// pieces per lane (pieces l, l + 64, l + 128 of K aux || V aux); compact aux is 1 KB, one piece
+// per lane (lanes 0-31 the K tile's 512 bytes, lanes 32-63 the V tile's).
+struct AuxRegs {
+    uint4 p0, p1, p2;
+};
+__device__ __forceinline__ void load_aux_regs(AuxRegs& r, const uint8_t* kt, const uint8_t* vt, size_t cb, int l,
+                                              int compact) {
+    if (compact) {
+        r.p0 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + (l & 31) * 16);
+    } else {
+        r.p0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
+        r.p1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + (l < 32 ? (64 + l) * 16 : (l - 32) * 16));
+        r.p2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
+    }
+}
+// Loaded aux -> fp32 rows a_K b_K s2_K a_V b_V s2_V in LDS.  A compact piece is 8 binary16
+// offsets (pieces 0-15 of a tile) or 16 E4M3 scales (pieces 16-23: a, 24-31: s2); both
+// conversions are exact.
+__device__ __forceinline__ void stage_aux(float (&aux)[6][kD], const AuxRegs& r, int l, int compact) {
+    if (!compact) {
+        reinterpret_cast<uint4*>(&aux[0][0])[l] = r.p0;
+        reinterpret_cast<uint4*>(&aux[0][0])[l + 64] = r.p1;
+        reinterpret_cast<uint4*>(&aux[0][0])[l + 128] = r.p2;
+        return;
+    }
+    const int part = l >> 5, p = l & 31;
+    const uint32_t w[4] = {r.p0.x, r.p0.y, r.p0.z, r.p0.w};
+    if (p < 16) {
+        float v[8];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            v[2 * k] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] & 0xFFFFu));
+            v[2 * k + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] >> 16));
+        }
+        float4* row = reinterpret_cast<float4*>(&aux[3 * part + 1][8 * p]);
+        row[0] = make_float4(v[0], v[1], v[2], v[3]);
+        row[1] = make_float4(v[4], v[5], v[6], v[7]);
+    } else {
+        float4* row = reinterpret_cast<float4*>(&aux[3 * part + (p < 24 ? 0 : 2)][16 * ((p - 16) & 7)]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+            const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[k], false);  // bytes 0, 1
+            const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[k], true);   // bytes 2, 3
+            row[k] = make_float4(lo[0], lo[1], hi[0], hi[1]);
+        }
+    }
 }
 
 template <int GQ>
@@ -154,7 +204,7 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     const int blk0 = split * a.bps;
     const int blk1 = last ? nbody : min(blk0 + a.bps, nbody);  // the last split takes any excess
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;    // first query head of the group
-    const size_t tb = tile_bytes(BITS), cb = code_bytes(BITS);
+    const size_t tb = tile_bytes(BITS, a.compact), cb = code_bytes(BITS);
 
     float m_run = -INFINITY, l_run = 0.f;  // per head n; l_run is this lane's partial sum
     float orot[8][4];                      // head n, channel 16*mt + 4*G + i (rotated domain)
@@ -197,9 +247,9 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
         for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
 
         // Lane l's part of a tile: its K and V code units (32*WPU bytes per 64-token half) and
-        // one 16-byte piece of the 3 KB of aux (pieces l, l + 64, l + 128 of K aux || V aux).
-        uint4 kc[2][2 * WPU], vc[2][2 * WPU], ax0, ax1, ax2;
-        const int ax1_off = l < 32 ? (64 + l) * 16 : (l - 32) * 16;  // piece l + 64: K aux or V aux
+        // its pieces of the aux.
+        uint4 kc[2][2 * WPU], vc[2][2 * WPU];
+        AuxRegs ar;
         auto load_tile = [&](int blk) {
             const uint8_t* kt = a.k_body + ((size_t)stream * a.max_blocks + blk) * tb;
             const uint8_t* vt = a.v_body + ((size_t)stream * a.max_blocks + blk) * tb;
@@ -210,17 +260,13 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                     kc[s][k] = reinterpret_cast<const uint4*>(kt)[(s * 64 + l) * 2 * WPU + k];
                     vc[s][k] = reinterpret_cast<const uint4*>(vt)[(s * 64 + l) * 2 * WPU + k];
                 }
-            ax0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
-            ax1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + ax1_off);
-            ax2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
+            load_aux_regs(ar, kt, vt, cb, l, a.compact);
         };
         load_tile(blk0);
 
         for (int blk = blk0; blk < blk1; ++blk) {
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp
-            reinterpret_cast<uint4*>(&sm.aux[0][0])[l] = ax0;
-            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 64] = ax1;
-            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 128] = ax2;
+            stage_aux(sm.aux, ar, l, a.compact);
             uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -600,7 +646,7 @@ void k_decode4(DecodeArgs a) {
     const int blk0 = split * a.bps;
     const int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
-    const size_t tb = tile_bytes(BITS), cb = code_bytes(BITS);
+    const size_t tb = tile_bytes(BITS, a.compact), cb = code_bytes(BITS);
 
     float m_run[NH], l_run[NH];  // head 4*hg + G; l_run is this lane's partial sum
     float orot[NH][8];           // head 4*hg + G, channel 16*mt + n (rotated domain)
@@ -656,17 +702,11 @@ void k_decode4(DecodeArgs a) {
         // One register buffer per tile part, refilled as soon as its current contents are
         // consumed: the next tile's aux right after it is staged in LDS, its key codes right
         // after the QK products, its value codes right after the PV products.
-        uint4 kc[2][2 * WPU], vc[2][2 * WPU], ax0, ax1, ax2;
-        const int ax1_off = l < 32 ? (64 + l) * 16 : (l - 32) * 16;
+        uint4 kc[2][2 * WPU], vc[2][2 * WPU];
+        AuxRegs ar;
         auto tile_k = [&](int b_) { return a.k_body + ((size_t)stream * a.max_blocks + b_) * tb; };
         auto tile_v = [&](int b_) { return a.v_body + ((size_t)stream * a.max_blocks + b_) * tb; };
-        auto load_aux = [&](int b_) {
-            const uint8_t* kt = tile_k(b_);
-            const uint8_t* vt = tile_v(b_);
-            ax0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
-            ax1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + ax1_off);
-            ax2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
-        };
+        auto load_aux = [&](int b_) { load_aux_regs(ar, tile_k(b_), tile_v(b_), cb, l, a.compact); };
         auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -680,9 +720,7 @@ void k_decode4(DecodeArgs a) {
         for (int blk = blk0; blk < blk1; ++blk) {
             const bool more = blk + 1 < blk1;
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
-            reinterpret_cast<uint4*>(&sm.aux[0][0])[l] = ax0;
-            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 64] = ax1;
-            reinterpret_cast<uint4*>(&sm.aux[0][0])[l + 128] = ax2;
+            stage_aux(sm.aux, ar, l, a.compact);
             __syncthreads();
             if (more) load_aux(blk + 1);
             // offsets as ratios b / a: keys per channel, values per token
@@ -1064,9 +1102,11 @@ size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan) {
     return (size_t)batch * n_q * plan.n_split * kPart * sizeof(float);
 }
 
-hipError_t launch_decode(const kvarn_cache& c, int bits, int n_sink, int n_q, const void* q, bool q_bf16, void* out,
-                         bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws, hipStream_t stream) {
+hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int n_sink, int n_q, const void* q, bool q_bf16,
+                         void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
+                         hipStream_t stream) {
     DecodeArgs a;
+    a.compact = compact;
     a.k_body = static_cast<const uint8_t*>(c.k_body);
     a.v_body = static_cast<const uint8_t*>(c.v_body);
     a.k_resid = static_cast<const uint16_t*>(c.k_resid);

@@ -201,8 +201,34 @@ __device__ __forceinline__ float clampf(float v, float lo, float hi) { return fm
 __device__ __forceinline__ float ln_hw(float v) { return __builtin_amdgcn_logf(v) * 0.6931471805599453f; }
 __device__ __forceinline__ float exp_hw(float v) { return __builtin_amdgcn_exp2f(v * kLog2e); }
 
+// ---- narrow formats of the compact aux (App. D: two FP8 scales and one FP16 zero point) -----
+// OCP E4M3: 4-bit exponent with bias 7, 3-bit mantissa, subnormals m * 2^-9, largest 448.
+// Grid value of x > 0 on the E4M3 grid of its binade (spacing 2^(e-3), 2^-9 below 2^-6),
+// nearest with ties to even or upward, saturating at 448.  Scaling by powers of two is exact.
+__device__ __forceinline__ float e4m3_round(float x, bool up) {
+    if (x >= 448.f) return 448.f;
+    int ex;
+    frexpf(x, &ex);  // x in [2^(ex-1), 2^ex)
+    const int E = max(ex - 1, -6);
+    const float q = x * ldexpf(1.f, 3 - E);
+    return (up ? ceilf(q) : rintf(q)) * ldexpf(1.f, E - 3);
+}
+// Byte of a value on the E4M3 grid (0 <= v <= 448).
+__device__ __forceinline__ uint32_t e4m3_bits(float v) {
+    if (v < 0.015625f) return (uint32_t)(v * 512.f);  // subnormal: m * 2^-9
+    const uint32_t u = __float_as_uint(v);
+    return ((((u >> 23) & 255u) - 120u) << 3) | ((u >> 20) & 7u);  // exponent - 127 + 7
+}
+// Nearest binary16 (ties to even), saturating at +-65504; returns the value and its bits.
+__device__ __forceinline__ float fp16_round(float x, uint32_t& bits) {
+    const _Float16 h = (_Float16)fminf(fmaxf(x, -65504.f), 65504.f);
+    bits = __builtin_bit_cast(uint16_t, h);
+    return (float)h;
+}
+
 // Quantize one tile.  src: token t at src + t*tstride elements, channels contiguous (16-byte
 // aligned rows).  dst: the packed tile (16-byte aligned).
+template <bool COMPACT>
 __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int kind, const QParams& P, uint8_t* dst,
                               int32_t* best_out, QuantSmem& sm) {
     const Lane L;
@@ -321,10 +347,25 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         u[m] = exp_hw(-bLc[m]);
         w[m] = exp_hw(-bLr[m]);
     }
+    float s2q[8];  // compact aux: the stored (E4M3) other-axis scale of this thread's rows/columns
+    if constexpr (COMPACT) {
+        // the other-axis scale is rounded first and the group RTN sees z = T / s2 (stored
+        // value); the group-axis scale is absorbed exactly (RTN of a group ignores a common
+        // factor)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+        for (int m = 0; m < 8; ++m)
+            s2q[m] = e4m3_round(clampf(kind == KVARN_KEYS ? Sr[m] : Sc[m], 0.015625f, 448.f), false);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[i][j] = x[i][j] * u[j] * w[i];
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[i][j] = x[i][j] / (kind == KVARN_KEYS ? s2q[i] : s2q[j]);
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[i][j] = x[i][j] * u[j] * w[i];
+        }
     }
 
     // ---- a6: RTN along the group axis (keys: per channel, values: per token) ----------------
@@ -355,11 +396,22 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         reduce_rows<OpMin>(mn);
         reduce_rows<OpMax>(mx);
     }
-    float s[8], inv_s[8];
+    // step and offset of each group: fp32 aux keeps them; the compact aux stores the step
+    // rounded upward to E4M3 (the stored range covers the group) and the nearest binary16 of
+    // the minimum, and the codes are chosen for those stored values
+    float s[8], inv_s[8], off[8];
+    uint32_t abits[8], bbits[8];
 #pragma unroll
     for (int m = 0; m < 8; ++m) {
-        s[m] = (mx[m] - mn[m]) / qmax;
-        if (s[m] == 0.f) s[m] = 1.f;
+        const float step = (mx[m] - mn[m]) / qmax;
+        if constexpr (COMPACT) {
+            s[m] = step == 0.f ? 1.f : e4m3_round(step, true);
+            off[m] = fp16_round(mn[m], bbits[m]);
+            abits[m] = e4m3_bits(s[m]);
+        } else {
+            s[m] = step == 0.f ? 1.f : step;
+            off[m] = mn[m];
+        }
         inv_s[m] = 1.0f / s[m];
     }
     // codes -> LDS (keys [t][c], values [c][t]), 8 bytes per thread per token / channel
@@ -369,7 +421,7 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
             uint32_t lo = 0, hi = 0;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - mn[j]) * inv_s[j]), 0.f, qmax);
+                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - off[j]) * inv_s[j]), 0.f, qmax);
                 if (j < 4) lo |= q << (8 * j); else hi |= q << (8 * (j - 4));
             }
             *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tr + i) * kD + 8 * L.tc]) = make_uint2(lo, hi);
@@ -380,7 +432,7 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
             uint32_t lo = 0, hi = 0;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - mn[i]) * inv_s[i]), 0.f, qmax);
+                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - off[i]) * inv_s[i]), 0.f, qmax);
                 if (i < 4) lo |= q << (8 * i); else hi |= q << (8 * (i - 4));
             }
             *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tc + j) * kG + 8 * L.tr]) = make_uint2(lo, hi);
@@ -389,7 +441,34 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
 
     // ---- a7: aux (absorbed scales) --------------------------------------------------------
     float* aux = reinterpret_cast<float*>(dst + code_bytes(P.bits));
-    if (kind == KVARN_KEYS) {
+    uint8_t* caux = dst + code_bytes(P.bits);  // compact: b16[128] | a8[128] | s2_8[128]
+    // group-axis values of 8 groups g0 .. g0 + 7 (a as E4M3 bytes, b as binary16), and the
+    // other-axis s2 of 8 indices o0 .. o0 + 7
+    auto put_group = [&](int g0) {
+        *reinterpret_cast<uint4*>(caux + 2 * g0) =
+            make_uint4(bbits[0] | bbits[1] << 16, bbits[2] | bbits[3] << 16, bbits[4] | bbits[5] << 16,
+                       bbits[6] | bbits[7] << 16);
+        *reinterpret_cast<uint2*>(caux + 256 + g0) =
+            make_uint2(abits[0] | abits[1] << 8 | abits[2] << 16 | abits[3] << 24,
+                       abits[4] | abits[5] << 8 | abits[6] << 16 | abits[7] << 24);
+    };
+    auto put_s2 = [&](int o0) {
+        uint32_t sb[8];
+#pragma unroll
+        for (int m = 0; m < 8; ++m) sb[m] = e4m3_bits(s2q[m]);
+        *reinterpret_cast<uint2*>(caux + 384 + o0) =
+            make_uint2(sb[0] | sb[1] << 8 | sb[2] << 16 | sb[3] << 24, sb[4] | sb[5] << 8 | sb[6] << 16 | sb[7] << 24);
+    };
+    if constexpr (COMPACT) {
+        if (kind == KVARN_KEYS) {
+            if (L.tr == 0) put_group(8 * L.tc);  // per channel
+            if (L.tc == 0) put_s2(8 * L.tr);     // per token
+        } else {
+            if (L.tc == 0) put_group(8 * L.tr);  // per token
+            if (L.tr == 0) put_s2(8 * L.tc);     // per channel
+        }
+    } else {
+      if (kind == KVARN_KEYS) {
         if (L.tr == 0) {  // per channel: a = s * S_c*, b = mn * S_c*
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -413,6 +492,7 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
 #pragma unroll
             for (int j = 0; j < 8; ++j) aux[2 * kD + 8 * L.tc + j] = Sc[j];
         }
+      }
     }
     if (best_out && L.tid == 0) *best_out = best;
     __syncthreads();
@@ -465,14 +545,16 @@ struct TileArgs {
     int32_t* best_iter;
 };
 
+template <bool COMPACT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_quantize_tiles(TileArgs a) {
     __shared__ QuantSmem sm;
     const int64_t tile = a.tile0 + blockIdx.x;
     const int64_t i = tile / a.n_inner, j = tile % a.n_inner;
     const size_t esz = a.x_bf16 ? 2 : 4;
     const char* src = static_cast<const char*>(a.x) + (size_t)(i * a.x_outer + j * a.x_inner) * esz;
-    uint8_t* dst = a.out + (size_t)(i * a.out_outer + j * a.out_inner) * tile_bytes(a.P.bits);
-    quantize_tile(src, a.x_bf16 != 0, a.x_token, a.kind, a.P, dst, a.best_iter ? a.best_iter + tile : nullptr, sm);
+    uint8_t* dst = a.out + (size_t)(i * a.out_outer + j * a.out_inner) * tile_bytes(a.P.bits, COMPACT);
+    quantize_tile<COMPACT>(src, a.x_bf16 != 0, a.x_token, a.kind, a.P, dst, a.best_iter ? a.best_iter + tile : nullptr,
+                           sm);
 }
 
 struct FlushArgs {
@@ -484,6 +566,7 @@ struct FlushArgs {
 // One workgroup per (sequence, kv head, K|V).  Runs after the append kernel has incremented
 // seq_len: a sequence whose residual just reached 128 tokens quantizes it into body tile
 // (len - n_sink)/128 - 1; every other workgroup exits at once.
+template <bool COMPACT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_flush(FlushArgs a) {
     __shared__ QuantSmem sm;
     const int kind = blockIdx.x & 1;
@@ -495,8 +578,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
     if (nb >= a.c.max_blocks) return;  // the append kernel refused the token and flagged it
     const uint16_t* src = static_cast<const uint16_t*>(kind ? a.c.v_resid : a.c.k_resid) + (size_t)stream * kG * kD;
     uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) +
-                   ((size_t)stream * a.c.max_blocks + nb) * tile_bytes(a.P.bits);
-    quantize_tile(src, true, kD, kind, a.P, dst, nullptr, sm);
+                   ((size_t)stream * a.c.max_blocks + nb) * tile_bytes(a.P.bits, COMPACT);
+    quantize_tile<COMPACT>(src, true, kD, kind, a.P, dst, nullptr, sm);
 }
 
 }  // namespace
@@ -510,7 +593,10 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
         const int64_t n = total - t0 < kMaxGrid ? total - t0 : kMaxGrid;
         TileArgs a{qp, kind, x_bf16 ? 1 : 0, x, t0, n_inner, x_outer, x_inner, x_token,
                    static_cast<uint8_t*>(out), out_outer, out_inner, best_iter};
-        hipLaunchKernelGGL(k_quantize_tiles, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        if (qp.compact)
+            hipLaunchKernelGGL(k_quantize_tiles<true>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL(k_quantize_tiles<false>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -520,7 +606,10 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
 hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream) {
     FlushArgs a{qp, c, n_sink};
     const int64_t n = (int64_t)c.batch * c.n_kv * 2;
-    hipLaunchKernelGGL(k_flush, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+    if (qp.compact)
+        hipLaunchKernelGGL(k_flush<true>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+    else
+        hipLaunchKernelGGL(k_flush<false>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

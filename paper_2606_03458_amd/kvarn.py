@@ -15,6 +15,7 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libkvarn.s
 
 KVARN_F32, KVARN_BF16 = 0, 1
 KVARN_KEYS, KVARN_VALUES = 0, 1
+KVARN_AUX_F32, KVARN_AUX_COMPACT = 0, 1
 STATUS = {0: "KVARN_OK", -1: "KVARN_EINVAL", -2: "KVARN_EUNSUPPORTED", -3: "KVARN_ECAPACITY", -4: "KVARN_EHIP",
           -5: "KVARN_EWORKSPACE"}
 EXPORTS = ("kvarn_params_init", "kvarn_tile_bytes", "kvarn_cache_sizes", "kvarn_quantize_block",
@@ -30,7 +31,7 @@ class KVarNError(RuntimeError):
 class kvarn_params(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("varn_iters", ctypes.c_int32), ("n_sink", ctypes.c_int32),
                 ("var_min", ctypes.c_float), ("var_max", ctypes.c_float), ("log_lo", ctypes.c_float),
-                ("log_hi", ctypes.c_float)]
+                ("log_hi", ctypes.c_float), ("aux_format", ctypes.c_int32)]
 
 
 class kvarn_cache(ctypes.Structure):
@@ -59,7 +60,7 @@ def lib():
         P, C = ctypes.POINTER(kvarn_params), ctypes.POINTER(kvarn_cache)
         L.kvarn_params_init.argtypes = [P, i32]
         L.kvarn_params_init.restype = ctypes.c_int
-        L.kvarn_tile_bytes.argtypes = [i32]
+        L.kvarn_tile_bytes.argtypes = [P]
         L.kvarn_tile_bytes.restype = sz
         L.kvarn_cache_sizes.argtypes = [P, i32, i32, i32, ctypes.POINTER(sz)]
         L.kvarn_cache_sizes.restype = ctypes.c_int
@@ -114,8 +115,8 @@ def kvarn_params_init(bits: int = 2, **overrides) -> kvarn_params:
     return p
 
 
-def kvarn_tile_bytes(bits: int) -> int:
-    return int(lib().kvarn_tile_bytes(bits))
+def kvarn_tile_bytes(p: kvarn_params) -> int:
+    return int(lib().kvarn_tile_bytes(ctypes.byref(p)))
 
 
 def kvarn_cache_sizes(p: kvarn_params, batch: int, n_kv: int, max_blocks: int) -> list[int]:
@@ -165,7 +166,8 @@ class Cache:
     def __init__(self, p: kvarn_params, batch: int, n_kv: int, max_blocks: int, device="cuda"):
         sizes = kvarn_cache_sizes(p, batch, n_kv, max_blocks)
         self.batch, self.n_kv, self.max_blocks, self.bits, self.n_sink = batch, n_kv, max_blocks, p.bits, p.n_sink
-        tb = kvarn_tile_bytes(p.bits)
+        self.aux = p.aux_format
+        tb = kvarn_tile_bytes(p)
         u8 = dict(dtype=torch.uint8, device=device)
         self.k_body = torch.zeros((batch, n_kv, max_blocks, tb), **u8)
         self.v_body = torch.zeros((batch, n_kv, max_blocks, tb), **u8)

@@ -31,10 +31,12 @@ def _dtype(spec) -> torch.dtype:
 
 def build(name: str, device="cuda", bits: int | None = None, n_sink: int = 0, context: int | None = None,
           layers: int | None = None, batch: int | None = None, extra_blocks: int = 0, seed: int | None = None,
-          keep_inputs: bool = False, best_iter: bool = False, n_q: int | None = None, n_kv: int | None = None):
+          keep_inputs: bool = False, best_iter: bool = False, n_q: int | None = None, n_kv: int | None = None,
+          aux: int = 0):
     """Create and fill the cache of workload `name` (see datagen.WORKLOADS).
 
-    Overrides (bits, context, layers, batch, n_sink, n_q, n_kv) make variants of the same shape.
+    Overrides (bits, context, layers, batch, n_sink, n_q, n_kv) make variants of the same shape;
+    aux selects the tile's aux format (0 fp32, 1 compact).
     Returns (Built, inputs) where inputs holds the K/V/best-iteration tensors if keep_inputs.
     """
     spec = dict(datagen.WORKLOADS[name])
@@ -54,6 +56,7 @@ def build(name: str, device="cuda", bits: int | None = None, n_sink: int = 0, co
     dt = _dtype(spec)
     p = K.kvarn_params_init(spec["bits"])
     p.n_sink = n_sink
+    p.aux_format = aux
     L, B, n_kv, T = spec["layers"], spec["batch"], spec["n_kv"], spec["context"]
     prefill = n_sink + ((T - n_sink) // 128) * 128 if T > n_sink else T
     tail = T - prefill

@@ -34,7 +34,14 @@ def test_params_and_sizes(K):
     p = K.kvarn_params_init(2)
     assert (p.bits, p.varn_iters, p.n_sink) == (2, 8, 0)
     assert p.log_lo == pytest.approx(-0.3) and p.log_hi == 10.0
-    assert K.kvarn_tile_bytes(2) == 5632 and K.kvarn_tile_bytes(4) == 9728 and K.kvarn_tile_bytes(3) == 0
+    p2, p4 = K.kvarn_params_init(2), K.kvarn_params_init(4)
+    assert K.kvarn_tile_bytes(p2) == 5632 and K.kvarn_tile_bytes(p4) == 9728
+    p2.aux_format = p4.aux_format = K.KVARN_AUX_COMPACT
+    assert K.kvarn_tile_bytes(p2) == 4608 and K.kvarn_tile_bytes(p4) == 8704
+    p2.bits = 3
+    assert K.kvarn_tile_bytes(p2) == 0
+    p4.aux_format = 2
+    assert K.kvarn_tile_bytes(p4) == 0
     with pytest.raises(K.KVarNError) as e:
         K.kvarn_params_init(3)
     assert e.value.status == -2
@@ -77,7 +84,8 @@ def test_quantize_validation(K):
     for field, val, code in [("bits", 3, -2), ("varn_iters", -1, -1), ("varn_iters", 65, -1), ("var_min", 0.0, -1),
                              ("var_min", float("nan"), -1), ("var_min", 1e-31, -1), ("var_max", 1e31, -1),
                              ("var_max", float("inf"), -1), ("log_lo", 11.0, -1), ("log_lo", -41.0, -1),
-                             ("log_hi", 41.0, -1), ("log_hi", float("nan"), -1), ("n_sink", -5, -1)]:
+                             ("log_hi", 41.0, -1), ("log_hi", float("nan"), -1), ("n_sink", -5, -1),
+                             ("aux_format", 2, -2), ("aux_format", -1, -2)]:
         q = K.kvarn_params_init(2)
         setattr(q, field, val)
         with pytest.raises(K.KVarNError) as e:

@@ -24,7 +24,7 @@ def _quantize(K, x: torch.Tensor, kind: int, bits: int, **pover):
     """x [n, 128, 128] on the GPU -> (tiles uint8 [n, tile_bytes], best [n])."""
     n = x.shape[0]
     p = K.kvarn_params_init(bits, **pover)
-    out = torch.zeros((n, K.kvarn_tile_bytes(bits)), dtype=torch.uint8, device="cuda")
+    out = torch.zeros((n, K.kvarn_tile_bytes(p)), dtype=torch.uint8, device="cuda")
     best = torch.full((n,), -1, dtype=torch.int32, device="cuda")
     dt = K.KVARN_F32 if x.dtype == torch.float32 else K.KVARN_BF16
     K.kvarn_quantize_block(p, kind, x, dt, n, 1, 128 * 128, 0, 128, out, 1, 0, best)
@@ -80,7 +80,7 @@ def test_quantize_strided_views(K):
     H, T, S = 3, 256, 2
     x = torch.randn((S, T, H, 128), device="cuda", dtype=torch.bfloat16) * 2
     p = K.kvarn_params_init(2)
-    tb = K.kvarn_tile_bytes(2)
+    tb = K.kvarn_tile_bytes(K.kvarn_params_init(2))
     out = torch.zeros((S * H, 5, tb), dtype=torch.uint8, device="cuda")
     for s in range(S):
         # outer = head, inner = block; out row s*H + h, tiles at blocks 1 and 3 (stride 2)

@@ -168,3 +168,16 @@ def test_degenerate_tiles(orc):
         r = orc.varn(T, p)
         assert np.all(np.isfinite(r.Sc)) and np.all(np.isfinite(r.Sr)) and np.all(np.isfinite(r.B))
         np.testing.assert_allclose(r.Lc[1], p.log_lo)  # 0.5*log(1e-8) = -9.2 clamps to -0.3
+
+
+def test_force_best_keeps_the_named_iteration(orc):
+    """The test-only force_best knob returns the scales recorded for that iteration, and -1 is
+    Algorithm 1's own selection."""
+    from tiles import tile
+    T = orc.hadamard128(tile("tinyK", 4))
+    base = orc.varn(T, orc.Params())
+    for k in (0, 3, 8):
+        r = orc.varn(T, orc.Params(force_best=k))
+        assert r.best_iter == k
+        assert np.allclose(np.log(r.Sc), base.Lc[k], rtol=0, atol=1e-12)
+        assert np.allclose(np.log(r.Sr), base.Lr[k], rtol=0, atol=1e-12)
