@@ -612,6 +612,21 @@ __device__ __forceinline__ uint32_t quad_transpose_bytes(uint32_t y, int j) {
     return perm((uint32_t)dpp_x1((int)t), t, selB);
 }
 
+// The codes of one unit as the B operand of the row-digit kernel.  At 2 bits one shift gives
+// all four byte planes: dwords 0 and 2 carry the codes, dwords 1 and 3 four times the codes;
+// the A operand compensates with elements kPlaneMul times larger in dwords 0 and 2.
+template <int BITS>
+__device__ __forceinline__ v4i unit_planes(const uint32_t* w) {
+    if constexpr (BITS == 2) {
+        const uint32_t x = w[0], x4 = x >> 4, M = 0x03030303u;
+        return v4i{(int)(x & M), (int)(x & (M << 2)), (int)(x4 & M), (int)(x4 & (M << 2))};
+    } else {
+        return unit_i8<BITS>(w);
+    }
+}
+template <int BITS>
+constexpr float kPlaneMul = BITS == 2 ? 4.f : 1.f;
+
 // Query heads are taken in groups of four (NH groups, g <= 4 * NH): every group repeats the
 // per-head work on the same code operands, which are extracted once per tile.
 template <int NH>
@@ -628,9 +643,14 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 &&
 void k_decode4(DecodeArgs a) {
     __shared__ Smem4<NH> sm;
     constexpr int WPU = BITS / 2;
-    constexpr int NHD = 4 * NH;                          // head slots
-    constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // fixed-point bound of q~ and p~
-    constexpr float MAGIC = 12582912.f;                  // 1.5 * 2^23: x + MAGIC rounds x to an integer
+    constexpr int NHD = 4 * NH;  // head slots
+    // Fixed point: q~ and p~ in even dwords of the A operand are scaled by MUL (the code planes
+    // there are not shifted up), so every product term carries weight MUL.  The exact sum is
+    // bounded by MUL * (2^BITS - 1) * 128 * QMAX < 2^31 and MUL * QMAX < 2^22 keeps the
+    // rounding below exact.
+    constexpr float MUL = kPlaneMul<BITS>;
+    constexpr int QMAX = 1048575;
+    constexpr float MAGIC = 12582912.f;  // 1.5 * 2^23: x + MAGIC rounds x to an integer
     constexpr uint32_t MAGIC_BITS = 0x4B400000u;
     // output role: head 4*hg + G, column n; A-operand role: row 4*h + j (digit j of head 4*hg + h)
     const int l = threadIdx.x, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
@@ -760,15 +780,18 @@ void k_decode4(DecodeArgs a) {
                     }
                     mx = row_max(mx);
                     const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
-                    float bs = 0.f;
+                    // channels 8n .. 8n + 3 sit in an even dword of the A operand, 8n + 4 ..
+                    // 8n + 7 in an odd one; beta is kept in units of MUL grid steps
+                    float bs_e = 0.f, bs_o = 0.f;
                     uint32_t y[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        const float yf = fmaf(qt[k], sc, MAGIC);
-                        bs = fmaf(yf - MAGIC, rk[k], bs);
+                        const float yf = fmaf(qt[k], k < 4 ? sc * MUL : sc, MAGIC);
+                        if (k < 4) bs_e = fmaf(yf - MAGIC, rk[k], bs_e);
+                        else bs_o = fmaf(yf - MAGIC, rk[k], bs_o);
                         y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
                     }
-                    bs = row_sum(bs);
+                    const float bs = row_sum(fmaf(bs_o, MUL, bs_e));
                     uint32_t d0, d1, d2, e0, e1, e2;
                     digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
                     digits4(y[4], y[5], y[6], y[7], e0, e1, e2);
@@ -777,7 +800,7 @@ void k_decode4(DecodeArgs a) {
                     reinterpret_cast<uint2*>(&sm.qp[hg][2][kap][Gq][G])[half] = make_uint2(d2, e2);
                     if (n == 0) {
                         sm.hv[4 * hg + G][0] = bs;
-                        sm.hv[4 * hg + G][1] = mx * (1.0f / (float)QMAX);
+                        sm.hv[4 * hg + G][1] = mx * (1.0f / (MUL * (float)QMAX));
                     }
                 }
             }
@@ -802,7 +825,7 @@ void k_decode4(DecodeArgs a) {
                         v4i c = {0, 0, 0, 0};
 #pragma unroll
                         for (int kap = 0; kap < 2; ++kap)
-                            c = mfma_i8(aq[kap], unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]), c);
+                            c = mfma_i8(aq[kap], unit_planes<BITS>(&kw[sg][(2 * tau + kap) * WPU]), c);
                         lg[hg][4 * sg + tau] =
                             ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
                     }
@@ -823,15 +846,17 @@ void k_decode4(DecodeArgs a) {
                 }
                 pmx = row_max(pmx);
                 const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
-                float gam = 0.f;
+                // tokens 16 tau + .. sit in dword tau of the A operand: even tau scaled by MUL
+                float gam_e = 0.f, gam_o = 0.f;
                 v4i ap[2];
 #pragma unroll
                 for (int sg = 0; sg < 2; ++sg) {
                     uint32_t D[4];
 #pragma unroll
                     for (int tau = 0; tau < 4; ++tau) {
-                        const float yf = fmaf(lg[hg][4 * sg + tau], psc, MAGIC);
-                        gam = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam);
+                        const float yf = fmaf(lg[hg][4 * sg + tau], (tau & 1) ? psc : psc * MUL, MAGIC);
+                        if (tau & 1) gam_o = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_o);
+                        else gam_e = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_e);
                         // bytes of y: the three digits plus 128 each, and 0x80 on top (digit
                         // slot 3 becomes zero); after the transpose lane (head, 4m + i) holds
                         // digit i of tokens 16 tau + 4m + {0..3}, which lane (m, 4 head + i)
@@ -842,7 +867,7 @@ void k_decode4(DecodeArgs a) {
                     }
                     ap[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
                 }
-                gam = row_sum(gam);
+                const float gam = row_sum(fmaf(gam_o, MUL, gam_e));  // MUL grid steps
 
                 // PV: head 4*hg + G, channel 16*mt + n
                 v4i acc[8];
@@ -852,9 +877,9 @@ void k_decode4(DecodeArgs a) {
                 for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
                     for (int mt = 0; mt < 8; ++mt)
-                        acc[mt] = mfma_i8(ap[sg], unit_i8<BITS>(&vw[sg][mt * WPU]), acc[mt]);
+                        acc[mt] = mfma_i8(ap[sg], unit_planes<BITS>(&vw[sg][mt * WPU]), acc[mt]);
                 if (hg == NH - 1 && more) load_codes(tile_v(blk + 1), vc);
-                const float fp = pmx * (1.0f / (float)QMAX);
+                const float fp = pmx * (1.0f / (MUL * (float)QMAX));
 #pragma unroll
                 for (int mt = 0; mt < 8; ++mt)
                     orot[hg][mt] = fmaf((float)digit_sum(acc[mt]) + gam, fp * sm.aux[5][16 * mt + n],
