@@ -52,12 +52,13 @@ class _Params(ctypes.Structure):
                 ("c_min", ctypes.c_double), ("c_max", ctypes.c_double),
                 ("log_lo", ctypes.c_double), ("log_hi", ctypes.c_double),
                 ("imb_floor", ctypes.c_double), ("ddof", ctypes.c_int32), ("aux", ctypes.c_int32),
-                ("force_best", ctypes.c_int32)]
+                ("force_best", ctypes.c_int32), ("rotate", ctypes.c_int32)]
 
 
 class _Cache(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_kv", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
                 ("n_sink", ctypes.c_int32), ("bits", ctypes.c_int32), ("aux", ctypes.c_int32),
+                ("rotate", ctypes.c_int32),
                 ("k_body", ctypes.c_void_p), ("v_body", ctypes.c_void_p),
                 ("k_resid", ctypes.c_void_p), ("v_resid", ctypes.c_void_p),
                 ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p),
@@ -72,7 +73,8 @@ class Params:
     iteration count of the runtime experiment (Sec. 4.2); c_min/c_max are unstated (unpinned).
     aux selects the stored aux format: 0 = fp32 vectors, 1 = compact (App. D: E4M3 scales,
     binary16 offset).  force_best (test use) keeps iteration k's scales instead of Algorithm 1's
-    selection: the outcome had k won a near-tie of Imb.
+    selection: the outcome had k won a near-tie of Imb.  rotate = 0 drops the Hadamard rotation
+    (with varn_iters = 0: KIVI-style RTN; with K > 0: VarN alone, the ablations of Fig. 1).
     """
     bits: int = 2
     varn_iters: int = 8
@@ -84,10 +86,11 @@ class Params:
     ddof: int = 1
     aux: int = 0
     force_best: int = -1
+    rotate: int = 1
 
     def c(self) -> _Params:
         return _Params(self.bits, self.varn_iters, self.c_min, self.c_max, self.log_lo, self.log_hi,
-                       self.imb_floor, self.ddof, self.aux, self.force_best)
+                       self.imb_floor, self.ddof, self.aux, self.force_best, self.rotate)
 
 
 _lib = None
@@ -112,7 +115,8 @@ def lib():
         L.kvo_tile_bytes.restype = ctypes.c_size_t
         L.kvo_pack_tile.argtypes = [vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp]
         L.kvo_unpack_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp]
-        L.kvo_dequantize_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp]
+        L.kvo_dequantize_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp]
+        L.kvo_error_decomposition.argtypes = [vp, vp, ctypes.c_int32, vp, vp, vp]
         L.kvo_e4m3_to_double.argtypes = [ctypes.c_uint8]
         L.kvo_e4m3_to_double.restype = ctypes.c_double
         L.kvo_e4m3_from_double.argtypes = [ctypes.c_double, ctypes.c_int]
@@ -251,11 +255,20 @@ def unpack_tile(tile, kind: int, bits: int, aux: int = 0):
     return codes, a, b, s2
 
 
-def dequantize_tile(tile, kind: int, bits: int, aux: int = 0) -> np.ndarray:
+def dequantize_tile(tile, kind: int, bits: int, aux: int = 0, rotate: int = 1) -> np.ndarray:
     tile = np.ascontiguousarray(tile, dtype=np.uint8)
     X = np.zeros((G, D))
-    lib().kvo_dequantize_tile(_p(tile), kind, bits, aux, _p(X))
+    lib().kvo_dequantize_tile(_p(tile), kind, bits, aux, rotate, _p(X))
     return X
+
+
+def error_decomposition(K, Kdq):
+    """Per-token (E_T, E_M, E_D) of Sec. 3.1 Eq. 3 for rows of 128."""
+    K, Kdq = _f64(K).reshape(-1, D), _f64(Kdq).reshape(-1, D)
+    n = K.shape[0]
+    ET, EM, ED = np.zeros(n), np.zeros(n), np.zeros(n)
+    lib().kvo_error_decomposition(_p(K), _p(Kdq), n, _p(ET), _p(EM), _p(ED))
+    return ET, EM, ED
 
 
 def e4m3_decode(v: int) -> float:
@@ -302,10 +315,10 @@ def quantize_tiles(x: np.ndarray, kind: int, params: Params = Params()) -> np.nd
 class HostCache:
     """Host copy of the cache in the shared layout (numpy arrays; bf16 held as uint16)."""
 
-    def __init__(self, batch, n_kv, max_blocks, bits=2, n_sink=0, aux=0):
+    def __init__(self, batch, n_kv, max_blocks, bits=2, n_sink=0, aux=0, rotate=1):
         tb = tile_bytes(bits, aux)
         self.batch, self.n_kv, self.max_blocks, self.bits, self.n_sink = batch, n_kv, max_blocks, bits, n_sink
-        self.aux = aux
+        self.aux, self.rotate = aux, rotate
         self.k_body = np.zeros((batch, n_kv, max_blocks, tb), dtype=np.uint8)
         self.v_body = np.zeros((batch, n_kv, max_blocks, tb), dtype=np.uint8)
         self.k_resid = np.zeros((batch, n_kv, G, D), dtype=np.uint16)
@@ -315,7 +328,7 @@ class HostCache:
         self.seq_len = np.zeros(batch, dtype=np.int32)
 
     def c(self) -> _Cache:
-        return _Cache(self.batch, self.n_kv, self.max_blocks, self.n_sink, self.bits, self.aux,
+        return _Cache(self.batch, self.n_kv, self.max_blocks, self.n_sink, self.bits, self.aux, self.rotate,
                       self.k_body.ctypes.data, self.v_body.ctypes.data, self.k_resid.ctypes.data,
                       self.v_resid.ctypes.data, self.k_sink.ctypes.data, self.v_sink.ctypes.data,
                       self.seq_len.ctypes.data)
@@ -349,7 +362,7 @@ def decode(cache: HostCache, q: np.ndarray, scale: float) -> np.ndarray:
 
 def append(cache: HostCache, k_new: np.ndarray, v_new: np.ndarray, params: Params = Params()) -> int:
     """Append one bf16 token per (sequence, kv head); flushes full residuals into the body."""
-    assert params.bits == cache.bits and params.aux == cache.aux
+    assert params.bits == cache.bits and params.aux == cache.aux and params.rotate == cache.rotate
     k_new = np.ascontiguousarray(k_new, dtype=np.uint16)
     v_new = np.ascontiguousarray(v_new, dtype=np.uint16)
     cc = cache.c()

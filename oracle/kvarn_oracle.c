@@ -43,6 +43,8 @@ typedef struct {
                             binary16 b) */
     int32_t force_best;  /* -1: Algorithm 1's selection.  k in 0..K: keep iteration k's scales
                             instead (test use: the outcome had iteration k won a near-tie) */
+    int32_t rotate;      /* 1: Hadamard rotation before VarN (KVarN); 0: none (the ablations of
+                            Fig. 1: KIVI-style RTN with K = 0, VarN alone with K > 0) */
 } kvo_params;
 
 /* ------------------------------------------------------------------------------------------
@@ -358,7 +360,8 @@ void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *
     double *Bal = malloc((size_t)G * D * sizeof(double));
     double Sc[D], Sr[G];
     memcpy(T, X, (size_t)G * D * sizeof(double));
-    for (int t = 0; t < G; ++t) kvo_hadamard128(T + (size_t)t * D);
+    if (p->rotate)
+        for (int t = 0; t < G; ++t) kvo_hadamard128(T + (size_t)t * D);
     kvo_varn(T, G, D, p, Sc, Sr, Bal, imb_hist, NULL, NULL, best_iter);
 
     if (p->aux == 1) {
@@ -491,7 +494,7 @@ void kvo_unpack_tile(const uint8_t *src, int kind, int bits, int aux, uint8_t *c
  *            values Xr[t][c] = (code * a[t] + b[t]) * s2[c]
  *   then X[t,:] = H Xr[t,:] (H is its own inverse).  Out: X[128*128] token-major.
  */
-void kvo_dequantize_tile(const uint8_t *src, int kind, int bits, int aux, double *X) {
+void kvo_dequantize_tile(const uint8_t *src, int kind, int bits, int aux, int rotate, double *X) {
     uint8_t *codes = malloc((size_t)G * D);
     float a[128], b[128], s2[128];
     kvo_unpack_tile(src, kind, bits, aux, codes, a, b, s2);
@@ -501,7 +504,7 @@ void kvo_dequantize_tile(const uint8_t *src, int kind, int bits, int aux, double
             X[(size_t)t * D + c] = kind == KVO_KEYS ? (q * (double)a[c] + (double)b[c]) * (double)s2[t]
                                                     : (q * (double)a[t] + (double)b[t]) * (double)s2[c];
         }
-        kvo_hadamard128(X + (size_t)t * D);
+        if (rotate) kvo_hadamard128(X + (size_t)t * D);
     }
     free(codes);
 }
@@ -552,7 +555,7 @@ void kvo_quantize_tiles(const void *x, int dtype, int64_t n_outer, int64_t n_inn
  *   seq_len:          [batch] int32
  * ------------------------------------------------------------------------------------------ */
 typedef struct {
-    int32_t batch, n_kv, max_blocks, n_sink, bits, aux;
+    int32_t batch, n_kv, max_blocks, n_sink, bits, aux, rotate;
     uint8_t *k_body, *v_body;
     uint16_t *k_resid, *v_resid, *k_sink, *v_sink;
     int32_t *seq_len;
@@ -589,9 +592,9 @@ void kvo_gather_stream(const kvo_cache *cc, int32_t bi, int32_t kh, double *K, d
         }
     for (int32_t blk = 0; blk < nb; ++blk, t += G) {
         kvo_dequantize_tile(cc->k_body + (stream * cc->max_blocks + blk) * tb, KVO_KEYS, cc->bits, cc->aux,
-                            K + (size_t)t * D);
+                            cc->rotate, K + (size_t)t * D);
         kvo_dequantize_tile(cc->v_body + (stream * cc->max_blocks + blk) * tb, KVO_VALUES, cc->bits, cc->aux,
-                            V + (size_t)t * D);
+                            cc->rotate, V + (size_t)t * D);
     }
     for (int32_t i = 0; i < nr; ++i, ++t)
         for (int c = 0; c < D; ++c) {
@@ -657,7 +660,7 @@ void kvo_decode(const kvo_cache *cc, int32_t n_q, const void *q, int dtype, doub
  * emptied.  Returns 0, or -3 if a sequence has no free body slot for the flush.
  */
 int kvo_append(kvo_cache *cc, const uint16_t *k_new, const uint16_t *v_new, const kvo_params *p) {
-    if (p->bits != cc->bits || p->aux != cc->aux) return -1;
+    if (p->bits != cc->bits || p->aux != cc->aux || p->rotate != cc->rotate) return -1;
     const size_t tb = kvo_tile_bytes(cc->bits, cc->aux);
     for (int32_t bi = 0; bi < cc->batch; ++bi) {
         int32_t len = cc->seq_len[bi];
@@ -689,4 +692,29 @@ int kvo_append(kvo_cache *cc, const uint16_t *k_new, const uint16_t *v_new, cons
         cc->seq_len[bi] = len + 1;
     }
     return 0;
+}
+
+/* ------------------------------------------------------------------------------------------
+ * Error decomposition of Sec. 3.1, Eq. 3, per token (row of 128): with the angle theta
+ * between k and its dequantized k_dq,
+ *   E_T = |k - k_dq|^2                         total error
+ *   E_M = (|k| - |k_dq|)^2                     magnitude error
+ *   E_D = 2 |k| |k_dq| (1 - cos theta)         directional error,   E_T = E_M + E_D.
+ * E_D is formed as 2 (|k| |k_dq| - k . k_dq), the same quantity without the angle.
+ * ------------------------------------------------------------------------------------------ */
+void kvo_error_decomposition(const double *K, const double *Kdq, int32_t n, double *ET, double *EM, double *ED) {
+    for (int32_t t = 0; t < n; ++t) {
+        const double *k = K + (size_t)t * D, *q = Kdq + (size_t)t * D;
+        double kk = 0.0, qq = 0.0, kq = 0.0, e = 0.0;
+        for (int c = 0; c < D; ++c) {
+            kk += k[c] * k[c];
+            qq += q[c] * q[c];
+            kq += k[c] * q[c];
+            e += (k[c] - q[c]) * (k[c] - q[c]);
+        }
+        const double nk = sqrt(kk), nq = sqrt(qq);
+        ET[t] = e;
+        EM[t] = (nk - nq) * (nk - nq);
+        ED[t] = 2.0 * (nk * nq - kq);
+    }
 }
