@@ -92,6 +92,11 @@ typedef struct {
     float log_lo;       /* clamp of the cumulative log-scales: -0.3 (Algorithm 1)       */
     float log_hi;       /* 10.0 (Algorithm 1)                                           */
     int32_t aux_format; /* KVARN_AUX_F32 (default) or KVARN_AUX_COMPACT                  */
+    int32_t rotate;     /* 1 (default): Hadamard rotation before VarN, as KVarN does.  0: no
+                         * rotation -- with varn_iters = 0 the quantizer is KIVI-style RTN,
+                         * with varn_iters > 0 VarN alone (the ablations of Fig. 1).  Tiles
+                         * then hold the unrotated domain and decode skips both rotations;
+                         * every call on one cache must use the same value. */
 } kvarn_params;
 typedef enum { KVARN_AUX_F32 = 0, KVARN_AUX_COMPACT = 1 } kvarn_aux_format;
 /* Accepted ranges (else KVARN_EINVAL): 1e-30 <= var_min <= var_max <= 1e30 and

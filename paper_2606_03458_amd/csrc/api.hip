@@ -15,6 +15,7 @@ int check_params(const kvarn_params* p) {
     if (!p) return KVARN_EINVAL;
     if (p->bits != 2 && p->bits != 4) return KVARN_EUNSUPPORTED;
     if (p->aux_format != KVARN_AUX_F32 && p->aux_format != KVARN_AUX_COMPACT) return KVARN_EUNSUPPORTED;
+    if (p->rotate != 0 && p->rotate != 1) return KVARN_EINVAL;
     if (p->varn_iters < 0 || p->varn_iters > 64) return KVARN_EINVAL;
     if (p->n_sink < 0 || p->n_sink > 1024) return KVARN_EINVAL;
     // ranges that keep exp(+-L) and log(v) of the quantizer inside the normal fp32 range
@@ -25,7 +26,7 @@ int check_params(const kvarn_params* p) {
 
 QParams qparams(const kvarn_params* p) {
     return QParams{p->bits, p->varn_iters, p->var_min, p->var_max, p->log_lo, p->log_hi,
-                   p->aux_format == KVARN_AUX_COMPACT ? 1 : 0};
+                   p->aux_format == KVARN_AUX_COMPACT ? 1 : 0, p->rotate};
 }
 
 int check_cache(const kvarn_params* p, const kvarn_cache* c) {
@@ -57,6 +58,7 @@ int kvarn_params_init(kvarn_params* p, int32_t bits) {
     p->log_lo = -0.3f;
     p->log_hi = 10.0f;
     p->aux_format = KVARN_AUX_F32;
+    p->rotate = 1;
     return KVARN_OK;
 }
 
@@ -155,7 +157,7 @@ int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int3
     const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
     const size_t need = decode_workspace_bytes(cache->batch, n_q, plan);
     if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return KVARN_EWORKSPACE;
-    hipError_t e = launch_decode(*cache, p->bits, p->aux_format == KVARN_AUX_COMPACT, p->n_sink, n_q, q,
+    hipError_t e = launch_decode(*cache, p->bits, p->aux_format == KVARN_AUX_COMPACT, p->rotate, p->n_sink, n_q, q,
                                  q_dtype == KVARN_BF16, out, out_dtype == KVARN_BF16, sm_scale, plan,
                                  static_cast<float*>(workspace), stream);
     return e == hipSuccess ? KVARN_OK : KVARN_EHIP;

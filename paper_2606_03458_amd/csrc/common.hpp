@@ -36,6 +36,7 @@ struct QParams {
     int iters;
     float var_min, var_max, log_lo, log_hi;
     int compact;  // aux format: 0 fp32, 1 compact
+    int rotate;   // 1: Hadamard rotation along head_dim before VarN; 0: none (ablations)
 };
 
 // Kernel launchers (defined in the .hip files; called by the host API).
@@ -57,8 +58,8 @@ struct DecodePlan {
 DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int n_sink, int max_blocks);
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan);
 
-hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int n_sink, int n_q, const void* q, bool q_bf16,
-                         void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
+hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate, int n_sink, int n_q, const void* q,
+                         bool q_bf16, void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
                          hipStream_t stream);
 
 }  // namespace kvarn

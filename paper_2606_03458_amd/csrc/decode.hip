@@ -59,6 +59,7 @@ struct DecodeArgs {
     int out_bf16;
     int n_kv, n_q, g, max_blocks, n_sink;
     int compact;       // aux format of the body tiles: 0 fp32, 1 compact (binary16 b, E4M3 a and s2)
+    int rotate;        // 1: body tiles hold the Hadamard-rotated domain; 0: unrotated (ablations)
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
     int n_split, bps;  // body splits per stream and body tiles per split
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
@@ -243,8 +244,10 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     if (blk0 < blk1) {
         for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] = load_q(qrow * kD + idx);
         __syncthreads();
-        lds_hadamard<GQ>(sm.q, g);
-        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
+        if (a.rotate) {
+            lds_hadamard<GQ>(sm.q, g);
+            for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
+        }
 
         // Lane l's part of a tile: its K and V code units (32*WPU bytes per 64-token half) and
         // its pieces of the aux.
@@ -520,13 +523,14 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
             if (G == 0) sm.hv[hn][3] = lt;
         }
         __syncthreads();
-        lds_hadamard<GQ>(sm.q, g);
+        if (a.rotate) lds_hadamard<GQ>(sm.q, g);
+        const float rs = a.rotate ? kInvSqrt128 : 1.f;
 #pragma unroll
         for (int h = 0; h < GQ; ++h) {
             if (h < g) {
                 const float L = sm.hv[h][3];
-                float o0 = sm.q[h][2 * l] * kInvSqrt128 + oplain[h][0];
-                float o1 = sm.q[h][2 * l + 1] * kInvSqrt128 + oplain[h][1];
+                float o0 = sm.q[h][2 * l] * rs + oplain[h][0];
+                float o1 = sm.q[h][2 * l + 1] * rs + oplain[h][1];
                 o0 = L > 0.f ? o0 / L : 0.f;
                 o1 = L > 0.f ? o1 / L : 0.f;
                 const size_t idx = (qrow + h) * kD + 2 * l;
@@ -709,13 +713,14 @@ void k_decode4(DecodeArgs a) {
         for (int idx = l; idx < NH * 32; idx += 64)
             sm.qp[idx >> 5][3][(idx >> 4) & 1][(idx >> 2) & 3][idx & 3] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
-        lds_hadamard<NHD>(sm.q, g);
-        // q~ role: head 4*hg + G, channels 8n .. 8n + 7 (rotated, normalized)
+        if (a.rotate) lds_hadamard<NHD>(sm.q, g);
+        // q~ role: head 4*hg + G, channels 8n .. 8n + 7 (rotated and normalized, or as given)
+        const float qs = a.rotate ? kInvSqrt128 : 1.f;
         float qr[NH][8];
 #pragma unroll
         for (int hg = 0; hg < NH; ++hg)
 #pragma unroll
-            for (int k = 0; k < 8; ++k) qr[hg][k] = sm.q[4 * hg + G][8 * n + k] * kInvSqrt128;
+            for (int k = 0; k < 8; ++k) qr[hg][k] = sm.q[4 * hg + G][8 * n + k] * qs;
         // source lane of the PV operand permutation (see above), as a byte address
         const int perm_addr = (16 * h + 4 * G + j) * 4;
 
@@ -989,13 +994,14 @@ void k_decode4(DecodeArgs a) {
             }
         }
         __syncthreads();
-        lds_hadamard<NHD>(sm.q, g);
+        if (a.rotate) lds_hadamard<NHD>(sm.q, g);
+        const float rs = a.rotate ? kInvSqrt128 : 1.f;
 #pragma unroll
         for (int hh = 0; hh < NHD; ++hh) {
             if (hh < g) {
                 const float L = sm.hv[hh][3];
-                float o0 = sm.q[hh][2 * l] * kInvSqrt128 + oplain[hh][0];
-                float o1 = sm.q[hh][2 * l + 1] * kInvSqrt128 + oplain[hh][1];
+                float o0 = sm.q[hh][2 * l] * rs + oplain[hh][0];
+                float o1 = sm.q[hh][2 * l + 1] * rs + oplain[hh][1];
                 o0 = L > 0.f ? o0 / L : 0.f;
                 o1 = L > 0.f ? o1 / L : 0.f;
                 const size_t idx = (qrow + hh) * kD + 2 * l;
@@ -1051,7 +1057,7 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
     }
     orot[c] = acc;
     __syncthreads();
-    for (int h = 1; h < kD; h <<= 1) {
+    for (int h = 1; a.rotate && h < kD; h <<= 1) {
         float x0 = 0.f, x1 = 0.f;
         int i0 = 0;
         if (c < 64) {
@@ -1066,7 +1072,7 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
         }
         __syncthreads();
     }
-    float o = orot[c] * kInvSqrt128 + pl;
+    float o = orot[c] * (a.rotate ? kInvSqrt128 : 1.f) + pl;
     o = L > 0.f ? o / L : 0.f;
     const size_t idx = bh * kD + c;
     if (a.out_bf16)
@@ -1127,11 +1133,12 @@ size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan) {
     return (size_t)batch * n_q * plan.n_split * kPart * sizeof(float);
 }
 
-hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int n_sink, int n_q, const void* q, bool q_bf16,
-                         void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
+hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate, int n_sink, int n_q, const void* q,
+                         bool q_bf16, void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
                          hipStream_t stream) {
     DecodeArgs a;
     a.compact = compact;
+    a.rotate = rotate;
     a.k_body = static_cast<const uint8_t*>(c.k_body);
     a.v_body = static_cast<const uint8_t*>(c.v_body);
     a.k_resid = static_cast<const uint16_t*>(c.k_resid);

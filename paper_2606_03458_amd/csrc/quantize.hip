@@ -255,38 +255,41 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         }
     }
 
-    // ---- a2: Hadamard along channels, butterflies of stride 1, 2, ..., 64 ------------------
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-#pragma unroll
-        for (int h = 1; h < 8; h <<= 1) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (!(j & h)) {
-                    const float a = x[i][j], b = x[i][j + h];
-                    x[i][j] = a + b;
-                    x[i][j + h] = a - b;
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int m = 1; m < 16; m <<= 1) {  // channel stride 8*m lives in lane tc ^ m
-        const bool upper = (L.tc & m) != 0;
+    // ---- a2: Hadamard along channels, butterflies of stride 1, 2, ..., 64 (not in the ablations
+    // without rotation) ----------------------------------------------------------------------
+    if (P.rotate) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                // partners ^1 and ^2 by DPP quad permutes, ^4 and ^8 through the LDS crossbar
-                const float p = m == 1 ? dppf<0xB1>(x[i][j]) : (m == 2 ? dppf<0x4E>(x[i][j]) : __shfl_xor(x[i][j], m));
-                x[i][j] = upper ? (p - x[i][j]) : (x[i][j] + p);
+            for (int h = 1; h < 8; h <<= 1) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (!(j & h)) {
+                        const float a = x[i][j], b = x[i][j + h];
+                        x[i][j] = a + b;
+                        x[i][j + h] = a - b;
+                    }
+                }
             }
         }
-    }
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
+        for (int m = 1; m < 16; m <<= 1) {  // channel stride 8*m lives in lane tc ^ m
+            const bool upper = (L.tc & m) != 0;
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[i][j] *= kInvSqrt128;
+            for (int i = 0; i < 8; ++i) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    // partners ^1 and ^2 by DPP quad permutes, ^4 and ^8 through the LDS crossbar
+                    const float p = m == 1 ? dppf<0xB1>(x[i][j]) : (m == 2 ? dppf<0x4E>(x[i][j]) : __shfl_xor(x[i][j], m));
+                    x[i][j] = upper ? (p - x[i][j]) : (x[i][j] + p);
+                }
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[i][j] *= kInvSqrt128;
+        }
     }
 
     // ---- a3/a4: VarN (Algorithm 1), Cur = T * u[c] * w[t] with u = exp(-L_c), w = exp(-L_r) -

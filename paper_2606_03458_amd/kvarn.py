@@ -31,7 +31,7 @@ class KVarNError(RuntimeError):
 class kvarn_params(ctypes.Structure):
     _fields_ = [("bits", ctypes.c_int32), ("varn_iters", ctypes.c_int32), ("n_sink", ctypes.c_int32),
                 ("var_min", ctypes.c_float), ("var_max", ctypes.c_float), ("log_lo", ctypes.c_float),
-                ("log_hi", ctypes.c_float), ("aux_format", ctypes.c_int32)]
+                ("log_hi", ctypes.c_float), ("aux_format", ctypes.c_int32), ("rotate", ctypes.c_int32)]
 
 
 class kvarn_cache(ctypes.Structure):
@@ -166,7 +166,7 @@ class Cache:
     def __init__(self, p: kvarn_params, batch: int, n_kv: int, max_blocks: int, device="cuda"):
         sizes = kvarn_cache_sizes(p, batch, n_kv, max_blocks)
         self.batch, self.n_kv, self.max_blocks, self.bits, self.n_sink = batch, n_kv, max_blocks, p.bits, p.n_sink
-        self.aux = p.aux_format
+        self.aux, self.rotate = p.aux_format, p.rotate
         tb = kvarn_tile_bytes(p)
         u8 = dict(dtype=torch.uint8, device=device)
         self.k_body = torch.zeros((batch, n_kv, max_blocks, tb), **u8)

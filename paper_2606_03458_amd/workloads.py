@@ -32,11 +32,12 @@ def _dtype(spec) -> torch.dtype:
 def build(name: str, device="cuda", bits: int | None = None, n_sink: int = 0, context: int | None = None,
           layers: int | None = None, batch: int | None = None, extra_blocks: int = 0, seed: int | None = None,
           keep_inputs: bool = False, best_iter: bool = False, n_q: int | None = None, n_kv: int | None = None,
-          aux: int = 0):
+          aux: int = 0, rotate: int = 1, varn_iters: int | None = None):
     """Create and fill the cache of workload `name` (see datagen.WORKLOADS).
 
     Overrides (bits, context, layers, batch, n_sink, n_q, n_kv) make variants of the same shape;
-    aux selects the tile's aux format (0 fp32, 1 compact).
+    aux selects the tile's aux format (0 fp32, 1 compact); rotate = 0 and varn_iters select the
+    ablation quantizers (no rotation, K = 0: KIVI-style RTN; no rotation, K > 0: VarN alone).
     Returns (Built, inputs) where inputs holds the K/V/best-iteration tensors if keep_inputs.
     """
     spec = dict(datagen.WORKLOADS[name])
@@ -57,6 +58,9 @@ def build(name: str, device="cuda", bits: int | None = None, n_sink: int = 0, co
     p = K.kvarn_params_init(spec["bits"])
     p.n_sink = n_sink
     p.aux_format = aux
+    p.rotate = rotate
+    if varn_iters is not None:
+        p.varn_iters = varn_iters
     L, B, n_kv, T = spec["layers"], spec["batch"], spec["n_kv"], spec["context"]
     prefill = n_sink + ((T - n_sink) // 128) * 128 if T > n_sink else T
     tail = T - prefill

@@ -56,7 +56,8 @@ def _tile_mismatch(codes, a, b, s2, r, qmax):
     return hard, excused, float(max(ea.max(), eb.max()))
 
 
-def compare_tiles(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gpu_best=None, params=None):
+def compare_tiles(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gpu_best=None, params=None,
+                  tie_fraction: float = TIE_FRACTION):
     """gpu_tiles [n, tile_bytes] uint8 (GPU output); X [n, 128, 128] float64 (exact input).
 
     A tile whose kept VarN iteration differs from the oracle's is still compared code by
@@ -83,24 +84,24 @@ def compare_tiles(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gp
                 near = [k for k in range(len(I)) if k != k_o and abs(I[k] - I[k_o]) <= 1e-5 * abs(I[k_o])]
                 assert near, (i, hard, aux, k_o, I)
             stats["best_ties"] += 1
-            _check_dequant_bound(gpu_tiles[i], X[i], kind, bits)
+            _check_dequant_bound(gpu_tiles[i], X[i], kind, bits, params.rotate)
             continue
         stats["codes"] += codes.size
         stats["excused"] += excused
         stats["max_aux_rel"] = max(stats["max_aux_rel"], aux)
-    assert stats["excused"] <= TIE_FRACTION * max(stats["codes"], 1) + 1, stats
+    assert stats["excused"] <= tie_fraction * max(stats["codes"], 1) + 1, stats
     assert stats["best_ties"] <= max(1, n // 100), stats
     return stats
 
 
-def _check_dequant_bound(tile: np.ndarray, X: np.ndarray, kind: int, bits: int):
-    """Rotated-domain error of a tile within half an RTN step times both scales."""
+def _check_dequant_bound(tile: np.ndarray, X: np.ndarray, kind: int, bits: int, rotate: int = 1):
+    """Error of a tile in its stored (rotated) domain within half an RTN step times both scales."""
     codes, a, b, s2 = oracle.unpack_tile(tile, kind, bits)
-    Xd = oracle.dequantize_tile(tile, kind, bits)
+    Xd = oracle.dequantize_tile(tile, kind, bits, rotate=rotate)
     a, b, s2 = (v.astype(np.float64) for v in (a, b, s2))
     step = np.outer(a, s2) if kind == 1 else np.outer(s2, a)
-    Xr = oracle.hadamard128(Xd)  # back to the rotated domain
-    T = oracle.hadamard128(X)
+    Xr = oracle.hadamard128(Xd) if rotate else Xd  # back to the stored domain
+    T = oracle.hadamard128(X) if rotate else X
     big = (np.abs(np.outer(b, s2)) if kind == 1 else np.abs(np.outer(s2, b))) + (1 << bits) * step
     assert np.all(np.abs(T - Xr) <= step / 2 + 1e-5 * big)
 
@@ -108,7 +109,7 @@ def _check_dequant_bound(tile: np.ndarray, X: np.ndarray, kind: int, bits: int):
 def host_cache(cache, bits=None) -> "oracle.HostCache":
     """Copy a GPU cache (paper_2606_03458_amd.kvarn.Cache) to an oracle host cache."""
     hc = oracle.HostCache(cache.batch, cache.n_kv, cache.max_blocks, bits=bits or cache.bits, n_sink=cache.n_sink,
-                          aux=cache.aux)
+                          aux=cache.aux, rotate=cache.rotate)
     hc.k_body[:] = cache.k_body.cpu().numpy()
     hc.v_body[:] = cache.v_body.cpu().numpy()
     hc.k_resid[:] = cache.k_resid.view(torch.int16).cpu().numpy().view(np.uint16)
@@ -148,7 +149,8 @@ def check_output(got: np.ndarray, ref: np.ndarray, bf16_out: bool, tol: float = 
 def host_streams(cache, streams) -> "oracle.HostCache":
     """Copy the (sequence, kv head) streams listed in `streams` of a GPU cache to an oracle host
     cache with one kv head per sequence (stream i of the list becomes sequence i)."""
-    hc = oracle.HostCache(len(streams), 1, cache.max_blocks, bits=cache.bits, n_sink=cache.n_sink, aux=cache.aux)
+    hc = oracle.HostCache(len(streams), 1, cache.max_blocks, bits=cache.bits, n_sink=cache.n_sink, aux=cache.aux,
+                          rotate=cache.rotate)
     lens = cache.seq_len.cpu().numpy()
     for i, (b, kh) in enumerate(streams):
         hc.k_body[i, 0] = cache.k_body[b, kh].cpu().numpy()

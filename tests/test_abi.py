@@ -85,7 +85,7 @@ def test_quantize_validation(K):
                              ("var_min", float("nan"), -1), ("var_min", 1e-31, -1), ("var_max", 1e31, -1),
                              ("var_max", float("inf"), -1), ("log_lo", 11.0, -1), ("log_lo", -41.0, -1),
                              ("log_hi", 41.0, -1), ("log_hi", float("nan"), -1), ("n_sink", -5, -1),
-                             ("aux_format", 2, -2), ("aux_format", -1, -2)]:
+                             ("aux_format", 2, -2), ("aux_format", -1, -2), ("rotate", 2, -1), ("rotate", -1, -1)]:
         q = K.kvarn_params_init(2)
         setattr(q, field, val)
         with pytest.raises(K.KVarNError) as e:
