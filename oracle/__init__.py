@@ -62,7 +62,7 @@ class _Cache(ctypes.Structure):
                 ("k_body", ctypes.c_void_p), ("v_body", ctypes.c_void_p),
                 ("k_resid", ctypes.c_void_p), ("v_resid", ctypes.c_void_p),
                 ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p),
-                ("seq_len", ctypes.c_void_p)]
+                ("seq_len", ctypes.c_void_p), ("block_table", ctypes.c_void_p), ("n_phys", ctypes.c_int32)]
 
 
 @dataclass
@@ -134,6 +134,9 @@ def lib():
         L.kvo_decode.argtypes = [ctypes.POINTER(_Cache), ctypes.c_int32, vp, ctypes.c_int, ctypes.c_double, vp]
         L.kvo_append.argtypes = [ctypes.POINTER(_Cache), vp, vp, ctypes.POINTER(_Params)]
         L.kvo_append.restype = ctypes.c_int
+        L.kvo_prefill.argtypes = [ctypes.POINTER(_Cache), vp, vp, ctypes.c_int, vp, ctypes.c_int32,
+                                  ctypes.POINTER(_Params)]
+        L.kvo_prefill.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -315,12 +318,16 @@ def quantize_tiles(x: np.ndarray, kind: int, params: Params = Params()) -> np.nd
 class HostCache:
     """Host copy of the cache in the shared layout (numpy arrays; bf16 held as uint16)."""
 
-    def __init__(self, batch, n_kv, max_blocks, bits=2, n_sink=0, aux=0, rotate=1):
+    def __init__(self, batch, n_kv, max_blocks, bits=2, n_sink=0, aux=0, rotate=1, n_phys=0):
+        """Dense body, or with n_phys > 0 a pool [n_phys][n_kv] of tiles and a block table
+        [batch][max_blocks] (filled with -1)."""
         tb = tile_bytes(bits, aux)
         self.batch, self.n_kv, self.max_blocks, self.bits, self.n_sink = batch, n_kv, max_blocks, bits, n_sink
-        self.aux, self.rotate = aux, rotate
-        self.k_body = np.zeros((batch, n_kv, max_blocks, tb), dtype=np.uint8)
-        self.v_body = np.zeros((batch, n_kv, max_blocks, tb), dtype=np.uint8)
+        self.aux, self.rotate, self.n_phys = aux, rotate, n_phys
+        shape = (n_phys, n_kv, tb) if n_phys > 0 else (batch, n_kv, max_blocks, tb)
+        self.k_body = np.zeros(shape, dtype=np.uint8)
+        self.v_body = np.zeros(shape, dtype=np.uint8)
+        self.block_table = np.full((batch, max_blocks), -1, dtype=np.int32) if n_phys > 0 else None
         self.k_resid = np.zeros((batch, n_kv, G, D), dtype=np.uint16)
         self.v_resid = np.zeros((batch, n_kv, G, D), dtype=np.uint16)
         self.k_sink = np.zeros((batch, n_kv, max(n_sink, 1), D), dtype=np.uint16)
@@ -331,7 +338,8 @@ class HostCache:
         return _Cache(self.batch, self.n_kv, self.max_blocks, self.n_sink, self.bits, self.aux, self.rotate,
                       self.k_body.ctypes.data, self.v_body.ctypes.data, self.k_resid.ctypes.data,
                       self.v_resid.ctypes.data, self.k_sink.ctypes.data, self.v_sink.ctypes.data,
-                      self.seq_len.ctypes.data)
+                      self.seq_len.ctypes.data,
+                      self.block_table.ctypes.data if self.block_table is not None else None, self.n_phys)
 
 
 def gather_stream(cache: HostCache, b: int, kh: int):
@@ -368,6 +376,20 @@ def append(cache: HostCache, k_new: np.ndarray, v_new: np.ndarray, params: Param
     cc = cache.c()
     pc = params.c()
     return lib().kvo_append(ctypes.byref(cc), _p(k_new), _p(v_new), ctypes.byref(pc))
+
+
+def prefill(cache: HostCache, k: np.ndarray, v: np.ndarray, cu_seqlens, max_len: int,
+            params: Params = Params()) -> int:
+    """Write whole prompts (rows cu[b] .. cu[b+1]-1 of k, v: [total][n_kv][128] fp32 or
+    bf16-as-uint16) into the cache: sink, quantized full groups, residual, seq_len."""
+    assert params.bits == cache.bits and params.aux == cache.aux and params.rotate == cache.rotate
+    assert k.dtype == v.dtype and k.dtype in (np.float32, np.uint16)
+    k, v = np.ascontiguousarray(k), np.ascontiguousarray(v)
+    cu = np.ascontiguousarray(cu_seqlens, dtype=np.int32)
+    cc = cache.c()
+    pc = params.c()
+    return lib().kvo_prefill(ctypes.byref(cc), _p(k), _p(v), 0 if k.dtype == np.float32 else 1, _p(cu), max_len,
+                             ctypes.byref(pc))
 
 
 # --------------------------------------------------------------------------------------------

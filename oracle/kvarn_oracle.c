@@ -559,7 +559,20 @@ typedef struct {
     uint8_t *k_body, *v_body;
     uint16_t *k_resid, *v_resid, *k_sink, *v_sink;
     int32_t *seq_len;
+    const int32_t *block_table; /* NULL: dense body; else [batch][max_blocks] pool block ids and
+                                   bodies [n_phys][n_kv] tiles (the paged layout) */
+    int32_t n_phys;
 } kvo_cache;
+
+/* Body tile blk of (sequence b, kv head kh): dense [batch][n_kv][max_blocks] or, paged, tile kh
+ * of pool block block_table[b][blk].  NULL for a pool id outside [0, n_phys). */
+static uint8_t *body_tile(const kvo_cache *cc, uint8_t *body, int32_t b, int32_t kh, int32_t blk) {
+    const size_t tb = kvo_tile_bytes(cc->bits, cc->aux);
+    if (!cc->block_table) return body + (((size_t)b * cc->n_kv + kh) * cc->max_blocks + blk) * tb;
+    const int32_t id = cc->block_table[(size_t)b * cc->max_blocks + blk];
+    if (id < 0 || id >= cc->n_phys) return NULL;
+    return body + ((size_t)id * cc->n_kv + kh) * tb;
+}
 
 static void region_sizes(const kvo_cache *cc, int32_t len, int32_t *n_sink_used, int32_t *n_blocks, int32_t *n_resid) {
     if (len <= cc->n_sink) {
@@ -583,7 +596,6 @@ void kvo_gather_stream(const kvo_cache *cc, int32_t bi, int32_t kh, double *K, d
     int32_t ns, nb, nr;
     region_sizes(cc, len, &ns, &nb, &nr);
     const size_t stream = (size_t)bi * cc->n_kv + kh;
-    const size_t tb = kvo_tile_bytes(cc->bits, cc->aux);
     int32_t t = 0;
     for (int32_t i = 0; i < ns; ++i, ++t)
         for (int c = 0; c < D; ++c) {
@@ -591,10 +603,10 @@ void kvo_gather_stream(const kvo_cache *cc, int32_t bi, int32_t kh, double *K, d
             V[(size_t)t * D + c] = kvo_bf16_to_double(cc->v_sink[(stream * cc->n_sink + i) * D + c]);
         }
     for (int32_t blk = 0; blk < nb; ++blk, t += G) {
-        kvo_dequantize_tile(cc->k_body + (stream * cc->max_blocks + blk) * tb, KVO_KEYS, cc->bits, cc->aux,
-                            cc->rotate, K + (size_t)t * D);
-        kvo_dequantize_tile(cc->v_body + (stream * cc->max_blocks + blk) * tb, KVO_VALUES, cc->bits, cc->aux,
-                            cc->rotate, V + (size_t)t * D);
+        kvo_dequantize_tile(body_tile(cc, cc->k_body, bi, kh, blk), KVO_KEYS, cc->bits, cc->aux, cc->rotate,
+                            K + (size_t)t * D);
+        kvo_dequantize_tile(body_tile(cc, cc->v_body, bi, kh, blk), KVO_VALUES, cc->bits, cc->aux, cc->rotate,
+                            V + (size_t)t * D);
     }
     for (int32_t i = 0; i < nr; ++i, ++t)
         for (int c = 0; c < D; ++c) {
@@ -661,7 +673,6 @@ void kvo_decode(const kvo_cache *cc, int32_t n_q, const void *q, int dtype, doub
  */
 int kvo_append(kvo_cache *cc, const uint16_t *k_new, const uint16_t *v_new, const kvo_params *p) {
     if (p->bits != cc->bits || p->aux != cc->aux || p->rotate != cc->rotate) return -1;
-    const size_t tb = kvo_tile_bytes(cc->bits, cc->aux);
     for (int32_t bi = 0; bi < cc->batch; ++bi) {
         int32_t len = cc->seq_len[bi];
         int32_t ns, nb, nr;
@@ -683,10 +694,10 @@ int kvo_append(kvo_cache *cc, const uint16_t *k_new, const uint16_t *v_new, cons
             memcpy(cc->k_resid + (stream * G + nr) * D, kn, D * 2);
             memcpy(cc->v_resid + (stream * G + nr) * D, vn, D * 2);
             if (nr + 1 == G) {
-                kvo_quantize_pack(cc->k_resid + stream * G * D, 1, D, KVO_KEYS, p,
-                                  cc->k_body + (stream * cc->max_blocks + nb) * tb);
-                kvo_quantize_pack(cc->v_resid + stream * G * D, 1, D, KVO_VALUES, p,
-                                  cc->v_body + (stream * cc->max_blocks + nb) * tb);
+                uint8_t *kt = body_tile(cc, cc->k_body, bi, kh, nb), *vt = body_tile(cc, cc->v_body, bi, kh, nb);
+                if (!kt || !vt) return -4;
+                kvo_quantize_pack(cc->k_resid + stream * G * D, 1, D, KVO_KEYS, p, kt);
+                kvo_quantize_pack(cc->v_resid + stream * G * D, 1, D, KVO_VALUES, p, vt);
             }
         }
         cc->seq_len[bi] = len + 1;
@@ -717,4 +728,50 @@ void kvo_error_decomposition(const double *K, const double *Kdq, int32_t n, doub
         EM[t] = (nk - nq) * (nk - nq);
         ED[t] = 2.0 * (nk * nq - kq);
     }
+}
+
+/*
+ * Prefill whole prompts (the bulk counterpart of appending them token by token): k, v are
+ * [total][n_kv][128] fp32 (dtype 0) or bf16 (dtype 1); sequence b owns rows cu[b] .. cu[b+1]-1.
+ * Its cache becomes: seq_len = L, the first min(L, n_sink) tokens in the sink (bf16), each full
+ * 128-token group after them quantized into body tiles 0, 1, ..., the remaining tokens in the
+ * residual (bf16).  A sequence with L > max_len or more groups than max_blocks is not written
+ * (seq_len 0) and the call returns -3; a bad pool id returns -4.
+ */
+int kvo_prefill(kvo_cache *cc, const void *k, const void *v, int dtype, const int32_t *cu, int32_t max_len,
+                const kvo_params *p) {
+    int ret = 0;
+    for (int32_t bi = 0; bi < cc->batch; ++bi) {
+        const int32_t L = cu[bi + 1] - cu[bi];
+        int32_t ns, nb, nr;
+        region_sizes(cc, L, &ns, &nb, &nr);
+        if (L < 0 || L > max_len || nb > cc->max_blocks) {
+            cc->seq_len[bi] = 0;
+            ret = -3;
+            continue;
+        }
+        for (int32_t kh = 0; kh < cc->n_kv; ++kh) {
+            const size_t stream = (size_t)bi * cc->n_kv + kh;
+            for (int32_t t = 0; t < ns + nr; ++t) { /* sink rows, then residual rows */
+                const int32_t row = t < ns ? t : L - nr + (t - ns);
+                const size_t at = ((size_t)(cu[bi] + row) * cc->n_kv + kh) * D;
+                uint16_t *kd = t < ns ? cc->k_sink + (stream * cc->n_sink + t) * D : cc->k_resid + (stream * G + t - ns) * D;
+                uint16_t *vd = t < ns ? cc->v_sink + (stream * cc->n_sink + t) * D : cc->v_resid + (stream * G + t - ns) * D;
+                for (int c = 0; c < D; ++c) {
+                    kd[c] = dtype == 0 ? kvo_double_to_bf16(((const float *)k)[at + c]) : ((const uint16_t *)k)[at + c];
+                    vd[c] = dtype == 0 ? kvo_double_to_bf16(((const float *)v)[at + c]) : ((const uint16_t *)v)[at + c];
+                }
+            }
+            const size_t esz = dtype == 0 ? 4 : 2;
+            for (int32_t blk = 0; blk < nb; ++blk) {
+                uint8_t *kt = body_tile(cc, cc->k_body, bi, kh, blk), *vt = body_tile(cc, cc->v_body, bi, kh, blk);
+                if (!kt || !vt) return -4;
+                const size_t at = ((size_t)(cu[bi] + ns + blk * G) * cc->n_kv + kh) * D;
+                kvo_quantize_pack((const uint8_t *)k + at * esz, dtype, (int64_t)cc->n_kv * D, KVO_KEYS, p, kt);
+                kvo_quantize_pack((const uint8_t *)v + at * esz, dtype, (int64_t)cc->n_kv * D, KVO_VALUES, p, vt);
+            }
+        }
+        cc->seq_len[bi] = L;
+    }
+    return ret;
 }
