@@ -111,7 +111,17 @@ typedef enum { KVARN_AUX_F32 = 0, KVARN_AUX_COMPACT = 1 } kvarn_aux_format;
  *   seq_len          [batch] int32: tokens held by each sequence (all regions)
  *   err_word         one uint32 or NULL: a kernel that finds no room sets bit 0 and drops
  *                    the write instead of writing out of bounds (a backstop only: the host
- *                    check of kvarn_append_token catches overflow from its length hint).
+ *                    check of kvarn_append_token catches overflow from its length hint); an
+ *                    invalid block id (below) sets bit 1.
+ *   block_table      NULL for the dense body above.  Otherwise the paged layout of serving
+ *                    engines: block_table is [batch][max_blocks] int32 on the device and
+ *                    k_body, v_body are pools of n_phys blocks, [n_phys][n_kv] tiles each;
+ *                    body tile blk of (sequence b, kv head h) is tile h of pool block
+ *                    block_table[b][blk].  Only the entries of tiles a call touches are read.
+ *                    An id outside [0, n_phys) sets bit 1 of err_word; decode then skips the
+ *                    sequence's body and flush / prefill do not write the tile.
+ *   n_phys           pool size in blocks, when block_table is set (pool bytes: n_phys * n_kv *
+ *                    kvarn_tile_bytes(p) for each of k_body and v_body).
  * A sequence of length L holds min(L, n_sink) sink tokens, (L - n_sink)/128 body tiles and
  * (L - n_sink) % 128 residual tokens (0 body and residual tokens while L <= n_sink). */
 typedef struct {
@@ -121,6 +131,8 @@ typedef struct {
     void *k_sink, *v_sink;
     int32_t *seq_len;
     uint32_t *err_word;
+    const int32_t *block_table;
+    int32_t n_phys;
 } kvarn_cache;
 
 /* Fill `p` with the defaults for `bits` (2 or 4; fp32 aux).  Returns KVARN_EINVAL for a null
@@ -154,6 +166,23 @@ KVARN_API int kvarn_quantize_block(const kvarn_params *p, int32_t kind, const vo
                          int64_t n_inner, int64_t x_outer_stride, int64_t x_inner_stride, int64_t x_token_stride,
                          void *out, int64_t out_outer_stride, int64_t out_inner_stride, int32_t *best_iter,
                          hipStream_t stream);
+
+/*
+ * Prefill whole prompts of different lengths in one call (the bulk write before decode):
+ *   k, v        [total_tokens][n_kv][128] in `dtype` (fp32 or bf16), unrotated, 16-byte
+ *               aligned; sequence b owns rows cu_seqlens[b] .. cu_seqlens[b+1] - 1
+ *   cu_seqlens  [batch + 1] int32 on the device: row offsets, non-decreasing, cu_seqlens[0] = 0
+ *   max_len     host bound on the prompt lengths; it sizes the launch
+ * Each sequence's contents are replaced by its prompt of length L: seq_len[b] = L, the first
+ * min(L, n_sink) tokens go to the sink, every full 128-token group after them is quantized
+ * (Fig. 2) into body tiles 0, 1, ... (through block_table when paged), and the remaining
+ * (L - n_sink) % 128 tokens go to the residual, as the same tokens appended one by one would
+ * leave them.  Sink and residual are stored as bf16.  A sequence with L > max_len or needing
+ * more than max_blocks tiles is not written: its seq_len is set to 0 and bit 0 of err_word is
+ * set.  Returns KVARN_EINVAL for null or misaligned pointers, a bad dtype or max_len < 0.
+ */
+KVARN_API int kvarn_prefill(const kvarn_params *p, const kvarn_cache *cache, const void *k, const void *v,
+                            int32_t dtype, const int32_t *cu_seqlens, int32_t max_len, hipStream_t stream);
 
 /*
  * Append one token to every (sequence, kv head) (the streaming write of Fig. 4's pseudo-decode):

@@ -38,6 +38,7 @@ int check_cache(const kvarn_params* p, const kvarn_cache* c) {
         return KVARN_EINVAL;
     if (p->n_sink > 0 && (!aligned(c->k_sink, 16) || !aligned(c->v_sink, 16))) return KVARN_EINVAL;
     if (!aligned(c->seq_len, 4)) return KVARN_EINVAL;
+    if (c->block_table && (c->n_phys <= 0 || !aligned(c->block_table, 4))) return KVARN_EINVAL;
     return KVARN_OK;
 }
 
@@ -134,6 +135,20 @@ int kvarn_append_token(const kvarn_params* p, const kvarn_cache* cache, const vo
         if (e != hipSuccess) return KVARN_EHIP;
     }
     return KVARN_OK;
+}
+
+int kvarn_prefill(const kvarn_params* p, const kvarn_cache* cache, const void* k, const void* v, int32_t dtype,
+                  const int32_t* cu_seqlens, int32_t max_len, hipStream_t stream) {
+    int st = check_params(p);
+    if (st) return st;
+    st = check_cache(p, cache);
+    if (st) return st;
+    if (check_dtype(dtype)) return KVARN_EINVAL;
+    if (!k || !v || !cu_seqlens || max_len < 0) return KVARN_EINVAL;
+    if (!aligned(k, 16) || !aligned(v, 16) || !aligned(cu_seqlens, 4)) return KVARN_EINVAL;
+    const hipError_t e = launch_prefill(qparams(p), *cache, p->n_sink, k, v, dtype == KVARN_BF16, cu_seqlens, max_len,
+                                        stream);
+    return e == hipSuccess ? KVARN_OK : KVARN_EHIP;
 }
 
 size_t kvarn_decode_workspace_bytes(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q,

@@ -46,6 +46,9 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
 
 hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream);
 
+hipError_t launch_prefill(const QParams& qp, const kvarn_cache& c, int n_sink, const void* k, const void* v,
+                          bool x_bf16, const int32_t* cu_seqlens, int max_len, hipStream_t stream);
+
 hipError_t launch_append(const kvarn_cache& c, int n_sink, const void* k_new, const void* v_new, bool bf16,
                          hipStream_t stream);
 

@@ -60,6 +60,9 @@ struct DecodeArgs {
     int n_kv, n_q, g, max_blocks, n_sink;
     int compact;       // aux format of the body tiles: 0 fp32, 1 compact (binary16 b, E4M3 a and s2)
     int rotate;        // 1: body tiles hold the Hadamard-rotated domain; 0: unrotated (ablations)
+    const int32_t* block_table;  // paged body: [batch][max_blocks] pool block ids, or null (dense)
+    int n_phys;                  // pool size in blocks (paged)
+    uint32_t* err_word;
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
     int n_split, bps;  // body splits per stream and body tiles per split
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
@@ -106,6 +109,29 @@ __device__ __forceinline__ void digits4_2(uint32_t y0, uint32_t y1, uint32_t y2,
     const uint32_t t01 = perm(y1, y0, 0x05010400u), t23 = perm(y3, y2, 0x05010400u);
     d0 = perm(t23, t01, 0x05040100u) ^ 0x80808080u;
     d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
+}
+
+// Body tile addressing.  Dense bodies: tile blk of a stream at stream * max_blocks + blk.
+// Paged bodies: tile kvh of pool block block_table[b][blk].  block_id gives what tile_index
+// takes: the block index (dense) or the pool block id (paged).
+__device__ __forceinline__ int block_id(const DecodeArgs& a, int b, int blk) {
+    return a.block_table ? a.block_table[(size_t)b * a.max_blocks + blk] : blk;
+}
+__device__ __forceinline__ size_t tile_index(const DecodeArgs& a, int stream, int kvh, int id) {
+    return a.block_table ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id;
+}
+// Paged bodies: the wave checks the pool ids of its tiles [blk0, blk1) once; an id outside the
+// pool sets bit 1 of err_word and the caller skips the body (nothing outside the pool is read).
+__device__ __forceinline__ bool body_ids_ok(const DecodeArgs& a, int b, int blk0, int blk1, int l) {
+    if (!a.block_table) return true;
+    bool bad = false;
+    for (int i = blk0 + l; i < blk1; i += 64) {
+        const int id = a.block_table[(size_t)b * a.max_blocks + i];
+        bad |= id < 0 || id >= a.n_phys;
+    }
+    if (!__any(bad)) return true;
+    if (l == 0 && a.err_word) __hip_atomic_fetch_or(a.err_word, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return false;
 }
 
 // The aux of one K tile and one V tile, as loaded by a wave: fp32 aux is 3 KB, three 16-byte
@@ -203,7 +229,8 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
     const bool last = split == a.n_split - 1;
     const int blk0 = split * a.bps;
-    const int blk1 = last ? nbody : min(blk0 + a.bps, nbody);  // the last split takes any excess
+    int blk1 = last ? nbody : min(blk0 + a.bps, nbody);  // the last split takes any excess
+    if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;    // first query head of the group
     const size_t tb = tile_bytes(BITS, a.compact), cb = code_bytes(BITS);
 
@@ -254,8 +281,9 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
         uint4 kc[2][2 * WPU], vc[2][2 * WPU];
         AuxRegs ar;
         auto load_tile = [&](int blk) {
-            const uint8_t* kt = a.k_body + ((size_t)stream * a.max_blocks + blk) * tb;
-            const uint8_t* vt = a.v_body + ((size_t)stream * a.max_blocks + blk) * tb;
+            const size_t ti = tile_index(a, stream, kvh, block_id(a, b, blk));
+            const uint8_t* kt = a.k_body + ti * tb;
+            const uint8_t* vt = a.v_body + ti * tb;
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
@@ -668,7 +696,8 @@ void k_decode4(DecodeArgs a) {
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
     const bool last = split == a.n_split - 1;
     const int blk0 = split * a.bps;
-    const int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
+    int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
+    if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
     const size_t tb = tile_bytes(BITS, a.compact), cb = code_bytes(BITS);
 
@@ -729,25 +758,29 @@ void k_decode4(DecodeArgs a) {
         // after the QK products, its value codes right after the PV products.
         uint4 kc[2][2 * WPU], vc[2][2 * WPU];
         AuxRegs ar;
-        auto tile_k = [&](int b_) { return a.k_body + ((size_t)stream * a.max_blocks + b_) * tb; };
-        auto tile_v = [&](int b_) { return a.v_body + ((size_t)stream * a.max_blocks + b_) * tb; };
-        auto load_aux = [&](int b_) { load_aux_regs(ar, tile_k(b_), tile_v(b_), cb, l, a.compact); };
+        // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
+        auto tile_k = [&](int id) { return a.k_body + tile_index(a, stream, kvh, id) * tb; };
+        auto tile_v = [&](int id) { return a.v_body + tile_index(a, stream, kvh, id) * tb; };
+        auto load_aux = [&](int id) { load_aux_regs(ar, tile_k(id), tile_v(id), cb, l, a.compact); };
         auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
                 for (int k = 0; k < 2 * WPU; ++k) c[s][k] = reinterpret_cast<const uint4*>(t)[(s * 64 + l) * 2 * WPU + k];
         };
-        load_codes(tile_k(blk0), kc);
-        load_codes(tile_v(blk0), vc);
-        load_aux(blk0);
+        const int id0 = block_id(a, b, blk0);
+        int id_next = blk0 + 1 < blk1 ? block_id(a, b, blk0 + 1) : 0;
+        load_codes(tile_k(id0), kc);
+        load_codes(tile_v(id0), vc);
+        load_aux(id0);
 
         for (int blk = blk0; blk < blk1; ++blk) {
             const bool more = blk + 1 < blk1;
+            const int id_after = blk + 2 < blk1 ? block_id(a, b, blk + 2) : 0;
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
             stage_aux(sm.aux, ar, l, a.compact);
             __syncthreads();
-            if (more) load_aux(blk + 1);
+            if (more) load_aux(id_next);
             // offsets as ratios b / a: keys per channel, values per token
             sm.aux[1][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l]);
             sm.aux[1][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l + 1]);
@@ -835,7 +868,7 @@ void k_decode4(DecodeArgs a) {
                             ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
                     }
             }
-            if (more) load_codes(tile_k(blk + 1), kc);
+            if (more) load_codes(tile_k(id_next), kc);
 
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
@@ -883,13 +916,14 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
                     for (int mt = 0; mt < 8; ++mt)
                         acc[mt] = mfma_i8(ap[sg], unit_planes<BITS>(&vw[sg][mt * WPU]), acc[mt]);
-                if (hg == NH - 1 && more) load_codes(tile_v(blk + 1), vc);
+                if (hg == NH - 1 && more) load_codes(tile_v(id_next), vc);
                 const float fp = pmx * (1.0f / (MUL * (float)QMAX));
 #pragma unroll
                 for (int mt = 0; mt < 8; ++mt)
                     orot[hg][mt] = fmaf((float)digit_sum(acc[mt]) + gam, fp * sm.aux[5][16 * mt + n],
                                         orot[hg][mt] * alpha);
             }
+            id_next = id_after;
         }
     }
 
@@ -1139,6 +1173,9 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     DecodeArgs a;
     a.compact = compact;
     a.rotate = rotate;
+    a.block_table = c.block_table;
+    a.n_phys = c.n_phys;
+    a.err_word = c.err_word;
     a.k_body = static_cast<const uint8_t*>(c.k_body);
     a.v_body = static_cast<const uint8_t*>(c.v_body);
     a.k_resid = static_cast<const uint16_t*>(c.k_resid);

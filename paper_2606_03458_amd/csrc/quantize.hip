@@ -537,6 +537,20 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
     }
 }
 
+// Body tile blk of (sequence b, kv head kh) in the cache's tiles: dense [batch][n_kv][max_blocks],
+// or paged (tile kh of pool block block_table[b][blk]).  -1 (and bit 1 of err_word) for a pool
+// id outside [0, n_phys).
+__device__ __forceinline__ int64_t body_tile(const kvarn_cache& c, int b, int kh, int blk) {
+    if (!c.block_table) return ((int64_t)b * c.n_kv + kh) * c.max_blocks + blk;
+    const int id = c.block_table[(size_t)b * c.max_blocks + blk];
+    if (id < 0 || id >= c.n_phys) {
+        if (threadIdx.x == 0 && c.err_word)
+            __hip_atomic_fetch_or(c.err_word, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return -1;
+    }
+    return (int64_t)id * c.n_kv + kh;
+}
+
 struct TileArgs {
     QParams P;
     int kind;
@@ -579,10 +593,91 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
     if (len <= a.n_sink || (len - a.n_sink) % kG != 0) return;
     const int nb = (len - a.n_sink) / kG - 1;
     if (nb >= a.c.max_blocks) return;  // the append kernel refused the token and flagged it
+    const int64_t ti = body_tile(a.c, b, (int)(stream % a.c.n_kv), nb);
+    if (ti < 0) return;
     const uint16_t* src = static_cast<const uint16_t*>(kind ? a.c.v_resid : a.c.k_resid) + (size_t)stream * kG * kD;
-    uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) +
-                   ((size_t)stream * a.c.max_blocks + nb) * tile_bytes(a.P.bits, COMPACT);
+    uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) + (size_t)ti * tile_bytes(a.P.bits, COMPACT);
     quantize_tile<COMPACT>(src, true, kD, kind, a.P, dst, nullptr, sm);
+}
+
+struct PrefillArgs {
+    QParams P;
+    kvarn_cache c;
+    int n_sink;
+    const void* k;
+    const void* v;
+    int x_bf16;
+    const int32_t* cu;  // [batch + 1] prompt offsets (rows of k, v)
+    int max_len;
+    int groups;         // body tiles per (sequence, kv head) the grid covers
+};
+
+// Prompt length of sequence b, or -1 when it cannot be written (longer than the launch bound or
+// than the body).
+__device__ __forceinline__ int prefill_len(const PrefillArgs& a, int b) {
+    const int L = a.cu[b + 1] - a.cu[b];
+    const int nb = L > a.n_sink ? (L - a.n_sink) / kG : 0;
+    return (L < 0 || L > a.max_len || nb > a.c.max_blocks) ? -1 : L;
+}
+
+// One workgroup per (sequence, kv head, K|V, body tile): quantizes the prompt's tile straight
+// from the packed rows (token stride n_kv * 128 elements).
+template <bool COMPACT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_prefill_tiles(PrefillArgs a) {
+    __shared__ QuantSmem sm;
+    const int blk = (int)(blockIdx.x % a.groups);
+    const int64_t rest = blockIdx.x / a.groups;
+    const int kind = (int)(rest & 1);
+    const int64_t stream = rest >> 1;
+    const int b = (int)(stream / a.c.n_kv), kh = (int)(stream % a.c.n_kv);
+    const int L = prefill_len(a, b);
+    if (L < 0 || blk >= (L > a.n_sink ? (L - a.n_sink) / kG : 0)) return;
+    const int64_t ti = body_tile(a.c, b, kh, blk);
+    if (ti < 0) return;
+    const size_t esz = a.x_bf16 ? 2 : 4;
+    const int64_t row = (int64_t)a.cu[b] + a.n_sink + (int64_t)blk * kG;
+    const char* src = static_cast<const char*>(kind ? a.v : a.k) + (size_t)((row * a.c.n_kv + kh) * kD) * esz;
+    uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) + (size_t)ti * tile_bytes(a.P.bits, COMPACT);
+    quantize_tile<COMPACT>(src, a.x_bf16 != 0, (int64_t)a.c.n_kv * kD, kind, a.P, dst, nullptr, sm);
+}
+
+// One workgroup per (sequence, kv head): sink and residual rows as bf16, then seq_len.
+__global__ __launch_bounds__(kThreads) void k_prefill_copy(PrefillArgs a) {
+    const int64_t stream = blockIdx.x;
+    const int b = (int)(stream / a.c.n_kv), kh = (int)(stream % a.c.n_kv);
+    const int L = prefill_len(a, b);
+    if (threadIdx.x == 0 && kh == 0) {
+        a.c.seq_len[b] = L < 0 ? 0 : L;
+        if (L < 0 && a.c.err_word)
+            __hip_atomic_fetch_or(a.c.err_word, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    if (L < 0) return;
+    const int ns = min(L, a.n_sink);
+    const int nr = L > a.n_sink ? (L - a.n_sink) % kG : 0;
+    const int r0 = L - nr;  // first residual row of the prompt
+    // rows [0, ns) -> sink, rows [r0, L) -> residual; 2 rows of 128 channels per pass
+    for (int i = threadIdx.x; i < (ns + nr) * kD; i += kThreads) {
+        const int t = i / kD, c = i % kD;
+        const int row = t < ns ? t : r0 + (t - ns);
+        const size_t at = ((size_t)(a.cu[b] + row) * a.c.n_kv + kh) * kD + c;
+        uint16_t kb, vb;
+        if (a.x_bf16) {
+            kb = static_cast<const uint16_t*>(a.k)[at];
+            vb = static_cast<const uint16_t*>(a.v)[at];
+        } else {
+            kb = f32_to_bf16(static_cast<const float*>(a.k)[at]);
+            vb = f32_to_bf16(static_cast<const float*>(a.v)[at]);
+        }
+        if (t < ns) {
+            const size_t o = ((size_t)stream * a.n_sink + t) * kD + c;
+            static_cast<uint16_t*>(a.c.k_sink)[o] = kb;
+            static_cast<uint16_t*>(a.c.v_sink)[o] = vb;
+        } else {
+            const size_t o = ((size_t)stream * kG + (t - ns)) * kD + c;
+            static_cast<uint16_t*>(a.c.k_resid)[o] = kb;
+            static_cast<uint16_t*>(a.c.v_resid)[o] = vb;
+        }
+    }
 }
 
 }  // namespace
@@ -604,6 +699,26 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+hipError_t launch_prefill(const QParams& qp, const kvarn_cache& c, int n_sink, const void* k, const void* v,
+                          bool x_bf16, const int32_t* cu_seqlens, int max_len, hipStream_t stream) {
+    int groups = max_len > n_sink ? (max_len - n_sink) / kG : 0;
+    if (groups > c.max_blocks) groups = c.max_blocks;
+    PrefillArgs a{qp, c, n_sink, k, v, x_bf16 ? 1 : 0, cu_seqlens, max_len, groups > 0 ? groups : 1};
+    const int64_t streams = (int64_t)c.batch * c.n_kv;
+    if (groups > 0) {
+        const int64_t n = streams * 2 * groups;
+        if (n >= (int64_t)1 << 31) return hipErrorInvalidValue;
+        if (qp.compact)
+            hipLaunchKernelGGL(k_prefill_tiles<true>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        else
+            hipLaunchKernelGGL(k_prefill_tiles<false>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(k_prefill_copy, dim3((unsigned)streams), dim3(kThreads), 0, stream, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream) {

@@ -18,7 +18,7 @@ KVARN_KEYS, KVARN_VALUES = 0, 1
 KVARN_AUX_F32, KVARN_AUX_COMPACT = 0, 1
 STATUS = {0: "KVARN_OK", -1: "KVARN_EINVAL", -2: "KVARN_EUNSUPPORTED", -3: "KVARN_ECAPACITY", -4: "KVARN_EHIP",
           -5: "KVARN_EWORKSPACE"}
-EXPORTS = ("kvarn_params_init", "kvarn_tile_bytes", "kvarn_cache_sizes", "kvarn_quantize_block",
+EXPORTS = ("kvarn_params_init", "kvarn_tile_bytes", "kvarn_cache_sizes", "kvarn_quantize_block", "kvarn_prefill",
            "kvarn_append_token", "kvarn_decode_workspace_bytes", "kvarn_decode_attention")
 
 
@@ -38,7 +38,8 @@ class kvarn_cache(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_kv", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
                 ("k_body", ctypes.c_void_p), ("v_body", ctypes.c_void_p), ("k_resid", ctypes.c_void_p),
                 ("v_resid", ctypes.c_void_p), ("k_sink", ctypes.c_void_p), ("v_sink", ctypes.c_void_p),
-                ("seq_len", ctypes.c_void_p), ("err_word", ctypes.c_void_p)]
+                ("seq_len", ctypes.c_void_p), ("err_word", ctypes.c_void_p), ("block_table", ctypes.c_void_p),
+                ("n_phys", ctypes.c_int32)]
 
 
 _lib = None
@@ -67,6 +68,8 @@ def lib():
         L.kvarn_quantize_block.argtypes = [P, i32, vp, i32, i64, i64, i64, i64, i64, vp, i64, i64, vp, vp]
         L.kvarn_quantize_block.restype = ctypes.c_int
         L.kvarn_append_token.argtypes = [P, C, vp, vp, i32, i32, vp]
+        L.kvarn_prefill.argtypes = [P, C, vp, vp, i32, vp, i32, vp]
+        L.kvarn_prefill.restype = ctypes.c_int
         L.kvarn_append_token.restype = ctypes.c_int
         L.kvarn_decode_workspace_bytes.argtypes = [P, C, i32, i32]
         L.kvarn_decode_workspace_bytes.restype = sz
@@ -134,6 +137,13 @@ def kvarn_quantize_block(p: kvarn_params, kind: int, x, x_dtype: int, n_outer: i
     _check("kvarn_quantize_block", st)
 
 
+def kvarn_prefill(p: kvarn_params, cache: "Cache", k, v, dtype: int, cu_seqlens, max_len: int, stream=None) -> None:
+    d = cache.desc()
+    st = lib().kvarn_prefill(ctypes.byref(p), ctypes.byref(d), _ptr(k), _ptr(v), dtype, _ptr(cu_seqlens), max_len,
+                             _stream(stream))
+    _check("kvarn_prefill", st)
+
+
 def kvarn_append_token(p: kvarn_params, cache: "Cache", k_new, v_new, dtype: int, host_len_before: int,
                        stream=None) -> None:
     d = cache.desc()
@@ -163,14 +173,19 @@ def kvarn_decode_attention(p: kvarn_params, cache: "Cache", n_q: int, q, q_dtype
 class Cache:
     """Caller-owned cache buffers in the layout of kvarn.h, allocated with torch."""
 
-    def __init__(self, p: kvarn_params, batch: int, n_kv: int, max_blocks: int, device="cuda"):
+    def __init__(self, p: kvarn_params, batch: int, n_kv: int, max_blocks: int, device="cuda", n_phys: int = 0):
+        """Dense body [batch][n_kv][max_blocks] tiles, or, with n_phys > 0, a paged pool
+        [n_phys][n_kv] tiles plus a block table [batch][max_blocks] (filled with -1: the
+        caller assigns pool blocks)."""
         sizes = kvarn_cache_sizes(p, batch, n_kv, max_blocks)
         self.batch, self.n_kv, self.max_blocks, self.bits, self.n_sink = batch, n_kv, max_blocks, p.bits, p.n_sink
-        self.aux, self.rotate = p.aux_format, p.rotate
+        self.aux, self.rotate, self.n_phys = p.aux_format, p.rotate, n_phys
         tb = kvarn_tile_bytes(p)
         u8 = dict(dtype=torch.uint8, device=device)
-        self.k_body = torch.zeros((batch, n_kv, max_blocks, tb), **u8)
-        self.v_body = torch.zeros((batch, n_kv, max_blocks, tb), **u8)
+        body_shape = (n_phys, n_kv, tb) if n_phys > 0 else (batch, n_kv, max_blocks, tb)
+        self.k_body = torch.zeros(body_shape, **u8)
+        self.v_body = torch.zeros(body_shape, **u8)
+        self.block_table = torch.full((batch, max_blocks), -1, dtype=torch.int32, device=device) if n_phys > 0 else None
         self.k_resid = torch.zeros((batch, n_kv, 128, 128), dtype=torch.bfloat16, device=device)
         self.v_resid = torch.zeros((batch, n_kv, 128, 128), dtype=torch.bfloat16, device=device)
         ns = max(p.n_sink, 0)
@@ -178,12 +193,12 @@ class Cache:
         self.v_sink = torch.zeros((batch, n_kv, ns, 128), dtype=torch.bfloat16, device=device) if ns else None
         self.seq_len = torch.zeros(batch, dtype=torch.int32, device=device)
         self.err_word = torch.zeros(1, dtype=torch.int32, device=device)
-        assert self.k_body.numel() == sizes[0] and self.k_resid.numel() * 2 == sizes[2]
+        assert (n_phys > 0 or self.k_body.numel() == sizes[0]) and self.k_resid.numel() * 2 == sizes[2]
 
     def desc(self) -> kvarn_cache:
         return kvarn_cache(self.batch, self.n_kv, self.max_blocks, _ptr(self.k_body), _ptr(self.v_body),
                            _ptr(self.k_resid), _ptr(self.v_resid), _ptr(self.k_sink), _ptr(self.v_sink),
-                           _ptr(self.seq_len), _ptr(self.err_word))
+                           _ptr(self.seq_len), _ptr(self.err_word), _ptr(self.block_table), self.n_phys)
 
 
 def quantize_into_body(p: kvarn_params, kind: int, x: torch.Tensor, body: torch.Tensor, block0: int = 0,
