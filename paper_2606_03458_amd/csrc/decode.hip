@@ -524,15 +524,22 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                     oplain[h][1] *= al;
                 }
             }
-            for (int t = 0; t < cn; ++t) {
-                const uint32_t v2 = reinterpret_cast<const uint32_t*>(Vp + (size_t)t * kD)[l];
-                const float v0 = __uint_as_float(v2 << 16), v1 = __uint_as_float(v2 & 0xFFFF0000u);
+            // rows in batches of 8 with all loads in flight; rows >= cn read as zero (their p is 0)
+            for (int t = 0; t < cn; t += 8) {
+                uint32_t v2[8];
 #pragma unroll
-                for (int h = 0; h < GQ; ++h) {
-                    if (h < g) {
-                        const float ph = sm.p[h][t];
-                        oplain[h][0] = fmaf(ph, v0, oplain[h][0]);
-                        oplain[h][1] = fmaf(ph, v1, oplain[h][1]);
+                for (int u = 0; u < 8; ++u)
+                    v2[u] = t + u < cn ? reinterpret_cast<const uint32_t*>(Vp + (size_t)(t + u) * kD)[l] : 0u;
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const float v0 = __uint_as_float(v2[u] << 16), v1 = __uint_as_float(v2[u] & 0xFFFF0000u);
+#pragma unroll
+                    for (int h = 0; h < GQ; ++h) {
+                        if (h < g) {
+                            const float ph = sm.p[h][t + u];
+                            oplain[h][0] = fmaf(ph, v0, oplain[h][0]);
+                            oplain[h][1] = fmaf(ph, v1, oplain[h][1]);
+                        }
                     }
                 }
             }
@@ -998,15 +1005,22 @@ void k_decode4(DecodeArgs a) {
                     oplain[hh][1] *= al;
                 }
             }
-            for (int t = 0; t < cn; ++t) {
-                const uint32_t v2 = reinterpret_cast<const uint32_t*>(Vp + (size_t)t * kD)[l];
-                const float v0 = __uint_as_float(v2 << 16), v1 = __uint_as_float(v2 & 0xFFFF0000u);
+            // rows in batches of 8 with all loads in flight; rows >= cn read as zero (their p is 0)
+            for (int t = 0; t < cn; t += 8) {
+                uint32_t v2[8];
 #pragma unroll
-                for (int hh = 0; hh < NHD; ++hh) {
-                    if (hh < g) {
-                        const float ph = sm.p[hh][t];
-                        oplain[hh][0] = fmaf(ph, v0, oplain[hh][0]);
-                        oplain[hh][1] = fmaf(ph, v1, oplain[hh][1]);
+                for (int u = 0; u < 8; ++u)
+                    v2[u] = t + u < cn ? reinterpret_cast<const uint32_t*>(Vp + (size_t)(t + u) * kD)[l] : 0u;
+#pragma unroll
+                for (int u = 0; u < 8; ++u) {
+                    const float v0 = __uint_as_float(v2[u] << 16), v1 = __uint_as_float(v2[u] & 0xFFFF0000u);
+#pragma unroll
+                    for (int hh = 0; hh < NHD; ++hh) {
+                        if (hh < g) {
+                            const float ph = sm.p[hh][t + u];
+                            oplain[hh][0] = fmaf(ph, v0, oplain[hh][0]);
+                            oplain[hh][1] = fmaf(ph, v1, oplain[hh][1]);
+                        }
                     }
                 }
             }

@@ -96,9 +96,10 @@ def test_quantize_validation(K):
 class _HostCache:
     """kvarn_cache descriptor over host addresses (validation only)."""
 
-    def __init__(self, K, batch=2, n_kv=2, max_blocks=1, sink=False):
+    def __init__(self, K, batch=2, n_kv=2, max_blocks=1, sink=False, table=None, n_phys=0):
         self.keep = []
         self.batch, self.n_kv, self.max_blocks = batch, n_kv, max_blocks
+        self.table, self.n_phys = table, n_phys
         ptrs = []
         for _ in range(7):
             b, a = _fake(1024)
@@ -111,7 +112,8 @@ class _HostCache:
         from paper_2606_03458_amd.kvarn import kvarn_cache
         p = self.ptrs
         return kvarn_cache(self.batch, self.n_kv, self.max_blocks, p[0], p[1], p[2], p[3],
-                           p[4] if self.sink else None, p[5] if self.sink else None, p[6], None)
+                           p[4] if self.sink else None, p[5] if self.sink else None, p[6], None, self.table,
+                           self.n_phys)
 
 
 def test_append_validation(K):
@@ -168,3 +170,26 @@ def test_no_cpu_fallback(K, monkeypatch, tmp_path):
     monkeypatch.setattr(mod, "_lib", None)
     with pytest.raises(ImportError):
         mod.lib()
+
+
+def test_prefill_validation(K):
+    p = K.kvarn_params_init(2)
+    c = _HostCache(K)
+    keep, buf = _fake(4096)
+    for args, code in [((None, buf, 1, buf, 10), -1), ((buf, None, 1, buf, 10), -1), ((buf, buf, 3, buf, 10), -1),
+                       ((buf, buf, 1, None, 10), -1), ((buf, buf, 1, buf, -1), -1), ((buf + 8, buf, 1, buf, 10), -1),
+                       ((buf, buf, 1, buf + 2, 10), -1)]:
+        with pytest.raises(K.KVarNError) as e:
+            K.kvarn_prefill(p, c, *args, stream=0)
+        assert e.value.status == code, args
+
+
+def test_paged_cache_validation(K):
+    """A block table needs a positive pool size and 4-byte alignment (checked before launch)."""
+    p = K.kvarn_params_init(2)
+    keep, tok = _fake(4096)
+    for table, n_phys in [(tok, 0), (tok + 2, 4)]:
+        c = _HostCache(K, table=table, n_phys=n_phys)
+        with pytest.raises(K.KVarNError) as e:
+            K.kvarn_append_token(p, c, tok, tok, 1, 0, stream=0)
+        assert e.value.status == -1, (table, n_phys)
