@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import check_output, compare_tiles, host_streams, q_to_host, tiles_to_host
+from gpu_util import check_output, compare_tiles, compare_tiles_compact, host_streams, q_to_host, tiles_to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -24,11 +24,12 @@ def K():
     return kvarn
 
 
-def _run(K, name, n_append, n_streams, n_tiles, out_dtype):
+def _run(K, name, n_append, n_streams, n_tiles, out_dtype, aux=0):
     from paper_2606_03458_amd import datagen, workloads
     spec = datagen.WORKLOADS[name]
     seed = datagen.SEEDS[name]
-    built, inputs = workloads.build(name, extra_blocks=(n_append + 127) // 128 + 1, best_iter=True)
+    built, inputs = workloads.build(name, extra_blocks=(n_append + 127) // 128 + 1, best_iter=True, aux=aux)
+    compare = compare_tiles_compact if aux else compare_tiles
     p, cache = built.params, built.cache
     T0 = built.length
     appended = []
@@ -77,7 +78,7 @@ def _run(K, name, n_append, n_streams, n_tiles, out_dtype):
             xs = torch.stack([X[b, kh, t * 128:(t + 1) * 128] for b, kh, t in sel])
             tiles = torch.stack([body[layer * B + b, kh, t] for b, kh, t in sel]).cpu().numpy()
             bi = np.array([int(best[(b * n_kv + kh) * nb + t]) for b, kh, t in sel])
-            stats.append(compare_tiles(tiles, tiles_to_host(xs), kind, p.bits, gpu_best=bi))
+            stats.append(compare(tiles, tiles_to_host(xs), kind, p.bits, gpu_best=bi))
         del Kx, Vx
     if n_append >= 128:
         kst = torch.stack([k for k, _ in appended])  # [128, L*B, n_kv, 128]
@@ -85,7 +86,7 @@ def _run(K, name, n_append, n_streams, n_tiles, out_dtype):
         for kind, X, body in ((K.KVARN_KEYS, kst, cache.k_body), (K.KVARN_VALUES, vst, cache.v_body)):
             xs = torch.stack([X[:, b, kh] for b, kh in streams[:n_tiles]])
             tiles = torch.stack([body[b, kh, nb] for b, kh in streams[:n_tiles]]).cpu().numpy()
-            stats.append(compare_tiles(tiles, tiles_to_host(xs), kind, p.bits))
+            stats.append(compare(tiles, tiles_to_host(xs), kind, p.bits))
     return worst, stats
 
 
@@ -98,3 +99,8 @@ def test_full_size_throughput(K):
 def test_full_size_stress(K):
     """Heavy-tailed keys, 40 q / 8 kv heads (GQA 5), batch 128, 16384-token 2-bit cache."""
     _run(K, "stress", n_append=130, n_streams=40, n_tiles=12, out_dtype=torch.float32)
+
+
+def test_full_size_throughput_compact(K):
+    """The throughput workload with the compact aux format (2.25 bits/element)."""
+    _run(K, "throughput", n_append=130, n_streams=40, n_tiles=12, out_dtype=torch.bfloat16, aux=1)
