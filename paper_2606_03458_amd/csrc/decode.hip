@@ -35,6 +35,7 @@ namespace {
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned v4u __attribute__((ext_vector_type(4)));
 
 constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
 
@@ -111,6 +112,12 @@ __device__ __forceinline__ void digits4_2(uint32_t y0, uint32_t y1, uint32_t y2,
     d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
 }
 
+// Body tiles are read once per decode step: non-temporal 16-byte loads stream them from HBM
+// faster than ordinary loads and leave the caches to reused data.
+__device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
+    return __builtin_bit_cast(uint4, __builtin_nontemporal_load(reinterpret_cast<const v4u*>(p)));
+}
+
 // Body tile addressing.  Dense bodies: tile blk of a stream at stream * max_blocks + blk.
 // Paged bodies: tile kvh of pool block block_table[b][blk].  block_id gives what tile_index
 // takes: the block index (dense) or the pool block id (paged).
@@ -143,11 +150,12 @@ struct AuxRegs {
 __device__ __forceinline__ void load_aux_regs(AuxRegs& r, const uint8_t* kt, const uint8_t* vt, size_t cb, int l,
                                               int compact) {
     if (compact) {
-        r.p0 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + (l & 31) * 16);
+        r.p0 = load_stream((l < 32 ? kt : vt) + cb + (l & 31) * 16);
+        r.p1 = r.p2 = r.p0;  // unused
     } else {
-        r.p0 = *reinterpret_cast<const uint4*>(kt + cb + l * 16);
-        r.p1 = *reinterpret_cast<const uint4*>((l < 32 ? kt : vt) + cb + (l < 32 ? (64 + l) * 16 : (l - 32) * 16));
-        r.p2 = *reinterpret_cast<const uint4*>(vt + cb + (32 + l) * 16);
+        r.p0 = load_stream(kt + cb + l * 16);
+        r.p1 = load_stream((l < 32 ? kt : vt) + cb + (l < 32 ? (64 + l) * 16 : (l - 32) * 16));
+        r.p2 = load_stream(vt + cb + (32 + l) * 16);
     }
 }
 // Loaded aux -> fp32 rows a_K b_K s2_K a_V b_V s2_V in LDS.  A compact piece is 8 binary16
@@ -288,8 +296,8 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
             for (int s = 0; s < 2; ++s)
 #pragma unroll
                 for (int k = 0; k < 2 * WPU; ++k) {
-                    kc[s][k] = reinterpret_cast<const uint4*>(kt)[(s * 64 + l) * 2 * WPU + k];
-                    vc[s][k] = reinterpret_cast<const uint4*>(vt)[(s * 64 + l) * 2 * WPU + k];
+                    kc[s][k] = load_stream(kt + 16 * ((s * 64 + l) * 2 * WPU + k));
+                    vc[s][k] = load_stream(vt + 16 * ((s * 64 + l) * 2 * WPU + k));
                 }
             load_aux_regs(ar, kt, vt, cb, l, a.compact);
         };
@@ -773,7 +781,7 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = reinterpret_cast<const uint4*>(t)[(s * 64 + l) * 2 * WPU + k];
+                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * ((s * 64 + l) * 2 * WPU + k));
         };
         const int id0 = block_id(a, b, blk0);
         int id_next = blk0 + 1 < blk1 ? block_id(a, b, blk0 + 1) : 0;
@@ -915,20 +923,15 @@ void k_decode4(DecodeArgs a) {
                 const float gam = row_sum(fmaf(gam_o, MUL, gam_e));  // MUL grid steps
 
                 // PV: head 4*hg + G, channel 16*mt + n
-                v4i acc[8];
-#pragma unroll
-                for (int mt = 0; mt < 8; ++mt) acc[mt] = v4i{0, 0, 0, 0};
-#pragma unroll
-                for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                    for (int mt = 0; mt < 8; ++mt)
-                        acc[mt] = mfma_i8(ap[sg], unit_planes<BITS>(&vw[sg][mt * WPU]), acc[mt]);
-                if (hg == NH - 1 && more) load_codes(tile_v(id_next), vc);
                 const float fp = pmx * (1.0f / (MUL * (float)QMAX));
 #pragma unroll
-                for (int mt = 0; mt < 8; ++mt)
-                    orot[hg][mt] = fmaf((float)digit_sum(acc[mt]) + gam, fp * sm.aux[5][16 * mt + n],
+                for (int mt = 0; mt < 8; ++mt) {
+                    v4i acc = mfma_i8(ap[0], unit_planes<BITS>(&vw[0][mt * WPU]), v4i{0, 0, 0, 0});
+                    acc = mfma_i8(ap[1], unit_planes<BITS>(&vw[1][mt * WPU]), acc);
+                    orot[hg][mt] = fmaf((float)digit_sum(acc) + gam, fp * sm.aux[5][16 * mt + n],
                                         orot[hg][mt] * alpha);
+                }
+                if (hg == NH - 1 && more) load_codes(tile_v(id_next), vc);
             }
             id_next = id_after;
         }
