@@ -147,11 +147,11 @@ __device__ __forceinline__ bool body_ids_ok(const DecodeArgs& a, int b, int blk0
 struct AuxRegs {
     uint4 p0, p1, p2;
 };
-__device__ __forceinline__ void load_aux_regs(AuxRegs& r, const uint8_t* kt, const uint8_t* vt, size_t cb, int l,
-                                              int compact) {
-    if (compact) {
+template <int CMP>
+__device__ __forceinline__ void load_aux_regs(AuxRegs& r, const uint8_t* kt, const uint8_t* vt, size_t cb, int l) {
+    if constexpr (CMP) {
         r.p0 = load_stream((l < 32 ? kt : vt) + cb + (l & 31) * 16);
-        r.p1 = r.p2 = r.p0;  // unused
+        r.p1 = r.p2 = make_uint4(0u, 0u, 0u, 0u);  // unused
     } else {
         r.p0 = load_stream(kt + cb + l * 16);
         r.p1 = load_stream((l < 32 ? kt : vt) + cb + (l < 32 ? (64 + l) * 16 : (l - 32) * 16));
@@ -161,8 +161,9 @@ __device__ __forceinline__ void load_aux_regs(AuxRegs& r, const uint8_t* kt, con
 // Loaded aux -> fp32 rows a_K b_K s2_K a_V b_V s2_V in LDS.  A compact piece is 8 binary16
 // offsets (pieces 0-15 of a tile) or 16 E4M3 scales (pieces 16-23: a, 24-31: s2); both
 // conversions are exact.
-__device__ __forceinline__ void stage_aux(float (&aux)[6][kD], const AuxRegs& r, int l, int compact) {
-    if (!compact) {
+template <int CMP>
+__device__ __forceinline__ void stage_aux(float (&aux)[6][kD], const AuxRegs& r, int l) {
+    if constexpr (!CMP) {
         reinterpret_cast<uint4*>(&aux[0][0])[l] = r.p0;
         reinterpret_cast<uint4*>(&aux[0][0])[l + 64] = r.p1;
         reinterpret_cast<uint4*>(&aux[0][0])[l + 128] = r.p2;
@@ -216,7 +217,60 @@ __device__ __forceinline__ void lds_hadamard(float (&x)[GQ][kD], int g) {
     }
 }
 
-template <int BITS, int GQ>
+// Query rows qrow .. qrow + g - 1 into LDS rows 0 .. NR - 1 (rows >= g zero): lane l writes
+// channels 2l, 2l + 1 of every row.  One branch on the dtype, so every load is in flight before
+// the first is used (q is only 4-byte aligned).
+template <int NR>
+__device__ __forceinline__ void q_to_lds(float (&q)[NR][kD], const DecodeArgs& a, size_t qrow, int g, int l) {
+    float v0[NR], v1[NR];
+    if (a.q_bf16) {
+        const uint32_t* q2 = static_cast<const uint32_t*>(a.q);
+#pragma unroll
+        for (int h = 0; h < NR; ++h) {
+            const uint32_t w = q2[(qrow + min(h, g - 1)) * (kD / 2) + l];
+            v0[h] = __uint_as_float(w << 16);
+            v1[h] = __uint_as_float(w & 0xFFFF0000u);
+        }
+    } else {
+        const float* q1 = static_cast<const float*>(a.q);
+#pragma unroll
+        for (int h = 0; h < NR; ++h) {
+            const size_t i = (qrow + min(h, g - 1)) * kD + 2 * l;
+            v0[h] = q1[i];
+            v1[h] = q1[i + 1];
+        }
+    }
+#pragma unroll
+    for (int h = 0; h < NR; ++h) {
+        q[h][2 * l] = h < g ? v0[h] : 0.f;
+        q[h][2 * l + 1] = h < g ? v1[h] : 0.f;
+    }
+}
+
+// NB runs of 8 consecutive query values, run r starting at element idx[r] (a multiple of 8), with
+// one branch on the dtype.
+template <int NB>
+__device__ __forceinline__ void load_q_runs(const DecodeArgs& a, const size_t (&idx)[NB], float (&v)[NB][8]) {
+    if (a.q_bf16) {
+        const uint32_t* q2 = static_cast<const uint32_t*>(a.q);
+#pragma unroll
+        for (int r = 0; r < NB; ++r)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const uint32_t w = q2[idx[r] / 2 + e];
+                v[r][2 * e] = __uint_as_float(w << 16);
+                v[r][2 * e + 1] = __uint_as_float(w & 0xFFFF0000u);
+            }
+    } else {
+        const float* q1 = static_cast<const float*>(a.q);
+#pragma unroll
+        for (int r = 0; r < NB; ++r)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[r][e] = q1[idx[r] + e];
+    }
+}
+
+template <int BITS, int GQ, int CMP>
 __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     __shared__ Smem<GQ> sm;
     constexpr int WPU = BITS / 2;                        // words per 16-code unit
@@ -240,7 +294,7 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     int blk1 = last ? nbody : min(blk0 + a.bps, nbody);  // the last split takes any excess
     if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;    // first query head of the group
-    const size_t tb = tile_bytes(BITS, a.compact), cb = code_bytes(BITS);
+    const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
 
     float m_run = -INFINITY, l_run = 0.f;  // per head n; l_run is this lane's partial sum
     float orot[8][4];                      // head n, channel 16*mt + 4*G + i (rotated domain)
@@ -251,10 +305,6 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
         for (int i = 0; i < 4; ++i) orot[mt][i] = 0.f;
 #pragma unroll
     for (int h = 0; h < GQ; ++h) oplain[h][0] = oplain[h][1] = 0.f;
-
-    auto load_q = [&](size_t idx) -> float {
-        return a.q_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.q)[idx]) : static_cast<const float*>(a.q)[idx];
-    };
 
     // Online-softmax step shared by body tiles and bf16 chunks: lg holds 32 logits of head n
     // (log2 units, -inf for absent tokens); turns lg into p and returns the rescale factor.
@@ -277,15 +327,10 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     };
 
     if (blk0 < blk1) {
-        for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] = load_q(qrow * kD + idx);
-        __syncthreads();
-        if (a.rotate) {
-            lds_hadamard<GQ>(sm.q, g);
-            for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
-        }
-
         // Lane l's part of a tile: its K and V code units (32*WPU bytes per 64-token half) and
-        // its pieces of the aux.
+        // its pieces of the aux.  The first tile's loads go out before the query set-up; the
+        // prefetch of the next tile is unconditional (past the last tile it re-reads it) so that
+        // no load sits behind a branch.
         uint4 kc[2][2 * WPU], vc[2][2 * WPU];
         AuxRegs ar;
         auto load_tile = [&](int blk) {
@@ -299,13 +344,20 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                     kc[s][k] = load_stream(kt + 16 * ((s * 64 + l) * 2 * WPU + k));
                     vc[s][k] = load_stream(vt + 16 * ((s * 64 + l) * 2 * WPU + k));
                 }
-            load_aux_regs(ar, kt, vt, cb, l, a.compact);
+            load_aux_regs<CMP>(ar, kt, vt, cb, l);
         };
         load_tile(blk0);
 
+        q_to_lds<GQ>(sm.q, a, qrow, g, l);
+        __syncthreads();
+        if (a.rotate) {
+            lds_hadamard<GQ>(sm.q, g);
+            for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
+        }
+
         for (int blk = blk0; blk < blk1; ++blk) {
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp
-            stage_aux(sm.aux, ar, l, a.compact);
+            stage_aux<CMP>(sm.aux, ar, l);
             uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -316,7 +368,7 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                     vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
                     vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
                 }
-            if (blk + 1 < blk1) load_tile(blk + 1);  // prefetch, consumed next iteration
+            load_tile(min(blk + 1, blk1 - 1));  // prefetch, consumed next iteration
             __syncthreads();
             // value offsets as ratios b_V / a_V (read after the next barrier)
             sm.aux[4][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l]);
@@ -469,15 +521,21 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     if (last && ns + nr > 0) {
         // q as the bf16 B operand (hi, plus lo when q is fp32): lane (G, n) holds q[n][32k + 8G ..]
         v8bf qh[4], ql[4];
+        {
+            size_t qi[4];
+            float qv[4][8];
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
+            for (int k = 0; k < 4; ++k) qi[k] = (qrow + min(hn, g - 1)) * kD + 32 * k + 8 * G;
+            load_q_runs<4>(a, qi, qv);
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const float v = head_lane ? load_q((qrow + hn) * kD + 32 * k + 8 * G + e) : 0.f;
-                const __bf16 hi = (__bf16)v;
-                qh[k][e] = hi;
-                ql[k][e] = (__bf16)(v - (float)hi);
-            }
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float v = head_lane ? qv[k][e] : 0.f;
+                    const __bf16 hi = (__bf16)v;
+                    qh[k][e] = hi;
+                    ql[k][e] = (__bf16)(v - (float)hi);
+                }
         }
         const bool two = !a.q_bf16;
         const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
@@ -494,11 +552,11 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
 #pragma unroll
             for (int tau = 0; tau < 8; ++tau) {
                 v4f acc = {0.f, 0.f, 0.f, 0.f};
-                const int arow = 16 * tau + (l & 15);  // A row of this lane
+                // A row of this lane; rows past the chunk read its last row (their logits are masked)
+                const int arow = min(16 * tau + (l & 15), cn - 1);
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    uint4 u = {0u, 0u, 0u, 0u};
-                    if (arow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)arow * kD + 32 * k + 8 * G);
+                    const uint4 u = *reinterpret_cast<const uint4*>(Kp + (size_t)arow * kD + 32 * k + 8 * G);
                     v8bf A;
                     __builtin_memcpy(&A, &u, 16);
                     acc = mfma_bf16(A, qh[k], acc);
@@ -532,14 +590,15 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
                     oplain[h][1] *= al;
                 }
             }
-            // rows in batches of 8 with all loads in flight; rows >= cn read as zero (their p is 0)
-            for (int t = 0; t < cn; t += 8) {
-                uint32_t v2[8];
+            // rows in batches of 32 with all loads in flight; rows past the chunk read its last
+            // row (their p is 0)
+            for (int t = 0; t < cn; t += 32) {
+                uint32_t v2[32];
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    v2[u] = t + u < cn ? reinterpret_cast<const uint32_t*>(Vp + (size_t)(t + u) * kD)[l] : 0u;
+                for (int u = 0; u < 32; ++u)
+                    v2[u] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t + u, cn - 1) * kD)[l];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
+                for (int u = 0; u < 32; ++u) {
                     const float v0 = __uint_as_float(v2[u] << 16), v1 = __uint_as_float(v2[u] & 0xFFFF0000u);
 #pragma unroll
                     for (int h = 0; h < GQ; ++h) {
@@ -685,7 +744,7 @@ struct Smem4 {
     float p[4 * NH][kG];       // probabilities of a bf16 chunk (sink / residual)
 };
 
-template <int BITS, int NH>
+template <int BITS, int NH, int CMP>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
     __shared__ Smem4<NH> sm;
@@ -714,7 +773,7 @@ void k_decode4(DecodeArgs a) {
     int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
     if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
-    const size_t tb = tile_bytes(BITS, a.compact), cb = code_bytes(BITS);
+    const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
 
     float m_run[NH], l_run[NH];  // head 4*hg + G; l_run is this lane's partial sum
     float orot[NH][8];           // head 4*hg + G, channel 16*mt + n (rotated domain)
@@ -726,9 +785,6 @@ void k_decode4(DecodeArgs a) {
         for (int mt = 0; mt < 8; ++mt) orot[hg][mt] = 0.f;
     }
 
-    auto load_q = [&](size_t idx) -> float {
-        return a.q_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(a.q)[idx]) : static_cast<const float*>(a.q)[idx];
-    };
     // online softmax of group hg over this lane's 8 logits (log2 units; -inf = absent) -> p,
     // returns alpha
     auto softmax_update = [](float (&lg)[8], bool maybe_absent, float& m, float& lsum) -> float {
@@ -752,8 +808,32 @@ void k_decode4(DecodeArgs a) {
     };
 
     if (blk0 < blk1) {
-        for (int idx = l; idx < NHD * kD; idx += 64)
-            sm.q[idx >> 7][idx & 127] = idx < g * kD ? load_q(qrow * kD + idx) : 0.f;
+        // One register buffer per tile part, refilled as soon as its current contents are
+        // consumed: the next tile's aux right after it is staged in LDS, its key codes right
+        // after the QK products, its value codes right after the PV products.  The first tile's
+        // loads go out before the query set-up.  The aux prefetch is unconditional (past the
+        // last tile it re-reads that tile's aux) so that it never waits behind a branch; the
+        // code prefetches are too, except in the 2-bit single-group variant, which schedules
+        // best (measured) with them skipped after the last tile.
+        uint4 kc[2][2 * WPU], vc[2][2 * WPU];
+        AuxRegs ar;
+        // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
+        auto tile_k = [&](int id) { return a.k_body + tile_index(a, stream, kvh, id) * tb; };
+        auto tile_v = [&](int id) { return a.v_body + tile_index(a, stream, kvh, id) * tb; };
+        auto load_aux = [&](int id) { load_aux_regs<CMP>(ar, tile_k(id), tile_v(id), cb, l); };
+        auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
+#pragma unroll
+            for (int s = 0; s < 2; ++s)
+#pragma unroll
+                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * ((s * 64 + l) * 2 * WPU + k));
+        };
+        const int id0 = block_id(a, b, blk0);
+        int id_next = block_id(a, b, min(blk0 + 1, blk1 - 1));
+        load_codes(tile_k(id0), kc);
+        load_codes(tile_v(id0), vc);
+        load_aux(id0);
+
+        q_to_lds<NHD>(sm.q, a, qrow, g, l);
         for (int idx = l; idx < NH * 32; idx += 64)
             sm.qp[idx >> 5][3][(idx >> 4) & 1][(idx >> 2) & 3][idx & 3] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
@@ -768,34 +848,12 @@ void k_decode4(DecodeArgs a) {
         // source lane of the PV operand permutation (see above), as a byte address
         const int perm_addr = (16 * h + 4 * G + j) * 4;
 
-        // One register buffer per tile part, refilled as soon as its current contents are
-        // consumed: the next tile's aux right after it is staged in LDS, its key codes right
-        // after the QK products, its value codes right after the PV products.
-        uint4 kc[2][2 * WPU], vc[2][2 * WPU];
-        AuxRegs ar;
-        // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
-        auto tile_k = [&](int id) { return a.k_body + tile_index(a, stream, kvh, id) * tb; };
-        auto tile_v = [&](int id) { return a.v_body + tile_index(a, stream, kvh, id) * tb; };
-        auto load_aux = [&](int id) { load_aux_regs(ar, tile_k(id), tile_v(id), cb, l, a.compact); };
-        auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * ((s * 64 + l) * 2 * WPU + k));
-        };
-        const int id0 = block_id(a, b, blk0);
-        int id_next = blk0 + 1 < blk1 ? block_id(a, b, blk0 + 1) : 0;
-        load_codes(tile_k(id0), kc);
-        load_codes(tile_v(id0), vc);
-        load_aux(id0);
-
         for (int blk = blk0; blk < blk1; ++blk) {
-            const bool more = blk + 1 < blk1;
-            const int id_after = blk + 2 < blk1 ? block_id(a, b, blk + 2) : 0;
+            const int id_after = block_id(a, b, min(blk + 2, blk1 - 1));
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
-            stage_aux(sm.aux, ar, l, a.compact);
+            stage_aux<CMP>(sm.aux, ar, l);
             __syncthreads();
-            if (more) load_aux(id_next);
+            load_aux(id_next);
             // offsets as ratios b / a: keys per channel, values per token
             sm.aux[1][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l]);
             sm.aux[1][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l + 1]);
@@ -883,7 +941,8 @@ void k_decode4(DecodeArgs a) {
                             ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
                     }
             }
-            if (more) load_codes(tile_k(id_next), kc);
+            const bool pf_codes = !(BITS == 2 && NH == 1) || blk + 1 < blk1;
+            if (pf_codes) load_codes(tile_k(id_next), kc);
 
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
@@ -931,7 +990,7 @@ void k_decode4(DecodeArgs a) {
                     orot[hg][mt] = fmaf((float)digit_sum(acc) + gam, fp * sm.aux[5][16 * mt + n],
                                         orot[hg][mt] * alpha);
                 }
-                if (hg == NH - 1 && more) load_codes(tile_v(id_next), vc);
+                if (hg == NH - 1 && pf_codes) load_codes(tile_v(id_next), vc);
             }
             id_next = id_after;
         }
@@ -946,19 +1005,25 @@ void k_decode4(DecodeArgs a) {
         // remainder (zero for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds
         // q[.][32k + 8G ..].  Loads are clamped to a valid head, then masked.
         v8bf aqs[NH][4];
+        {
+            size_t qi[4 * NH];
+            float qv[4 * NH][8];
 #pragma unroll
-        for (int hg = 0; hg < NH; ++hg) {
-            const int qh = 4 * hg + h;
-            const bool use = qh < g && j < 2;
-            const size_t base = (qrow + min(qh, g - 1)) * kD + 8 * G;
+            for (int hg = 0; hg < NH; ++hg)
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
+                for (int k = 0; k < 4; ++k) qi[4 * hg + k] = (qrow + min(4 * hg + h, g - 1)) * kD + 32 * k + 8 * G;
+            load_q_runs<4 * NH>(a, qi, qv);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float v = use ? load_q(base + 32 * k + e) : 0.f;
-                    const __bf16 hi = (__bf16)v;
-                    aqs[hg][k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
-                }
+            for (int hg = 0; hg < NH; ++hg) {
+                const bool use = 4 * hg + h < g && j < 2;
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        const float v = use ? qv[4 * hg + k][e] : 0.f;
+                        const __bf16 hi = (__bf16)v;
+                        aqs[hg][k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
+                    }
             }
         }
         const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
@@ -972,30 +1037,35 @@ void k_decode4(DecodeArgs a) {
             const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
                                          : a.v_resid + (size_t)stream * kG * kD;
             __syncthreads();  // the previous chunk is done with sm.p / sm.hv
+            // logits of head 4*hg + G, token 16*tau + n.  Rows past the chunk read its last row
+            // (in bounds) and are masked, so no load waits behind a branch.
+            float lg[NH][8];
+#pragma unroll
+            for (int tau = 0; tau < 8; ++tau) {
+                const int trow = 16 * tau + n;
+                const uint16_t* kr = Kp + (size_t)min(trow, cn - 1) * kD + 8 * G;
+                v8bf B[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const uint4 u = *reinterpret_cast<const uint4*>(kr + 32 * k);
+                    __builtin_memcpy(&B[k], &u, 16);
+                }
+#pragma unroll
+                for (int hg = 0; hg < NH; ++hg) {
+                    v4f acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) acc = mfma_bf16(aqs[hg][k], B[k], acc);
+                    lg[hg][tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
+                }
+            }
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
-                // logits of head 4*hg + G, token 16*tau + n
-                float lg[8];
-#pragma unroll
-                for (int tau = 0; tau < 8; ++tau) {
-                    v4f acc = {0.f, 0.f, 0.f, 0.f};
-                    const int trow = 16 * tau + n;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        uint4 u = {0u, 0u, 0u, 0u};
-                        if (trow < cn) u = *reinterpret_cast<const uint4*>(Kp + (size_t)trow * kD + 32 * k + 8 * G);
-                        v8bf B;
-                        __builtin_memcpy(&B, &u, 16);
-                        acc = mfma_bf16(aqs[hg][k], B, acc);
-                    }
-                    lg[tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
-                }
-                const float alpha = softmax_update(lg, true, m_run[hg], l_run[hg]);
+                const float alpha = softmax_update(lg[hg], true, m_run[hg], l_run[hg]);
 #pragma unroll
                 for (int mt = 0; mt < 8; ++mt) orot[hg][mt] *= alpha;
                 if (4 * hg + G < g) {
 #pragma unroll
-                    for (int tau = 0; tau < 8; ++tau) sm.p[4 * hg + G][16 * tau + n] = lg[tau];
+                    for (int tau = 0; tau < 8; ++tau) sm.p[4 * hg + G][16 * tau + n] = lg[hg][tau];
                     if (n == 0) sm.hv[4 * hg + G][2] = alpha;
                 }
             }
@@ -1008,14 +1078,15 @@ void k_decode4(DecodeArgs a) {
                     oplain[hh][1] *= al;
                 }
             }
-            // rows in batches of 8 with all loads in flight; rows >= cn read as zero (their p is 0)
-            for (int t = 0; t < cn; t += 8) {
-                uint32_t v2[8];
+            // rows in batches of 32 with all loads in flight; rows past the chunk read its last
+            // row (their p is 0)
+            for (int t = 0; t < cn; t += 32) {
+                uint32_t v2[32];
 #pragma unroll
-                for (int u = 0; u < 8; ++u)
-                    v2[u] = t + u < cn ? reinterpret_cast<const uint32_t*>(Vp + (size_t)(t + u) * kD)[l] : 0u;
+                for (int u = 0; u < 32; ++u)
+                    v2[u] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t + u, cn - 1) * kD)[l];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
+                for (int u = 0; u < 32; ++u) {
                     const float v0 = __uint_as_float(v2[u] << 16), v1 = __uint_as_float(v2[u] & 0xFFFF0000u);
 #pragma unroll
                     for (int hh = 0; hh < NHD; ++hh) {
@@ -1132,26 +1203,26 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
         static_cast<float*>(a.out)[idx] = o;
 }
 
-template <int BITS, int GQ>
+template <int BITS, int GQ, int CMP>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
     if constexpr (GQ == 4)
-        hipLaunchKernelGGL((k_decode4<BITS, 1>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+        hipLaunchKernelGGL((k_decode4<BITS, 1, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     else if constexpr (GQ == 8)
-        hipLaunchKernelGGL((k_decode4<BITS, 2>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+        hipLaunchKernelGGL((k_decode4<BITS, 2, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     else
-        hipLaunchKernelGGL((k_decode<BITS, GQ>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+        hipLaunchKernelGGL((k_decode<BITS, GQ, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_split == 1) return e;
     hipLaunchKernelGGL(k_decode_merge, dim3((unsigned)(batch * a.n_q)), dim3(128), 0, stream, a);
     return hipGetLastError();
 }
 
-template <int BITS>
+template <int BITS, int CMP>
 hipError_t launch_bits(const DecodeArgs& a, int batch, hipStream_t stream) {
-    if (a.g <= 4) return launch_cfg<BITS, 4>(a, batch, stream);
-    if (a.g <= 8) return launch_cfg<BITS, 8>(a, batch, stream);
-    return launch_cfg<BITS, 16>(a, batch, stream);
+    if (a.g <= 4) return launch_cfg<BITS, 4, CMP>(a, batch, stream);
+    if (a.g <= 8) return launch_cfg<BITS, 8, CMP>(a, batch, stream);
+    return launch_cfg<BITS, 16, CMP>(a, batch, stream);
 }
 
 }  // namespace
@@ -1213,7 +1284,8 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
     a.ws = ws;
-    return bits == 2 ? launch_bits<2>(a, c.batch, stream) : launch_bits<4>(a, c.batch, stream);
+    if (compact) return bits == 2 ? launch_bits<2, 1>(a, c.batch, stream) : launch_bits<4, 1>(a, c.batch, stream);
+    return bits == 2 ? launch_bits<2, 0>(a, c.batch, stream) : launch_bits<4, 0>(a, c.batch, stream);
 }
 
 }  // namespace kvarn
