@@ -813,8 +813,8 @@ void k_decode4(DecodeArgs a) {
         // after the QK products, its value codes right after the PV products.  The first tile's
         // loads go out before the query set-up.  The aux prefetch is unconditional (past the
         // last tile it re-reads that tile's aux) so that it never waits behind a branch; the
-        // code prefetches are too, except in the 2-bit single-group variant, which schedules
-        // best (measured) with them skipped after the last tile.
+        // code prefetches are too in the two-group variant (no spills that way), while the
+        // single-group variants schedule best (measured) with them skipped after the last tile.
         uint4 kc[2][2 * WPU], vc[2][2 * WPU];
         AuxRegs ar;
         // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
@@ -941,7 +941,7 @@ void k_decode4(DecodeArgs a) {
                             ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
                     }
             }
-            const bool pf_codes = !(BITS == 2 && NH == 1) || blk + 1 < blk1;
+            const bool pf_codes = !(NH == 1) || blk + 1 < blk1;
             if (pf_codes) load_codes(tile_k(id_next), kc);
 
 #pragma unroll
