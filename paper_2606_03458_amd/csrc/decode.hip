@@ -127,6 +127,11 @@ __device__ __forceinline__ int block_id(const DecodeArgs& a, int b, int blk) {
 __device__ __forceinline__ size_t tile_index(const DecodeArgs& a, int stream, int kvh, int id) {
     return a.block_table ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id;
 }
+template <int PG>
+__device__ __forceinline__ int block_id_t(const DecodeArgs& a, int b, int blk) {
+    if constexpr (PG) return a.block_table[(size_t)b * a.max_blocks + blk];
+    else return blk;
+}
 // Paged bodies: the wave checks the pool ids of its tiles [blk0, blk1) once; an id outside the
 // pool sets bit 1 of err_word and the caller skips the body (nothing outside the pool is read).
 __device__ __forceinline__ bool body_ids_ok(const DecodeArgs& a, int b, int blk0, int blk1, int l) {
@@ -744,7 +749,7 @@ struct Smem4 {
     float p[4 * NH][kG];       // probabilities of a bf16 chunk (sink / residual)
 };
 
-template <int BITS, int NH, int CMP>
+template <int BITS, int NH, int CMP, int PG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
     __shared__ Smem4<NH> sm;
@@ -771,7 +776,7 @@ void k_decode4(DecodeArgs a) {
     const bool last = split == a.n_split - 1;
     const int blk0 = split * a.bps;
     int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
-    if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
+    if (PG && blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
     const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
 
@@ -815,23 +820,25 @@ void k_decode4(DecodeArgs a) {
         // last tile it re-reads that tile's aux) so that it never waits behind a branch; the
         // code prefetches are too in the two-group variant (no spills that way), while the
         // single-group variants schedule best (measured) with them skipped after the last tile.
-        uint4 kc[2][2 * WPU], vc[2][2 * WPU];
-        AuxRegs ar;
+        struct TileRegs {
+            uint4 k[2][2 * WPU], v[2][2 * WPU];
+            AuxRegs ar;
+        };
+        TileRegs ra, rb;
         // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
-        auto tile_k = [&](int id) { return a.k_body + tile_index(a, stream, kvh, id) * tb; };
-        auto tile_v = [&](int id) { return a.v_body + tile_index(a, stream, kvh, id) * tb; };
-        auto load_aux = [&](int id) { load_aux_regs<CMP>(ar, tile_k(id), tile_v(id), cb, l); };
+        auto tile_k = [&](int id) { return a.k_body + (PG ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id) * tb; };
+        auto tile_v = [&](int id) { return a.v_body + (PG ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id) * tb; };
+        auto load_aux = [&](TileRegs& r, int id) { load_aux_regs<CMP>(r.ar, tile_k(id), tile_v(id), cb, l); };
         auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
                 for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * ((s * 64 + l) * 2 * WPU + k));
         };
-        const int id0 = block_id(a, b, blk0);
-        int id_next = block_id(a, b, min(blk0 + 1, blk1 - 1));
-        load_codes(tile_k(id0), kc);
-        load_codes(tile_v(id0), vc);
-        load_aux(id0);
+        const int id0 = block_id_t<PG>(a, b, blk0);
+        load_codes(tile_k(id0), ra.k);
+        load_codes(tile_v(id0), ra.v);
+        load_aux(ra, id0);
 
         q_to_lds<NHD>(sm.q, a, qrow, g, l);
         for (int idx = l; idx < NH * 32; idx += 64)
@@ -848,12 +855,12 @@ void k_decode4(DecodeArgs a) {
         // source lane of the PV operand permutation (see above), as a byte address
         const int perm_addr = (16 * h + 4 * G + j) * 4;
 
-        for (int blk = blk0; blk < blk1; ++blk) {
-            const int id_after = block_id(a, b, min(blk + 2, blk1 - 1));
+        // One tile: consume cur, prefetch tile id_next into nxt.
+        auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
-            stage_aux<CMP>(sm.aux, ar, l);
+            stage_aux<CMP>(sm.aux, cur.ar, l);
             __syncthreads();
-            load_aux(id_next);
+            load_aux(nxt, id_next);
             // offsets as ratios b / a: keys per channel, values per token
             sm.aux[1][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l]);
             sm.aux[1][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l + 1]);
@@ -865,10 +872,10 @@ void k_decode4(DecodeArgs a) {
             for (int s = 0; s < 2; ++s)
 #pragma unroll
                 for (int k = 0; k < 2 * WPU; ++k) {
-                    kw[s][4 * k] = kc[s][k].x; kw[s][4 * k + 1] = kc[s][k].y;
-                    kw[s][4 * k + 2] = kc[s][k].z; kw[s][4 * k + 3] = kc[s][k].w;
-                    vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
-                    vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
+                    kw[s][4 * k] = cur.k[s][k].x; kw[s][4 * k + 1] = cur.k[s][k].y;
+                    kw[s][4 * k + 2] = cur.k[s][k].z; kw[s][4 * k + 3] = cur.k[s][k].w;
+                    vw[s][4 * k] = cur.v[s][k].x; vw[s][4 * k + 1] = cur.v[s][k].y;
+                    vw[s][4 * k + 2] = cur.v[s][k].z; vw[s][4 * k + 3] = cur.v[s][k].w;
                 }
             // q~ = q_rot * a_K as fixed point on a per-head grid, then three digit planes; beta
             // in grid units from the same rounded integers times b_K / a_K
@@ -941,8 +948,7 @@ void k_decode4(DecodeArgs a) {
                             ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
                     }
             }
-            const bool pf_codes = !(NH == 1) || blk + 1 < blk1;
-            if (pf_codes) load_codes(tile_k(id_next), kc);
+            load_codes(tile_k(id_next), nxt.k);
 
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
@@ -990,10 +996,20 @@ void k_decode4(DecodeArgs a) {
                     orot[hg][mt] = fmaf((float)digit_sum(acc) + gam, fp * sm.aux[5][16 * mt + n],
                                         orot[hg][mt] * alpha);
                 }
-                if (hg == NH - 1 && pf_codes) load_codes(tile_v(id_next), vc);
+                if (hg == NH - 1) load_codes(tile_v(id_next), nxt.v);
             }
-            id_next = id_after;
+        };
+        // Tiles in pairs, alternating the buffers, so that no register copy (and no wait for a
+        // prefetch) is needed between iterations; prefetches past the last tile re-read it.
+        int blk = blk0;
+        int id_n = block_id_t<PG>(a, b, min(blk0 + 1, blk1 - 1));
+        for (; blk + 1 < blk1; blk += 2) {
+            const int id_nn = block_id_t<PG>(a, b, min(blk + 2, blk1 - 1));
+            step(ra, rb, id_n);
+            id_n = block_id_t<PG>(a, b, min(blk + 3, blk1 - 1));
+            step(rb, ra, id_nn);
         }
+        if (blk < blk1) step(ra, rb, id_n);
     }
 
     // ---- sink and residual (bf16, unrotated): last split only ------------------------------
@@ -1206,11 +1222,15 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
 template <int BITS, int GQ, int CMP>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
-    if constexpr (GQ == 4)
-        hipLaunchKernelGGL((k_decode4<BITS, 1, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
-    else if constexpr (GQ == 8)
-        hipLaunchKernelGGL((k_decode4<BITS, 2, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
-    else
+    const dim3 grid((unsigned)(streams * a.n_split));
+    const bool pg = a.block_table != nullptr;
+    if constexpr (GQ == 4) {
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1>), grid, dim3(64), 0, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0>), grid, dim3(64), 0, stream, a);
+    } else if constexpr (GQ == 8) {
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 1>), grid, dim3(64), 0, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0>), grid, dim3(64), 0, stream, a);
+    } else
         hipLaunchKernelGGL((k_decode<BITS, GQ, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_split == 1) return e;
