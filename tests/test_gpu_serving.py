@@ -119,6 +119,31 @@ def test_paged_equals_dense(K):
     check_output(o_p.cpu().numpy(), oracle.decode(host_cache(dense), q_to_host(q), SCALE), bf16_out=False)
 
 
+@pytest.mark.parametrize("bits", [2, 4])
+@pytest.mark.parametrize("aux", [0, 1])
+@pytest.mark.parametrize("g", [4, 5, 12])
+def test_paged_every_kernel(K, bits, aux, g):
+    """Every decode kernel (code width x aux format x query-group class 1-4, 5-8, 9-16) on a
+    permuted pool: bit-equal to the dense layout and within the output bar of the oracle, with
+    ragged lengths (a residual, an exact block boundary, a sequence shorter than one block)."""
+    lens = [9 * 128 + 77, 3 * 128, 90]  # 9 body tiles: the plan splits the longest stream in two
+    B, H, MB = len(lens), 2, 10
+    k, v, cu = _prompts(lens, H, torch.bfloat16, seed=11 + bits + 2 * aux + g)
+    p = K.kvarn_params_init(bits, aux_format=aux)
+    dense = K.Cache(p, B, H, MB)
+    n_phys = B * MB + 3
+    paged = K.Cache(p, B, H, MB, n_phys=n_phys)
+    perm = torch.randperm(n_phys, generator=torch.Generator().manual_seed(g))[:B * MB]
+    paged.block_table.copy_(perm.view(B, MB).to(torch.int32))
+    for c in (dense, paged):
+        K.kvarn_prefill(p, c, k, v, K.KVARN_BF16, cu, max(lens))
+    q = torch.randn((B, g * H, 128), device="cuda").to(torch.bfloat16)
+    o_d, o_p = _decode(K, p, dense, q, max(lens)), _decode(K, p, paged, q, max(lens))
+    assert torch.equal(o_d, o_p)
+    assert int(paged.err_word[0]) == 0
+    check_output(o_d.cpu().numpy(), oracle.decode(host_cache(dense), q_to_host(q), SCALE), bf16_out=False)
+
+
 def test_serving_error_flags(K):
     """Conditions the kernels check themselves: a prompt longer than max_len is not written
     (seq_len 0, bit 0); a pool id outside the pool sets bit 1, and decode then skips that
