@@ -1180,17 +1180,42 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
     const int c = threadIdx.x;
     const size_t bh = blockIdx.x;
     const float* P = a.ws + bh * a.n_split * kPart;
+    const int S = a.n_split;
+    // Splits in batches of 8 with every load of a batch in flight (indices past the last split
+    // are clamped, their values unused): two passes, the maximum, then the weighted sums.
+    constexpr int U = 8;
     float M = -INFINITY;
-    for (int s = 0; s < a.n_split; ++s)
-        if (P[s * kPart + 1] > 0.f) M = fmaxf(M, P[s * kPart]);
+    for (int s0 = 0; s0 < S; s0 += U) {
+        float mm[U], ll[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = min(s0 + u, S - 1);
+            mm[u] = P[s * kPart];
+            ll[u] = P[s * kPart + 1];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (s0 + u < S && ll[u] > 0.f) M = fmaxf(M, mm[u]);
+    }
     float L = 0.f, acc = 0.f, pl = 0.f;
-    for (int s = 0; s < a.n_split; ++s) {
-        const float l = P[s * kPart + 1];
-        if (l > 0.f) {
-            const float w = exp2f(P[s * kPart] - M);
-            L += w * l;
-            acc += w * P[s * kPart + 4 + c];
-            pl += w * P[s * kPart + 132 + c];
+    for (int s0 = 0; s0 < S; s0 += U) {
+        float mm[U], ll[U], ov[U], pv[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const float* Ps = P + min(s0 + u, S - 1) * kPart;
+            mm[u] = Ps[0];
+            ll[u] = Ps[1];
+            ov[u] = Ps[4 + c];
+            pv[u] = Ps[132 + c];
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (s0 + u < S && ll[u] > 0.f) {
+                const float w = exp2f(mm[u] - M);
+                L += w * ll[u];
+                acc += w * ov[u];
+                pl += w * pv[u];
+            }
         }
     }
     orot[c] = acc;
