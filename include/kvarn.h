@@ -49,12 +49,16 @@
  *   Dequantized rotated tile, both formats: keys (code[t][c]*a[c] + b[c]) * s2[t]; values
  *   (code[t][c]*a[t] + b[t]) * s2[c]; un-rotate each token with the orthonormal Hadamard
  *   matrix.
- *   Code layout: codes form units of 16; unit u is bits/2 little-endian 32-bit words starting
- *   at word u*bits/2.  Code e = 4*s + q (s, q in 0..3) of a unit sits in word s/(8/bits) of
- *   the unit, at bit 8*q + bits*(s % (8/bits)).  For token t, channel c, sigma = t/64:
+ *   Code layout: codes form units of 16; a unit is bits/2 little-endian 32-bit words.  With
+ *   u = 512*sigma + 8*L + w (L in 0..63, w in 0..7) and p = 8/bits, unit u starts at word
+ *   512*(bits/2)*sigma + 256*(w/p) + 4*L + (bits/2)*(w%p).  Code e = 4*s + q (s, q in 0..3)
+ *   of a unit sits in word s/p of the unit, at bit 8*q + bits*(s%p).  For token t, channel c,
+ *   sigma = t/64:
  *     keys:   u = (sigma*64 + 16*((c%64)/16) + t%16)*8 + 2*((t%64)/16) + c/64,  e = c % 16
  *     values: u = (sigma*64 + 16*((t%16)/4) + c%16)*8 + c/16,  e = 4*((t%64)/16) + t%4
- *   (Each 64-token half of a tile is the register image of 64 GPU lanes x 8 units.)
+ *   (Each 64-token half of a tile is the register image of 64 GPU lanes x 8 units: lane L
+ *   holds units 8L .. 8L+7 as 2 or 4 pieces of 16 bytes, piece k at byte 1024*k + 16*L of
+ *   the half, so that each 16-byte load of a wave reads 1 KB of consecutive bytes.)
  */
 #ifndef KVARN_H
 #define KVARN_H

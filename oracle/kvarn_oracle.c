@@ -398,10 +398,12 @@ void kvo_quantize_tile(const double *X, int kind, const kvo_params *p, uint8_t *
  *     codes region: bits * 2048 bytes (128 x 128 codes of `bits` bits)
  *     aux 0: a[128], b[128], s2[128]: little-endian binary32, in index order (token or channel)
  *     aux 1: b[128] little-endian binary16, then a[128] and s2[128] as E4M3 bytes
- * Codes are grouped in "units" of 16 codes; unit u occupies bits/2 consecutive 32-bit
- * little-endian words starting at word u * bits/2.  Inside a unit, code number e = 4*s + q
- * (s, q in 0..3) sits in word  s / (8/bits)  at bit  8*q + bits*(s % (8/bits)).
- * The unit index and e of code (t, c) are, with sigma = t / 64:
+ * Codes are grouped in "units" of 16 codes; a unit is bits/2 consecutive 32-bit
+ * little-endian words.  Write unit u as u = 512*sigma + 8*L + w (sigma in 0..1, L in 0..63,
+ * w in 0..7) and p = 8/bits; unit u starts at word
+ *     512*(bits/2)*sigma + 256*(w / p) + 4*L + (bits/2)*(w % p).
+ * Inside a unit, code number e = 4*s + q (s, q in 0..3) sits in word  s / p  at bit
+ * 8*q + bits*(s % p).  The unit index and e of code (t, c) are, with sigma = t / 64:
  *   keys:   unit = (sigma*64 + 16*((c % 64) / 16) + t % 16) * 8 + 2*((t % 64) / 16) + c / 64,
  *           e = c % 16
  *   values: unit = (sigma*64 + 16*((t % 16) / 4) + c % 16) * 8 + c / 16,
@@ -421,7 +423,9 @@ static void code_location(int kind, int bits, int t, int c, size_t *word, int *s
         e = 4 * ((t % 64) / 16) + t % 4;
     }
     int s = e / 4, q = e % 4, per = 8 / bits;
-    *word = unit * (size_t)(bits / 2) + (size_t)(s / per);
+    size_t wpu = (size_t)(bits / 2), sg = unit / 512, L = (unit / 8) % 64, w = unit % 8;
+    size_t start = 512 * wpu * sg + 256 * (w / (size_t)per) + 4 * L + wpu * (w % (size_t)per);
+    *word = start + (size_t)(s / per);
     *shift = 8 * q + bits * (s % per);
 }
 

@@ -346,8 +346,8 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
             for (int s = 0; s < 2; ++s)
 #pragma unroll
                 for (int k = 0; k < 2 * WPU; ++k) {
-                    kc[s][k] = load_stream(kt + 16 * ((s * 64 + l) * 2 * WPU + k));
-                    vc[s][k] = load_stream(vt + 16 * ((s * 64 + l) * 2 * WPU + k));
+                    kc[s][k] = load_stream(kt + 16 * (s * 128 * WPU + 64 * k + l));
+                    vc[s][k] = load_stream(vt + 16 * (s * 128 * WPU + 64 * k + l));
                 }
             load_aux_regs<CMP>(ar, kt, vt, cb, l);
         };
@@ -833,7 +833,7 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * ((s * 64 + l) * 2 * WPU + k));
+                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * (s * 128 * WPU + 64 * k + l));
         };
         const int id0 = block_id_t<PG>(a, b, blk0);
         load_codes(tile_k(id0), ra.k);

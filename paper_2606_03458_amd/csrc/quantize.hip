@@ -500,17 +500,14 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
     if (best_out && L.tid == 0) *best_out = best;
     __syncthreads();
 
-    // ---- a7: pack; thread tid assembles units 4*tid .. 4*tid+3 -----------------------------
-    // Unit u: sigma = u / 512, lane' = (u / 8) % 64, w = u % 8.  Its 16 codes e = 4s + q come
-    // from four 4-byte LDS reads d_s (byte q = code e); code e goes to bit 8q + bits*(s % per)
-    // of word s / per, per = 8 / bits, so a word is the OR of d_s shifted by bits*(s % per).
-    uint32_t words[8];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int unit = 4 * L.tid + k;
-        const int sigma = unit >> 9, lanep = (unit >> 3) & 63, wsel = unit & 7;
+    // ---- a7: pack ------------------------------------------------------------------------------
+    // Unit (sigma, lane L, w): its 16 codes e = 4s + q come from four 4-byte LDS reads d_s (byte
+    // q = code e); code e goes to bit 8q + bits*(s % p) of word s / p, p = 8 / bits, so a word
+    // is the OR of d_s shifted by bits*(s % p).  A 16-byte piece holds p units of one lane:
+    // piece k of lane L in half sigma is stored at piece index 128*(bits/2)*sigma + 64*k + L, so
+    // thread tid writes piece tid (and tid + 256 at 4 bits) and every store is contiguous.
+    auto gather = [&](int sigma, int lanep, int wsel, uint32_t (&d)[4]) {
         const int m = lanep & 15, G4 = lanep >> 4;
-        uint32_t d[4];
         if (kind == KVARN_KEYS) {
             const int t = 64 * sigma + 16 * (wsel >> 1) + m;
             const int c0 = 64 * (wsel & 1) + 16 * G4;
@@ -522,18 +519,32 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
             for (int ss = 0; ss < 4; ++ss)
                 d[ss] = *reinterpret_cast<const uint32_t*>(&sm.codes[c * kG + 64 * sigma + 16 * ss + 4 * G4]);
         }
-        if (P.bits == 2) {
-            words[k] = d[0] | (d[1] << 2) | (d[2] << 4) | (d[3] << 6);
-        } else {
-            words[2 * k] = d[0] | (d[1] << 4);
-            words[2 * k + 1] = d[2] | (d[3] << 4);
-        }
-    }
+    };
     if (P.bits == 2) {
-        reinterpret_cast<uint4*>(dst)[L.tid] = make_uint4(words[0], words[1], words[2], words[3]);
+        const int sigma = L.tid >> 7, k = (L.tid >> 6) & 1, lanep = L.tid & 63;
+        uint32_t w[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            uint32_t d[4];
+            gather(sigma, lanep, 4 * k + i, d);
+            w[i] = d[0] | (d[1] << 2) | (d[2] << 4) | (d[3] << 6);
+        }
+        reinterpret_cast<uint4*>(dst)[L.tid] = make_uint4(w[0], w[1], w[2], w[3]);
     } else {
-        reinterpret_cast<uint4*>(dst)[2 * L.tid] = make_uint4(words[0], words[1], words[2], words[3]);
-        reinterpret_cast<uint4*>(dst)[2 * L.tid + 1] = make_uint4(words[4], words[5], words[6], words[7]);
+#pragma unroll
+        for (int pi = 0; pi < 2; ++pi) {
+            const int pc = L.tid + 256 * pi;
+            const int sigma = pc >> 8, k = (pc >> 6) & 3, lanep = pc & 63;
+            uint32_t w[4];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                uint32_t d[4];
+                gather(sigma, lanep, 2 * k + i, d);
+                w[2 * i] = d[0] | (d[1] << 4);
+                w[2 * i + 1] = d[2] | (d[3] << 4);
+            }
+            reinterpret_cast<uint4*>(dst)[pc] = make_uint4(w[0], w[1], w[2], w[3]);
+        }
     }
 }
 

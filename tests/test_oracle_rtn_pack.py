@@ -43,52 +43,37 @@ def test_tile_bytes_and_bits_per_element(orc):
     assert orc.tile_bytes(2) * 8 / 16384 == 2.75 and orc.tile_bytes(4) * 8 / 16384 == 4.75
 
 
-# Hand-derived word / bit positions from the format description (2-bit tiles):
-#   keys:   unit = (sigma*64 + 16*((c%64)//16) + t%16)*8 + 2*((t%64)//16) + c//64, e = c%16
-#   values: unit = (sigma*64 + 16*((t%16)//4) + c%16)*8 + c//16,  e = 4*((t%64)//16) + t%4
-#   code e = 4s + q sits in word unit at bit 8q + 2s.
+# Hand-derived word / bit positions from the format description, 2-bit and 4-bit tiles
+# (tests/golden/format_2bit_positions.txt; the derivation rules are in its header).
 def _hand_positions():
-    """Hand-derived 2-bit positions, tests/golden/format_2bit_positions.txt."""
+    """Rows (kind, (t, c), {bits: (word, bit)})."""
     import os
     path = os.path.join(os.path.dirname(__file__), "golden", "format_2bit_positions.txt")
     table = {0: [], 1: []}
     with open(path) as fh:
         for line in fh:
             if line.strip() and not line.startswith("#"):
-                k, t, c, w, bit = (int(v) for v in line.split())
-                table[k].append(((t, c), w, bit))
+                k, t, c, w2, b2, w4, b4 = (int(v) for v in line.split())
+                table[k].append(((t, c), {2: (w2, b2), 4: (w4, b4)}))
     return table
 
 
-HAND_2BIT = _hand_positions()
+HAND = _hand_positions()
 
 
 @pytest.mark.parametrize("kind", [0, 1])
-def test_pack_hand_positions(orc, kind):
-    for (t, c), word, bit in HAND_2BIT[kind]:
+@pytest.mark.parametrize("bits", [2, 4])
+def test_pack_hand_positions(orc, kind, bits):
+    code = 3 if bits == 2 else 13
+    for (t, c), pos in HAND[kind]:
+        word, bit = pos[bits]
         codes = np.zeros((128, 128), dtype=np.uint8)
-        codes[t, c] = 3
-        packed = orc.pack_tile(codes, np.zeros(128), np.zeros(128), np.zeros(128), kind, 2)
-        words = packed[:4096].view("<u4")
+        codes[t, c] = code
+        packed = orc.pack_tile(codes, np.zeros(128), np.zeros(128), np.zeros(128), kind, bits)
+        words = packed[:bits * 2048].view("<u4")
         nz = np.flatnonzero(words)
         assert list(nz) == [word], (t, c, nz)
-        assert words[word] == 3 << bit, (t, c, hex(words[word]))
-
-
-@pytest.mark.parametrize("kind", [0, 1])
-def test_pack_hand_positions_4bit(orc, kind):
-    # 4-bit: a unit is two words; code e = 4s + q lies in word 2*unit + s//2 at bit 8q + 4(s%2)
-    for (t, c), word2, bit2 in HAND_2BIT[kind]:
-        e_s = bit2 % 8 // 2
-        q = bit2 // 8
-        word = 2 * word2 + e_s // 2
-        bit = 8 * q + 4 * (e_s % 2)
-        codes = np.zeros((128, 128), dtype=np.uint8)
-        codes[t, c] = 13
-        packed = orc.pack_tile(codes, np.zeros(128), np.zeros(128), np.zeros(128), kind, 4)
-        words = packed[:8192].view("<u4")
-        assert list(np.flatnonzero(words)) == [word]
-        assert words[word] == 13 << bit
+        assert words[word] == code << bit, (t, c, hex(words[word]))
 
 
 @pytest.mark.parametrize("kind", [0, 1])
