@@ -813,21 +813,21 @@ void k_decode4(DecodeArgs a) {
     };
 
     if (blk0 < blk1) {
-        // One register buffer per tile part, refilled as soon as its current contents are
-        // consumed: the next tile's aux right after it is staged in LDS, its key codes right
-        // after the QK products, its value codes right after the PV products.  The first tile's
-        // loads go out before the query set-up.  The aux prefetch is unconditional (past the
-        // last tile it re-reads that tile's aux) so that it never waits behind a branch; the
-        // code prefetches are too in the two-group variant (no spills that way), while the
-        // single-group variants schedule best (measured) with them skipped after the last tile.
+        // Two register buffers, one tile each, alternate between tiles.  While a tile is
+        // consumed from one, the next tile's parts go into the other: its aux right after the
+        // current aux is staged in LDS, its key codes after the QK products, its value codes
+        // after the PV products.  The first tile's loads go out before the query set-up.  No
+        // load sits behind a branch (the prefetch past the last tile re-reads that tile), so
+        // each wait counts exactly the loads it needs.
         struct TileRegs {
             uint4 k[2][2 * WPU], v[2][2 * WPU];
             AuxRegs ar;
         };
         TileRegs ra, rb;
         // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
-        auto tile_k = [&](int id) { return a.k_body + (PG ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id) * tb; };
-        auto tile_v = [&](int id) { return a.v_body + (PG ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id) * tb; };
+        auto tile_of = [&](int id) { return PG ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id; };
+        auto tile_k = [&](int id) { return a.k_body + tile_of(id) * tb; };
+        auto tile_v = [&](int id) { return a.v_body + tile_of(id) * tb; };
         auto load_aux = [&](TileRegs& r, int id) { load_aux_regs<CMP>(r.ar, tile_k(id), tile_v(id), cb, l); };
         auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
 #pragma unroll
@@ -1000,7 +1000,7 @@ void k_decode4(DecodeArgs a) {
             }
         };
         // Tiles in pairs, alternating the buffers, so that no register copy (and no wait for a
-        // prefetch) is needed between iterations; prefetches past the last tile re-read it.
+        // prefetch) is needed between iterations.
         int blk = blk0;
         int id_n = block_id_t<PG>(a, b, min(blk0 + 1, blk1 - 1));
         for (; blk + 1 < blk1; blk += 2) {
