@@ -15,6 +15,7 @@ constexpr int kThreads = 256;
 
 struct QuantSmem {
     float red[2][4][kD];          // column partials [buffer][wave][channel]
+    float rpick[4][4][8];         // row variances of each DPP row [wave][row][token], for the row update
     float rstat[2][4][2];         // per-wave row max / min [buffer][wave][max, min]
     alignas(16) uint8_t codes[kG * kD];  // keys: [token][channel]; values: [channel][token]
 };
@@ -201,6 +202,42 @@ __device__ __forceinline__ float clampf(float v, float lo, float hi) { return fm
 __device__ __forceinline__ float ln_hw(float v) { return __builtin_amdgcn_logf(v) * 0.6931471805599453f; }
 __device__ __forceinline__ float exp_hw(float v) { return __builtin_amdgcn_exp2f(v * kLog2e); }
 
+// ---- shared log-scale updates ----------------------------------------------------------------
+// The four lanes of a wave that hold the same eight columns (lanes l, l^16, l^32, l^48) each
+// update two of them, columns 2G and 2G + 1 of the eight (G = lane / 16); the sixteen lanes of
+// a DPP row, which hold the same eight tokens, update token tc % 8.  The results are gathered
+// back into every lane: with equal operands a 16-lane-row swap returns the (even row, odd row)
+// values of a row pair and a half swap the (lower half, upper half) values; a DPP row
+// broadcast returns lane i of the row.
+__device__ __forceinline__ void gather_cols(const float (&own)[2], float (&out)[8]) {
+    const auto a0 = __builtin_amdgcn_permlane16_swap(__float_as_uint(own[0]), __float_as_uint(own[0]), false, false);
+    const auto a1 = __builtin_amdgcn_permlane16_swap(__float_as_uint(own[1]), __float_as_uint(own[1]), false, false);
+    // a0 = (column 2*(G&2), column 2*(G&2) + 2), a1 = the same + 1; the half swap then gives the
+    // values of rows 0-1 and 2-3
+    const auto b0 = __builtin_amdgcn_permlane32_swap(a0[0], a0[0], false, false);  // columns 0, 4
+    const auto b1 = __builtin_amdgcn_permlane32_swap(a0[1], a0[1], false, false);  // columns 2, 6
+    const auto b2 = __builtin_amdgcn_permlane32_swap(a1[0], a1[0], false, false);  // columns 1, 5
+    const auto b3 = __builtin_amdgcn_permlane32_swap(a1[1], a1[1], false, false);  // columns 3, 7
+    out[0] = __uint_as_float(b0[0]); out[4] = __uint_as_float(b0[1]);
+    out[2] = __uint_as_float(b1[0]); out[6] = __uint_as_float(b1[1]);
+    out[1] = __uint_as_float(b2[0]); out[5] = __uint_as_float(b2[1]);
+    out[3] = __uint_as_float(b3[0]); out[7] = __uint_as_float(b3[1]);
+}
+__device__ __forceinline__ void gather_rows(float own, float (&out)[8]) {
+    out[0] = dppf<0x150>(own); out[1] = dppf<0x151>(own); out[2] = dppf<0x152>(own); out[3] = dppf<0x153>(own);
+    out[4] = dppf<0x154>(own); out[5] = dppf<0x155>(own); out[6] = dppf<0x156>(own); out[7] = dppf<0x157>(own);
+}
+// v[2G + q] in lane row G (v the same in the four rows): a row-pair swap of two registers keeps
+// the first one's even rows and moves the second one's even rows into the odd rows; a half swap
+// of two registers keeps the first one's low half and moves the second one's low half up.
+__device__ __forceinline__ float pick_col(const float (&v)[8], int q) {
+    auto p16 = [](float a, float b) {
+        return __uint_as_float(__builtin_amdgcn_permlane16_swap(__float_as_uint(a), __float_as_uint(b), false, false)[0]);
+    };
+    const float lo = p16(v[q], v[2 + q]), hi = p16(v[4 + q], v[6 + q]);  // rows: v[q], v[2+q], v[q], v[2+q]
+    return __uint_as_float(__builtin_amdgcn_permlane32_swap(__float_as_uint(lo), __float_as_uint(hi), false, false)[0]);
+}
+
 // ---- narrow formats of the compact aux (App. D: two FP8 scales and one FP16 zero point) -----
 // OCP E4M3: 4-bit exponent with bias 7, 3-bit mantissa, subnormals m * 2^-9, largest 448.
 // Grid value of x > 0 on the E4M3 grid of its binade (spacing 2^(e-3), 2^-9 below 2^-6),
@@ -293,12 +330,14 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
     }
 
     // ---- a3/a4: VarN (Algorithm 1), Cur = T * u[c] * w[t] with u = exp(-L_c), w = exp(-L_r) -
-    float Lc[8], Lr[8], u[8], w[8], bLc[8], bLr[8], cv[8], rv[8];
+    // Each lane keeps the log-scales it updates (columns 2G, 2G + 1 and token tc % 8 of its
+    // eight, current and best) and all eight scale factors u, w (gathered).
+    const int G = L.lane >> 4, ir = L.tc & 7;
+    float Lc2[2] = {0.f, 0.f}, bLc2[2] = {0.f, 0.f}, uo[2] = {1.f, 1.f};
+    float Lr1 = 0.f, bLr1 = 0.f, wo = 1.f;
+    float u[8], w[8], cv[8], rv[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-        Lc[k] = Lr[k] = bLc[k] = bLr[k] = 0.f;
-        u[k] = w[k] = 1.f;
-    }
+    for (int k = 0; k < 8; ++k) u[k] = w[k] = 1.f;
     float rmax, rmin;
     row_var(x, u, rv);  // variance over channels of T's rows
     row_stat(rv, rmax, rmin);
@@ -308,19 +347,26 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
     for (int k = 1; k <= P.iters; ++k) {
         // column update from the current column variances u^2 * var_t(T w)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const float v = clampf(u[j] * u[j] * cv[j], P.var_min, P.var_max);
-            Lc[j] = clampf(Lc[j] + 0.5f * ln_hw(v), P.log_lo, P.log_hi);
-            u[j] = exp_hw(-Lc[j]);
+        for (int q = 0; q < 2; ++q) {
+            const float v = clampf(uo[q] * uo[q] * pick_col(cv, q), P.var_min, P.var_max);
+            Lc2[q] = clampf(Lc2[q] + 0.5f * ln_hw(v), P.log_lo, P.log_hi);
+            uo[q] = exp_hw(-Lc2[q]);
         }
+        gather_cols(uo, u);
         // row update from the row variances w^2 * var_c(T u)
         row_var(x, u, rv);
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const float v = clampf(w[i] * w[i] * rv[i], P.var_min, P.var_max);
-            Lr[i] = clampf(Lr[i] + 0.5f * ln_hw(v), P.log_lo, P.log_hi);
-            w[i] = exp_hw(-Lr[i]);
+        {
+            // the row's variances pass through LDS inside the wave to the lane that updates
+            // token ir (LDS operations of a wave complete in order: no barrier)
+            if (L.tc == 0) {
+                *reinterpret_cast<float4*>(&sm.rpick[L.wave][G][0]) = make_float4(rv[0], rv[1], rv[2], rv[3]);
+                *reinterpret_cast<float4*>(&sm.rpick[L.wave][G][4]) = make_float4(rv[4], rv[5], rv[6], rv[7]);
+            }
+            const float v = clampf(wo * wo * sm.rpick[L.wave][G][ir], P.var_min, P.var_max);
+            Lr1 = clampf(Lr1 + 0.5f * ln_hw(v), P.log_lo, P.log_hi);
+            wo = exp_hw(-Lr1);
         }
+        gather_rows(wo, w);
         // imbalance of the new Cur; its column statistics seed the next column update
         float vr[8], vc[8];
 #pragma unroll
@@ -333,22 +379,20 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         if (I <= I_best) {  // later iteration wins ties
             I_best = I;
             best = k;
-#pragma unroll
-            for (int m = 0; m < 8; ++m) {
-                bLc[m] = Lc[m];
-                bLr[m] = Lr[m];
-            }
+            bLc2[0] = Lc2[0];
+            bLc2[1] = Lc2[1];
+            bLr1 = Lr1;
         }
     }
 
     // ---- a5: balanced tile B = T / S_c* / S_r* ---------------------------------------------
     float Sc[8], Sr[8];
-#pragma unroll
-    for (int m = 0; m < 8; ++m) {
-        Sc[m] = exp_hw(bLc[m]);
-        Sr[m] = exp_hw(bLr[m]);
-        u[m] = exp_hw(-bLc[m]);
-        w[m] = exp_hw(-bLr[m]);
+    {
+        const float sc[2] = {exp_hw(bLc2[0]), exp_hw(bLc2[1])}, ui[2] = {exp_hw(-bLc2[0]), exp_hw(-bLc2[1])};
+        gather_cols(sc, Sc);
+        gather_cols(ui, u);
+        gather_rows(exp_hw(bLr1), Sr);
+        gather_rows(exp_hw(-bLr1), w);
     }
     float s2q[8];  // compact aux: the stored (E4M3) other-axis scale of this thread's rows/columns
     if constexpr (COMPACT) {
