@@ -59,7 +59,6 @@ struct DecodeArgs {
     void* out;
     int out_bf16;
     int n_kv, n_q, g, max_blocks, n_sink;
-    int compact;       // aux format of the body tiles: 0 fp32, 1 compact (binary16 b, E4M3 a and s2)
     int rotate;        // 1: body tiles hold the Hadamard-rotated domain; 0: unrotated (ablations)
     const int32_t* block_table;  // paged body: [batch][max_blocks] pool block ids, or null (dense)
     int n_phys;                  // pool size in blocks (paged)
@@ -1304,7 +1303,6 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
                          bool q_bf16, void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
                          hipStream_t stream) {
     DecodeArgs a;
-    a.compact = compact;
     a.rotate = rotate;
     a.block_table = c.block_table;
     a.n_phys = c.n_phys;
