@@ -104,3 +104,50 @@ def test_full_size_stress(K):
 def test_full_size_throughput_compact(K):
     """The throughput workload with the compact aux format (2.25 bits/element)."""
     _run(K, "throughput", n_append=130, n_streams=40, n_tiles=12, out_dtype=torch.bfloat16, aux=1)
+
+
+@pytest.mark.parametrize("bits,aux", [(2, 0), (4, 0), (2, 1)])
+def test_full_size_streaming(K, bits, aux):
+    """The streaming workload's shape (64 sequences x 8 kv heads, 32 q heads) from an empty
+    cache: 261 tokens appended one step at a time (two flushes of 1024 tiles each), decoded at
+    the steps around the flushes in the benchmark's launch configuration; sampled streams are
+    recomputed by the oracle from the GPU cache, and the flushed tiles are re-quantized by the
+    oracle from the appended tokens."""
+    from paper_2606_03458_amd import datagen
+    spec = datagen.WORKLOADS["streaming"]
+    seed = datagen.SEEDS["streaming"]
+    B, n_kv, n_q = spec["batch"], spec["n_kv"], spec["n_q"]
+    g, T = n_q // n_kv, 2 * 128 + 5
+    p = K.kvarn_params_init(bits, aux_format=aux)
+    cache = K.Cache(p, B, n_kv, 3)
+    sig = datagen.channel_log_scales(seed * 1000, n_kv, spec["dist"], device="cuda")
+    Kx, Vx = datagen.kv_tokens(seed * 1000, 0, B, n_kv, T, spec["dist"], dtype=torch.bfloat16, device="cuda",
+                               sigma_c=sig)
+    rng = np.random.default_rng(seed)
+    total = B * n_kv
+    pick = np.unique(np.concatenate([[0, total - 1], rng.choice(total, 14, replace=False)]))
+    streams = [divmod(int(s), n_kv) for s in pick]
+    ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, n_q, T)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    for t in range(T):
+        kt, vt = Kx[:, :, t].contiguous(), Vx[:, :, t].contiguous()
+        assert K.kvarn_append_token(p, cache, kt, vt, K.KVARN_BF16, t) is None
+        if t in (0, 126, 127, 128, 255, T - 1):
+            q = datagen.queries(seed, t, B, n_q, dtype=torch.bfloat16, device="cuda")
+            out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+            K.kvarn_decode_attention(p, cache, n_q, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE, t + 1, ws, ws_bytes)
+            torch.cuda.synchronize()
+            assert np.all(cache.seq_len.cpu().numpy() == t + 1)
+            hc = host_streams(cache, streams)
+            qh = q_to_host(q)
+            qs = np.stack([qh[b, kh * g:(kh + 1) * g] for b, kh in streams])
+            ref = oracle.decode(hc, qs, SCALE)
+            got = np.stack([out[b, kh * g:(kh + 1) * g].cpu().numpy() for b, kh in streams])
+            check_output(got, ref, bf16_out=False)
+    assert int(cache.err_word.item()) == 0
+    compare = compare_tiles_compact if aux else compare_tiles
+    for blk in range(2):
+        for kind, X, body in ((K.KVARN_KEYS, Kx, cache.k_body), (K.KVARN_VALUES, Vx, cache.v_body)):
+            xs = torch.stack([X[b, kh, 128 * blk:128 * (blk + 1)] for b, kh in streams])
+            tiles = torch.stack([body[b, kh, blk] for b, kh in streams]).cpu().numpy()
+            compare(tiles, tiles_to_host(xs), kind, bits)
