@@ -53,8 +53,9 @@ hipError_t launch_append(const kvarn_cache& c, int n_sink, const void* k_new, co
                          hipStream_t stream);
 
 struct DecodePlan {
-    int n_split;           // body splits per (sequence, kv head)
-    int blocks_per_split;  // body tiles per split
+    int n_split;           // splits per (sequence, kv head)
+    int res_split;         // 1: the last split attends only sink + residual
+    int blocks_per_split;  // body tiles per body split
     int max_blocks_used;   // upper bound of body tiles over the batch
 };
 

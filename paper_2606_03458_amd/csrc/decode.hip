@@ -24,7 +24,8 @@
 //
 // Sink and residual tokens (bf16, unrotated) use the bf16 matrix cores for q . k (q as a bf16
 // pair hi + lo when it is fp32) and plain FMAs for p . v.  One wave owns a (split, sequence,
-// kv head); the last split also takes sink + residual.  A single split writes the final
+// kv head); the last split also takes sink + residual (or only those when the stream is split:
+// then they run beside the body splits instead of after one of them).  A single split writes the final
 // output directly (inverse rotation in LDS); several splits write partials that the merge
 // kernel combines by log-sum-exp.
 #include "common.hpp"
@@ -64,7 +65,8 @@ struct DecodeArgs {
     int n_phys;                  // pool size in blocks (paged)
     uint32_t* err_word;
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
-    int n_split, bps;  // body splits per stream and body tiles per split
+    int n_split, bps;  // splits per stream and body tiles per body split
+    int res_split;     // 1: the last split holds only sink + residual (n_split - 1 body splits)
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
 };
 
@@ -293,9 +295,12 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     const int ns = min(len, a.n_sink);
     const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
+    // the last split attends sink + residual; with res_split it holds nothing else
     const bool last = split == a.n_split - 1;
-    const int blk0 = split * a.bps;
-    int blk1 = last ? nbody : min(blk0 + a.bps, nbody);  // the last split takes any excess
+    const bool res_only = a.res_split && last;
+    const bool body_last = split == a.n_split - 1 - a.res_split;  // takes any excess of body tiles
+    const int blk0 = res_only ? 0 : split * a.bps;
+    int blk1 = res_only ? 0 : (body_last ? nbody : min(blk0 + a.bps, nbody));
     if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;    // first query head of the group
     const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
@@ -772,9 +777,12 @@ void k_decode4(DecodeArgs a) {
     const int ns = min(len, a.n_sink);
     const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
+    // the last split attends sink + residual; with res_split it holds nothing else
     const bool last = split == a.n_split - 1;
-    const int blk0 = split * a.bps;
-    int blk1 = last ? nbody : min(blk0 + a.bps, nbody);
+    const bool res_only = a.res_split && last;
+    const bool body_last = split == a.n_split - 1 - a.res_split;  // takes any excess of body tiles
+    const int blk0 = res_only ? 0 : split * a.bps;
+    int blk1 = res_only ? 0 : (body_last ? nbody : min(blk0 + a.bps, nbody));
     if (PG && blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
     const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
     const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
@@ -1284,6 +1292,7 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     const int per_simd = g <= 4 ? (bits == 2 ? 3 : 2) : (g <= 8 ? 2 : 1);
     int want = (1024 * per_simd + streams - 1) / streams;
     if (want > nb / 4) want = nb / 4;
+    p.res_split = 0;
     if (want <= 1) {
         p.n_split = 1;
         p.blocks_per_split = nb > 0 ? nb : 1;
@@ -1291,6 +1300,14 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     }
     p.blocks_per_split = (nb + want - 1) / want;
     p.n_split = (nb + p.blocks_per_split - 1) / p.blocks_per_split;
+    // A split stream is merged anyway: its sink + residual (bf16, a latency-bound chain of
+    // dependent loads) get a split of their own, which runs beside the body splits -- when the
+    // extra waves still fit in the one round of resident waves (otherwise body waves would
+    // wait for free slots behind them; measured: GQA-5 stress 28 % slower).
+    if ((long long)streams * (p.n_split + 1) <= 1024LL * per_simd) {
+        p.res_split = 1;
+        p.n_split += 1;
+    }
     return p;
 }
 
@@ -1326,6 +1343,7 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.scale_log2 = sm_scale * kLog2e;
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
+    a.res_split = plan.res_split;
     a.ws = ws;
     if (compact) return bits == 2 ? launch_bits<2, 1>(a, c.batch, stream) : launch_bits<4, 1>(a, c.batch, stream);
     return bits == 2 ? launch_bits<2, 0>(a, c.batch, stream) : launch_bits<4, 0>(a, c.batch, stream);
