@@ -44,7 +44,10 @@
  *     s2 is rounded to nearest first and the tile is quantized against the stored s2; a is the
  *     RTN step rounded upward (the stored range covers the group), b the nearest binary16 of
  *     the group minimum, and codes are chosen for the stored a and b.  Scales are kept within
- *     [2^-6, 448] and b within +-65504.  Tile size 4608 bytes at 2 bits (2.25 bits/element),
+ *     [2^-6, 448] and b within +-65504.  When the largest step of a tile exceeds 448, a
+ *     tile-wide power of two 2^e moves from a and b into s2 (the smallest e that fits, as far
+ *     as the largest s2 stays within 448; only when no other-axis scale is below 2^-6), which
+ *     leaves every dequantized value unchanged.  Tile size 4608 bytes at 2 bits (2.25 bits/element),
  *     8704 at 4 bits.
  *   Dequantized rotated tile, both formats: keys (code[t][c]*a[c] + b[c]) * s2[t]; values
  *   (code[t][c]*a[t] + b[t]) * s2[c]; un-rotate each token with the orthonormal Hadamard

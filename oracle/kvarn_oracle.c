@@ -299,28 +299,64 @@ void kvo_rtn_group(const double *x, int n, int stride, int bits, uint8_t *codes,
  *
  * Compact aux (p->aux == 1): the stored values are narrow, so they are rounded first and the
  * codes are computed against the stored values ("absorb, then round"):
- *   s2  = E4M3 nearest of the other-axis scale (kept within [2^-6, 448]);
- *   z   = T / s2 along the other axis (= B times the group-axis Sinkhorn scale: RTN of a group
- *         does not depend on a common factor, so that scale is absorbed exactly);
+ *   s2  = E4M3 nearest of 2^e times the other-axis scale (kept within [2^-6, 448]);
+ *   z   = T / s2 along the other axis (= B times the group-axis Sinkhorn scale, over 2^e: RTN
+ *         of a group does not depend on a common factor, so that scale is absorbed exactly);
  *   per group: mn, mx of z, step = (mx - mn) / (2^bits - 1) (1 when mx == mn),
  *   a   = E4M3 of step rounded upward (so [b, b + qmax * a] covers the group), b = binary16
  *         nearest of mn, u = (z - b) / a, code = clamp(round-half-even(u), 0, qmax).
+ *   e   = a tile-wide power of two moved from a and b into s2 (App. D stores both scales in
+ *         FP8 but does not say how the magnitude is split; both are E4M3, at most 448, while
+ *         their product is fixed by the data): the smallest e >= 0 for which the largest step
+ *         of the tile is at most 448, taken no further than the largest other-axis scale
+ *         times 2^e stays within 448, and only when no other-axis scale lies below 2^-6
+ *         (the clamp of s2; with Algorithm 1's log clamp at -0.3 none does).  Without it a key
+ *         tile of magnitude ~100 with outlier channels saturates a at 448 and its range no
+ *         longer covers the group.
  * The dequantized value (code * a + b) * s2 then keeps the RTN error bound a * s2 / 2 (plus the
  * rounding of b).
  * Optional debug outputs (NULL to skip): T_out[128*128], Bal_out[128*128], u_out[128*128]
  * (token-major unrounded quotients), Sc_out[128], Sr_out[128], imb_hist[K+1], best_iter,
  * pre_out[3*128]: a, b, s2 before their rounding to the stored format.
  * ------------------------------------------------------------------------------------------ */
+/* Stored (E4M3) other-axis scale for a tile-wide shift 2^e. */
+static double stored_s2(double so, int e) {
+    return kvo_e4m3_to_double(kvo_e4m3_from_double(clampd(ldexp(so, e), ldexp(1.0, -6), 448.0), 0));
+}
+
+/* Largest group step (mx - mn) / qmax of z = T / s2 over the tile, for the shift 2^e. */
+static double largest_step(const double *T, const double *So, int e, int kind, double qmax) {
+    double best = 0.0;
+    for (int g = 0; g < 128; ++g) {
+        double mn = INFINITY, mx = -INFINITY;
+        for (int i = 0; i < 128; ++i) {
+            const double x = kind == KVO_KEYS ? T[(size_t)i * D + g] : T[(size_t)g * D + i];
+            const double z = x / stored_s2(So[i], e);
+            mn = fmin(mn, z);
+            mx = fmax(mx, z);
+        }
+        best = fmax(best, (mx - mn) / qmax);
+    }
+    return best;
+}
+
 static void quantize_compact(const double *T, const double *Sc, const double *Sr, int kind, int bits,
                              uint8_t *codes, float *a, float *b, float *s2, double *u_out, double *pre_out) {
     const double qmax = (double)((1 << bits) - 1);
     const double *So = kind == KVO_KEYS ? Sr : Sc; /* other-axis scale: per token for keys */
+    double so_max = 0.0, so_min = INFINITY;
+    for (int i = 0; i < 128; ++i) {
+        so_max = fmax(so_max, So[i]);
+        so_min = fmin(so_min, So[i]);
+    }
+    int e = 0;
+    if (so_min >= ldexp(1.0, -6))
+        while (largest_step(T, So, e, kind, qmax) > 448.0 && ldexp(so_max, e + 1) <= 448.0) ++e;
     double s2q[128];
     for (int i = 0; i < 128; ++i) {
-        const double v = clampd(So[i], ldexp(1.0, -6), 448.0);
-        s2q[i] = kvo_e4m3_to_double(kvo_e4m3_from_double(v, 0));
+        s2q[i] = stored_s2(So[i], e);
         s2[i] = (float)s2q[i];
-        if (pre_out) pre_out[256 + i] = So[i];
+        if (pre_out) pre_out[256 + i] = ldexp(So[i], e);
     }
     double z[128];
     for (int g = 0; g < 128; ++g) { /* group: channel g (keys) or token g (values) */

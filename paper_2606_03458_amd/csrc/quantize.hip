@@ -443,6 +443,51 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         reduce_rows<OpMin>(mn);
         reduce_rows<OpMax>(mx);
     }
+    if constexpr (COMPACT) {
+        // Both stored scales are E4M3 (at most 448) while their product is fixed by the data:
+        // when the largest group step of the tile exceeds 448, a tile-wide 2^e moves from the
+        // group scale into s2 (z / 2^e and s2 * 2^e leave every dequantized value unchanged,
+        // and both products are exact), for the smallest such e >= 0 and no further than the
+        // largest other-axis scale times 2^e stays within 448.  The shift needs every
+        // other-axis scale at least 2^-6 (true unless log_lo is set below -4.1), so that s2 was
+        // not clamped and scaling the stored s2 by 2^e equals storing 2^e times the scale.
+        float st[3] = {0.f, 0.f, -__builtin_inff()};  // largest step, largest and -smallest other-axis scale
+#pragma unroll
+        for (int m = 0; m < 8; ++m) {
+            const float so = kind == KVARN_KEYS ? Sr[m] : Sc[m];
+            st[0] = fmaxf(st[0], (mx[m] - mn[m]) / qmax);
+            st[1] = fmaxf(st[1], so);
+            st[2] = fmaxf(st[2], -so);
+        }
+#pragma unroll
+        for (int k = 0; k < 3; ++k) st[k] = across_rows<OpMax>(row16<OpMax>(st[k]));
+        if (L.lane == 0) {
+#pragma unroll
+            for (int k = 0; k < 3; ++k) sm.red[buf][L.wave][k] = st[k];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int k = 0; k < 3; ++k)
+            st[k] = fmaxf(fmaxf(sm.red[buf][0][k], sm.red[buf][1][k]), fmaxf(sm.red[buf][2][k], sm.red[buf][3][k]));
+        buf ^= 1;
+        int e = 0;
+        if (-st[2] >= 0.015625f)
+            while (e < 64 && ldexpf(st[0], -e) > 448.f && ldexpf(st[1], e + 1) <= 448.f) ++e;
+        if (e > 0) {
+            const float down = ldexpf(1.f, -e), up = ldexpf(1.f, e);
+#pragma unroll
+            for (int m = 0; m < 8; ++m) {
+                mn[m] *= down;
+                mx[m] *= down;
+                s2q[m] *= up;
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) x[i][j] *= down;
+            }
+        }
+    }
     // step and offset of each group: fp32 aux keeps them; the compact aux stores the step
     // rounded upward to E4M3 (the stored range covers the group) and the nearest binary16 of
     // the minimum, and the codes are chosen for those stored values

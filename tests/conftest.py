@@ -8,8 +8,25 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 
+_CAPMAN = None
+
+
 def pytest_configure(config):
+    global _CAPMAN
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
+    _CAPMAN = config.pluginmanager.getplugin("capturemanager")
+
+
+def announce(msg: str) -> None:
+    """Write msg to the process's real stderr, past pytest's fd-level capture, so that a case
+    that ends the process is still named in what it printed."""
+    if _CAPMAN is not None:
+        with _CAPMAN.global_and_fixture_disabled():
+            sys.stderr.write(msg + "\n")
+            sys.stderr.flush()
+    else:
+        sys.__stderr__.write(msg + "\n")
+        sys.__stderr__.flush()
 
 
 @pytest.fixture(scope="session")
@@ -23,8 +40,7 @@ def orc():
 def _announce_gpu_case(request):
     """Name every GPU test on the real stderr (not captured) before it touches the device."""
     if request.node.get_closest_marker("gpu") is not None:
-        sys.__stderr__.write(f"\n[gpu case] {request.node.nodeid}\n")
-        sys.__stderr__.flush()
+        announce(f"[gpu case] {request.node.nodeid}")
     yield
 
 

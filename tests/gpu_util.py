@@ -170,7 +170,9 @@ def host_streams(cache, streams) -> "oracle.HostCache":
 # of a rounding boundary of the narrow format.  Such an E4M3 scale tie changes the codes of a
 # whole row or group, so the tile takes the dequantization-bound route (at most 1 % of tiles,
 # as for VarN iteration ties); a binary16 offset tie may move b by one step, which widens the
-# code tie window of that group by the shift |db| / a.
+# code tie window of that group by the shift |db| / a.  The tile-wide power of two moved into
+# s2 is an integer decided by comparisons with 448; a tile near such a threshold may take the
+# other value (all of s2, a and b then differ by that power of two) and takes the bound route.
 FORMAT_TIE = 1e-5
 _E4M3 = None
 
@@ -196,6 +198,16 @@ def _near_fp16_midpoint(x: float) -> bool:
     return min(abs(m - x) for m in mids) <= FORMAT_TIE * abs(x)
 
 
+def _near_shift_tie(r, kind) -> bool:
+    """The tile-wide power of two moved into s2 was decided near one of its thresholds: the
+    largest step times 2^-j near 448, or the largest other-axis scale times 2^(j+1) near 448."""
+    so = (r.Sr if kind == 0 else r.Sc).astype(np.float64)
+    e = int(round(np.log2(r.pre[2][0] / so[0])))
+    m0 = float(np.max(r.pre[0])) * 2.0 ** e
+    near = lambda x: abs(x / 448.0 - 1.0) <= FORMAT_TIE
+    return any(near(m0 * 2.0 ** -j) or near(so.max() * 2.0 ** (j + 1)) for j in range(e + 1))
+
+
 def _compact_tile_status(codes, a, b, s2, r, kind):
     """("match", excused codes, b steps) if the tile meets the bar, ("tie", ...) if it differs
     only where a format tie allows, ("mismatch", ...) otherwise."""
@@ -204,6 +216,7 @@ def _compact_tile_status(codes, a, b, s2, r, kind):
         pre_s2 = np.clip(r.pre[2], 2.0 ** -6, 448.0)
         tie = all(_near_e4m3_boundary(pre_s2[k], False) for k in s2_bad) and \
             all(_near_e4m3_boundary(r.pre[0][k], True) for k in a_bad)
+        tie = tie or _near_shift_tie(r, kind)
         return ("tie" if tie else "mismatch"), 0, 0
     b_bad = np.flatnonzero(b != r.b)
     for k in b_bad:
@@ -222,10 +235,11 @@ def _compact_tile_status(codes, a, b, s2, r, kind):
     return "match", int(mism.sum()), int(b_bad.size)
 
 
-def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gpu_best=None):
+def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gpu_best=None,
+                          varn_iters: int = 8):
     """compare_tiles for the compact aux format (see the comment above for the tie rules).  As
     there, a tile whose kept VarN iteration differs is still compared value by value first."""
-    params = oracle.Params(bits=bits, aux=1)
+    params = oracle.Params(bits=bits, aux=1, varn_iters=varn_iters)
     n = gpu_tiles.shape[0]
     stats = dict(tiles=n, codes=0, excused=0, best_differs=0, ties=0, b_steps=0)
     for i in range(n):
@@ -238,7 +252,7 @@ def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits:
             # a near-tie of Imb: compare against the oracle's outcome for the GPU's iteration
             I, k_g, k_o = r.imb, int(gpu_best[i]), r.best_iter
             assert abs(I[k_g] - I[k_o]) <= 1e-5 * abs(I[k_o]), (i, k_g, k_o, I)
-            r = oracle.quantize_tile(X[i], kind, oracle.Params(bits=bits, aux=1, force_best=k_g))
+            r = oracle.quantize_tile(X[i], kind, oracle.Params(bits=bits, aux=1, varn_iters=varn_iters, force_best=k_g))
             status, excused, b_steps = _compact_tile_status(codes, a, b, s2, r, kind)
             differs = False
         elif status != "match" and gpu_best is None:
@@ -247,7 +261,7 @@ def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits:
             for k in range(len(I)):
                 if k == k_o or abs(I[k] - I[k_o]) > 1e-5 * abs(I[k_o]):
                     continue
-                rk = oracle.quantize_tile(X[i], kind, oracle.Params(bits=bits, aux=1, force_best=k))
+                rk = oracle.quantize_tile(X[i], kind, oracle.Params(bits=bits, aux=1, varn_iters=varn_iters, force_best=k))
                 st = _compact_tile_status(codes, a, b, s2, rk, kind)
                 if st[0] == "match":
                     status, excused, b_steps = st

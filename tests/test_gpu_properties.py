@@ -1,0 +1,127 @@
+"""GPU parity over random configurations (Hypothesis, derandomized so that every run draws the
+same cases; no shrinking, so a failure is reported as drawn): quantized tiles of random structure,
+magnitude, bit width, kind, aux format and input dtype, and decode attention over prefilled
+caches of random batch, kv heads, query group size, sink size, ragged lengths, dense or paged
+body and query / output dtypes.  All through the C ABI against the oracle, to the same bars as
+the fixed-case parity tests (gpu_util)."""
+import numpy as np
+import pytest
+import torch
+from hypothesis import HealthCheck, Phase, given, settings
+from hypothesis import strategies as st
+
+import oracle
+from gpu_util import check_output, compare_tiles, compare_tiles_compact, host_cache, q_to_host, tiles_to_host
+from test_oracle_properties import STRUCTURES, make_tile
+
+pytestmark = pytest.mark.gpu
+
+SETTINGS = dict(derandomize=True, database=None, deadline=None, phases=[Phase.explicit, Phase.generate],
+                suppress_health_check=[HealthCheck.too_slow, HealthCheck.function_scoped_fixture])
+SCALE = 1.0 / np.sqrt(128.0)
+
+
+@pytest.fixture(scope="module")
+def K():
+    from paper_2606_03458_amd import kvarn
+    kvarn.lib()
+    torch.cuda.set_device(0)
+    return kvarn
+
+
+def _announce(case):
+    from conftest import announce
+    announce(f"[gpu property case] {case}")
+
+
+quant_cases = st.fixed_dictionaries(dict(
+    structure=st.sampled_from(STRUCTURES), seed=st.integers(0, 2 ** 31 - 1), log_scale=st.floats(-3.0, 3.5),
+    bits=st.sampled_from([2, 4]), kind=st.sampled_from([0, 1]), aux=st.sampled_from([0, 1]),
+    bf16=st.booleans(), varn_iters=st.sampled_from([0, 1, 8])))
+
+
+@settings(max_examples=40, **SETTINGS)
+@given(case=quant_cases)
+def test_gpu_quantize_property(K, case):
+    _announce(case)
+    c = case
+    n = 4
+    X = np.stack([make_tile(c["structure"], c["seed"] + i, c["log_scale"]) for i in range(n)])
+    x = torch.tensor(X, dtype=torch.float32, device="cuda")
+    if c["bf16"]:
+        x = x.to(torch.bfloat16)
+    Xh = tiles_to_host(x)  # exact input as the kernel sees it
+    p = K.kvarn_params_init(c["bits"], aux_format=c["aux"], varn_iters=c["varn_iters"])
+    out = torch.zeros((n, K.kvarn_tile_bytes(p)), dtype=torch.uint8, device="cuda")
+    best = torch.full((n,), -1, dtype=torch.int32, device="cuda")
+    dt = K.KVARN_BF16 if c["bf16"] else K.KVARN_F32
+    K.kvarn_quantize_block(p, c["kind"], x, dt, n, 1, 128 * 128, 0, 128, out, 1, 0, best)
+    torch.cuda.synchronize()
+    tiles, gbest = out.cpu().numpy(), best.cpu().numpy()
+    assert np.all((gbest >= 0) & (gbest <= c["varn_iters"]))
+    if c["aux"] == 0:
+        compare_tiles(tiles, Xh, c["kind"], c["bits"], gbest,
+                      params=oracle.Params(bits=c["bits"], varn_iters=c["varn_iters"]))
+    else:
+        compare_tiles_compact(tiles, Xh, c["kind"], c["bits"], gbest, varn_iters=c["varn_iters"])
+
+
+decode_cases = st.fixed_dictionaries(dict(
+    bits=st.sampled_from([2, 4]), aux=st.sampled_from([0, 1]), n_sink=st.sampled_from([0, 1, 64, 128]),
+    n_kv=st.integers(1, 3), g=st.integers(1, 16), paged=st.booleans(), q_bf16=st.booleans(),
+    out_bf16=st.booleans(), seed=st.integers(0, 2 ** 31 - 1), hint_extra=st.integers(1, 300),
+    lens=st.lists(st.integers(0, 7 * 128 + 127), min_size=1, max_size=4)))
+
+
+def _decode(K, p, cache, q, q_dt, out_dtype, max_len):
+    ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, q.shape[1], max_len)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device="cuda")
+    out = torch.full(q.shape, float("nan"), dtype=out_dtype, device="cuda")
+    odt = K.KVARN_BF16 if out_dtype == torch.bfloat16 else K.KVARN_F32
+    K.kvarn_decode_attention(p, cache, q.shape[1], q, q_dt, out, odt, SCALE, max_len, ws, ws_bytes)
+    torch.cuda.synchronize()
+    return out
+
+
+@settings(max_examples=30, **SETTINGS)
+@given(case=decode_cases)
+def test_gpu_decode_property(K, case):
+    _announce(case)
+    c = case
+    lens, nkv, g, ns = c["lens"], c["n_kv"], c["g"], c["n_sink"]
+    B = len(lens)
+    MB = max(1, max((L - ns) // 128 for L in lens) + 1)
+    gen = torch.Generator(device="cuda").manual_seed(c["seed"])
+    total = int(sum(lens))
+    sc = torch.exp(torch.randn((1, nkv, 128), generator=gen, device="cuda"))
+    k = (torch.randn((max(total, 1), nkv, 128), generator=gen, device="cuda") * sc).to(torch.bfloat16)
+    v = torch.randn((max(total, 1), nkv, 128), generator=gen, device="cuda").to(torch.bfloat16)
+    cu = torch.tensor(np.concatenate([[0], np.cumsum(lens)]), dtype=torch.int32, device="cuda")
+    p = K.kvarn_params_init(c["bits"], aux_format=c["aux"], n_sink=ns)
+    dense = K.Cache(p, B, nkv, MB)
+    caches = [dense]
+    if c["paged"]:
+        n_phys = B * MB + 3
+        paged = K.Cache(p, B, nkv, MB, n_phys=n_phys)
+        perm = torch.randperm(n_phys, generator=torch.Generator().manual_seed(c["seed"]))[:B * MB]
+        paged.block_table.copy_(perm.view(B, MB).to(torch.int32))
+        caches.append(paged)
+    for cache in caches:
+        K.kvarn_prefill(p, cache, k, v, K.KVARN_BF16, cu, max(lens))
+    torch.cuda.synchronize()
+    assert all(int(cache.err_word[0]) == 0 for cache in caches)
+    np.testing.assert_array_equal(dense.seq_len.cpu().numpy(), lens)
+
+    q = torch.randn((B, g * nkv, 128), generator=gen, device="cuda") * 2.0
+    q_dt = K.KVARN_F32
+    if c["q_bf16"]:
+        q, q_dt = q.to(torch.bfloat16), K.KVARN_BF16
+    out_dtype = torch.bfloat16 if c["out_bf16"] else torch.float32
+    max_len = max(lens) + c["hint_extra"]
+    outs = [_decode(K, p, cache, q, q_dt, out_dtype, max_len) for cache in caches]
+    if len(outs) == 2:
+        assert torch.equal(outs[0], outs[1])  # the block table changes addresses, not results
+    got = outs[0].float().cpu().numpy()
+    assert np.all(np.isfinite(got))
+    ref = oracle.decode(host_cache(dense), q_to_host(q), SCALE)
+    check_output(got, ref, bf16_out=c["out_bf16"])

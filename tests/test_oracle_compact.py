@@ -114,3 +114,45 @@ def test_compact_matches_fp32_format_codes_mostly():
     r8 = oracle.quantize_tile(X, 0, oracle.Params(bits=2, aux=1))
     assert r32.best_iter == r8.best_iter
     assert (r32.codes == r8.codes).mean() > 0.8
+
+
+@pytest.mark.parametrize("kind,dist", [(0, "tinyK"), (0, "stressK"), (1, "tinyV")])
+def test_compact_tile_shift_keeps_large_tiles_in_range(kind, dist):
+    """E4M3 holds at most 448 in each of a and s2, while their product is fixed by the data.  A
+    tile whose largest step exceeds 448 moves a tile-wide power of two 2^e into s2: the smallest
+    such e, every dequantized value within the stored format's bound, and errors as small
+    (relative to the tile) as at unit magnitude.  Unit-magnitude tiles keep e = 0."""
+    bits = 2
+    base = make_tile(dist, seed=29)
+    errs = {}
+    for mag in (1.0, 300.0, 3000.0):
+        X = base * mag
+        r = oracle.quantize_tile(X, kind, oracle.Params(bits=bits, aux=1))
+        So = (r.Sr if kind == 0 else r.Sc).astype(np.float64)
+        ratio = r.pre[2] / So
+        e = int(round(np.log2(ratio[0])))
+        assert np.all(ratio == 2.0 ** e)
+        # largest step without the shift, from the E4M3-rounded unshifted s2 (power-of-two
+        # scaling commutes with E4M3 rounding in the normal range)
+        s2_0 = torch.tensor(np.clip(So, 2.0 ** -6, 448.0)).to(torch.float8_e4m3fn).double().numpy()
+        Z0 = r.T / s2_0[:, None] if kind == 0 else r.T / s2_0[None, :]
+        Zg0 = Z0.T if kind == 0 else Z0
+        m0 = float(((Zg0.max(axis=1) - Zg0.min(axis=1)) / ((1 << bits) - 1)).max())
+        if mag == 1.0:
+            assert e == 0 and m0 <= 448.0
+        if e > 0:  # smallest e: one less would not fit (and s2 times 2^e stays within 448)
+            assert m0 * 2.0 ** -(e - 1) > 448.0 >= m0 * 2.0 ** -e
+            assert np.all(So * 2.0 ** e <= 448.0)
+        if mag == 3000.0 and kind == 0:
+            assert e > 0 and m0 > 448.0  # without the shift, a would saturate
+        a, b, s2 = (v.astype(np.float64) for v in (r.a, r.b, r.s2))
+        assert a.max() <= 448.0 and s2.max() <= 448.0
+        if kind == 0:
+            dq = (r.codes * a[None, :] + b[None, :]) * s2[:, None]
+            tol = (a[None, :] / 2 + np.abs(b - r.pre[1])[None, :]) * s2[:, None]
+        else:
+            dq = (r.codes * a[:, None] + b[:, None]) * s2[None, :]
+            tol = (a[:, None] / 2 + np.abs(b - r.pre[1])[:, None]) * s2[None, :]
+        assert np.all(np.abs(r.T - dq) <= tol * (1 + 1e-12) + 1e-12 * np.abs(r.T))
+        errs[mag] = np.linalg.norm(r.T - dq) / np.linalg.norm(r.T)
+    assert errs[300.0] < 1.5 * errs[1.0] and errs[3000.0] < 1.5 * errs[1.0], errs
