@@ -276,6 +276,34 @@ __device__ __forceinline__ void load_q_runs(const DecodeArgs& a, const size_t (&
     }
 }
 
+// o_plain[h] += sum over the chunk's rows of p[h][t] * V[t] for every head slot h, this lane's
+// two channels 2l, 2l + 1 (V bf16, unrotated).  Rows in batches of 32 with all loads in flight;
+// rows past the chunk read its last row (their p is 0).  p is read four tokens at a time, and
+// each head accumulates its tokens in ascending order.
+template <int NHS>
+__device__ __forceinline__ void pv_plain(float (&oplain)[NHS][2], const float (&p)[NHS][kG], const uint16_t* Vp,
+                                         int cn, int l) {
+    for (int t = 0; t < cn; t += 32) {
+        uint32_t v2[32];
+#pragma unroll
+        for (int u = 0; u < 32; ++u)
+            v2[u] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t + u, cn - 1) * kD)[l];
+#pragma unroll
+        for (int u = 0; u < 32; u += 4) {
+#pragma unroll
+            for (int hh = 0; hh < NHS; ++hh) {
+                const float4 ph = *reinterpret_cast<const float4*>(&p[hh][t + u]);
+                const float pv[4] = {ph.x, ph.y, ph.z, ph.w};
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    oplain[hh][0] = fmaf(pv[i], __uint_as_float(v2[u + i] << 16), oplain[hh][0]);
+                    oplain[hh][1] = fmaf(pv[i], __uint_as_float(v2[u + i] & 0xFFFF0000u), oplain[hh][1]);
+                }
+            }
+        }
+    }
+}
+
 template <int BITS, int GQ, int CMP>
 __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
     __shared__ Smem<GQ> sm;
@@ -583,42 +611,23 @@ __global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
 #pragma unroll
                 for (int i = 0; i < 4; ++i) orot[mt][i] *= alpha;
             __syncthreads();  // the previous chunk is done with sm.p / sm.hv
-            if (head_lane) {
+            // every head slot writes its row (slots past g: p = 0, alpha = 1), so that the PV
+            // loop below runs over all slots without a branch per head and token
+            if (n < GQ) {
 #pragma unroll
                 for (int tau = 0; tau < 8; ++tau)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) sm.p[hn][16 * tau + 4 * G + i] = lg[4 * tau + i];
-                if (G == 0) sm.hv[hn][2] = alpha;
+                    for (int i = 0; i < 4; ++i) sm.p[hn][16 * tau + 4 * G + i] = head_lane ? lg[4 * tau + i] : 0.f;
+                if (G == 0) sm.hv[hn][2] = head_lane ? alpha : 1.f;
             }
             __syncthreads();
 #pragma unroll
             for (int h = 0; h < GQ; ++h) {
-                if (h < g) {
-                    const float al = sm.hv[h][2];
-                    oplain[h][0] *= al;
-                    oplain[h][1] *= al;
-                }
+                const float al = sm.hv[h][2];
+                oplain[h][0] *= al;
+                oplain[h][1] *= al;
             }
-            // rows in batches of 32 with all loads in flight; rows past the chunk read its last
-            // row (their p is 0)
-            for (int t = 0; t < cn; t += 32) {
-                uint32_t v2[32];
-#pragma unroll
-                for (int u = 0; u < 32; ++u)
-                    v2[u] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t + u, cn - 1) * kD)[l];
-#pragma unroll
-                for (int u = 0; u < 32; ++u) {
-                    const float v0 = __uint_as_float(v2[u] << 16), v1 = __uint_as_float(v2[u] & 0xFFFF0000u);
-#pragma unroll
-                    for (int h = 0; h < GQ; ++h) {
-                        if (h < g) {
-                            const float ph = sm.p[h][t + u];
-                            oplain[h][0] = fmaf(ph, v0, oplain[h][0]);
-                            oplain[h][1] = fmaf(ph, v1, oplain[h][1]);
-                        }
-                    }
-                }
-            }
+            pv_plain<GQ>(oplain, sm.p, Vp, cn, l);
         }
     }
 
@@ -931,38 +940,42 @@ void k_decode4(DecodeArgs a) {
             }
             __syncthreads();
 
-            // logits of head 4*hg + G, token 64*sg + 16*tau + n
+            // logits of head 4*hg + G, token 64*sg + 16*tau + n.  Tokens outer, head groups
+            // inner: the code planes of a token block are extracted once and used at once.
             float lg[NH][8];
+            v4i aq[NH][2];
+            float beta[NH], fqs[NH];
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
-                v4i aq[2];
 #pragma unroll
                 for (int kap = 0; kap < 2; ++kap) {
                     const uint4 u = sm.qp[hg][j][kap][G][h];
-                    aq[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+                    aq[hg][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
-                const float beta = sm.hv[4 * hg + G][0];                 // q~ grid units
-                const float fqs = sm.hv[4 * hg + G][1] * a.scale_log2;  // grid step * scale
-#pragma unroll
-                for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                    for (int tau = 0; tau < 4; ++tau) {
-                        v4i c = {0, 0, 0, 0};
-#pragma unroll
-                        for (int kap = 0; kap < 2; ++kap)
-                            c = mfma_i8(aq[kap], unit_planes<BITS>(&kw[sg][(2 * tau + kap) * WPU]), c);
-                        lg[hg][4 * sg + tau] =
-                            ((float)digit_sum(c) + beta) * (fqs * sm.aux[2][64 * sg + 16 * tau + n]);
-                    }
+                beta[hg] = sm.hv[4 * hg + G][0];
+                fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
             }
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+                for (int tau = 0; tau < 4; ++tau) {
+                    const v4i b0 = unit_planes<BITS>(&kw[sg][(2 * tau) * WPU]);
+                    const v4i b1 = unit_planes<BITS>(&kw[sg][(2 * tau + 1) * WPU]);
+                    const float s2k = sm.aux[2][64 * sg + 16 * tau + n];
+#pragma unroll
+                    for (int hg = 0; hg < NH; ++hg) {
+                        v4i c = mfma_i8(aq[hg][0], b0, v4i{0, 0, 0, 0});
+                        c = mfma_i8(aq[hg][1], b1, c);
+                        lg[hg][4 * sg + tau] = ((float)digit_sum(c) + beta[hg]) * (fqs[hg] * s2k);
+                    }
+                }
             load_codes(tile_k(id_next), nxt.k);
 
+            v4i ap[NH][2];
+            float alpha[NH], gam[NH], fp[NH];
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
-                const float alpha = softmax_update(lg[hg], false, m_run[hg], l_run[hg]);
-
-                // p~ = p * a_V as fixed point on a per-head grid; gamma from the same rounded
-                // integers
+                alpha[hg] = softmax_update(lg[hg], false, m_run[hg], l_run[hg]);
                 float pmx = 0.f;
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
@@ -971,9 +984,7 @@ void k_decode4(DecodeArgs a) {
                 }
                 pmx = row_max(pmx);
                 const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
-                // tokens 16 tau + .. sit in dword tau of the A operand: even tau scaled by MUL
                 float gam_e = 0.f, gam_o = 0.f;
-                v4i ap[2];
 #pragma unroll
                 for (int sg = 0; sg < 2; ++sg) {
                     uint32_t D[4];
@@ -982,29 +993,28 @@ void k_decode4(DecodeArgs a) {
                         const float yf = fmaf(lg[hg][4 * sg + tau], (tau & 1) ? psc : psc * MUL, MAGIC);
                         if (tau & 1) gam_o = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_o);
                         else gam_e = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_e);
-                        // bytes of y: the three digits plus 128 each, and 0x80 on top (digit
-                        // slot 3 becomes zero); after the transpose lane (head, 4m + i) holds
-                        // digit i of tokens 16 tau + 4m + {0..3}, which lane (m, 4 head + i)
-                        // takes as A operand
                         const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
                         const uint32_t t = quad_transpose_bytes(y, j);
                         D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t) ^ 0x80808080u;
                     }
-                    ap[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
+                    ap[hg][sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
                 }
-                const float gam = row_sum(fmaf(gam_o, MUL, gam_e));  // MUL grid steps
-
-                // PV: head 4*hg + G, channel 16*mt + n
-                const float fp = pmx * (1.0f / (MUL * (float)QMAX));
-#pragma unroll
-                for (int mt = 0; mt < 8; ++mt) {
-                    v4i acc = mfma_i8(ap[0], unit_planes<BITS>(&vw[0][mt * WPU]), v4i{0, 0, 0, 0});
-                    acc = mfma_i8(ap[1], unit_planes<BITS>(&vw[1][mt * WPU]), acc);
-                    orot[hg][mt] = fmaf((float)digit_sum(acc) + gam, fp * sm.aux[5][16 * mt + n],
-                                        orot[hg][mt] * alpha);
-                }
-                if (hg == NH - 1) load_codes(tile_v(id_next), nxt.v);
+                gam[hg] = row_sum(fmaf(gam_o, MUL, gam_e));
+                fp[hg] = pmx * (1.0f / (MUL * (float)QMAX));
             }
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) {
+                const v4i v0 = unit_planes<BITS>(&vw[0][mt * WPU]);
+                const v4i v1 = unit_planes<BITS>(&vw[1][mt * WPU]);
+                const float s2v = sm.aux[5][16 * mt + n];
+#pragma unroll
+                for (int hg = 0; hg < NH; ++hg) {
+                    v4i acc = mfma_i8(ap[hg][0], v0, v4i{0, 0, 0, 0});
+                    acc = mfma_i8(ap[hg][1], v1, acc);
+                    orot[hg][mt] = fmaf((float)digit_sum(acc) + gam[hg], fp[hg] * s2v, orot[hg][mt] * alpha[hg]);
+                }
+            }
+            load_codes(tile_v(id_next), nxt.v);
         };
         // Tiles in pairs, alternating the buffers, so that no register copy (and no wait for a
         // prefetch) is needed between iterations.
@@ -1086,41 +1096,21 @@ void k_decode4(DecodeArgs a) {
                 const float alpha = softmax_update(lg[hg], true, m_run[hg], l_run[hg]);
 #pragma unroll
                 for (int mt = 0; mt < 8; ++mt) orot[hg][mt] *= alpha;
-                if (4 * hg + G < g) {
+                // every head slot writes its row (slots past g: p = 0, alpha = 1), so that the
+                // PV loop below runs over all slots without a branch per head and token
+                const bool real = 4 * hg + G < g;
 #pragma unroll
-                    for (int tau = 0; tau < 8; ++tau) sm.p[4 * hg + G][16 * tau + n] = lg[hg][tau];
-                    if (n == 0) sm.hv[4 * hg + G][2] = alpha;
-                }
+                for (int tau = 0; tau < 8; ++tau) sm.p[4 * hg + G][16 * tau + n] = real ? lg[hg][tau] : 0.f;
+                if (n == 0) sm.hv[4 * hg + G][2] = real ? alpha : 1.f;
             }
             __syncthreads();
 #pragma unroll
             for (int hh = 0; hh < NHD; ++hh) {
-                if (hh < g) {
-                    const float al = sm.hv[hh][2];
-                    oplain[hh][0] *= al;
-                    oplain[hh][1] *= al;
-                }
+                const float al = sm.hv[hh][2];
+                oplain[hh][0] *= al;
+                oplain[hh][1] *= al;
             }
-            // rows in batches of 32 with all loads in flight; rows past the chunk read its last
-            // row (their p is 0)
-            for (int t = 0; t < cn; t += 32) {
-                uint32_t v2[32];
-#pragma unroll
-                for (int u = 0; u < 32; ++u)
-                    v2[u] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t + u, cn - 1) * kD)[l];
-#pragma unroll
-                for (int u = 0; u < 32; ++u) {
-                    const float v0 = __uint_as_float(v2[u] << 16), v1 = __uint_as_float(v2[u] & 0xFFFF0000u);
-#pragma unroll
-                    for (int hh = 0; hh < NHD; ++hh) {
-                        if (hh < g) {
-                            const float ph = sm.p[hh][t + u];
-                            oplain[hh][0] = fmaf(ph, v0, oplain[hh][0]);
-                            oplain[hh][1] = fmaf(ph, v1, oplain[hh][1]);
-                        }
-                    }
-                }
-            }
+            pv_plain<NHD>(oplain, sm.p, Vp, cn, l);
         }
     }
 
