@@ -125,3 +125,69 @@ def test_gpu_decode_property(K, case):
     assert np.all(np.isfinite(got))
     ref = oracle.decode(host_cache(dense), q_to_host(q), SCALE)
     check_output(got, ref, bf16_out=c["out_bf16"])
+
+
+append_cases = st.fixed_dictionaries(dict(
+    bits=st.sampled_from([2, 4]), aux=st.sampled_from([0, 1]), n_sink=st.sampled_from([0, 3, 128]),
+    n_kv=st.integers(1, 2), seed=st.integers(0, 2 ** 31 - 1), steps=st.integers(1, 200), lock_step=st.booleans(),
+    lens=st.lists(st.integers(0, 2 * 128 + 60), min_size=1, max_size=3)))
+
+
+@settings(max_examples=15, **SETTINGS)
+@given(case=append_cases)
+def test_gpu_append_property(K, case):
+    """Prefilled prompts of random lengths, then `steps` appends (with the lock-step length hint
+    when all lengths agree, else without): sink and residual rows bit-equal to the oracle's,
+    every body tile (prefilled or flushed) to the tile bar against its 128 input tokens, and
+    decode over the result to the output bar."""
+    _announce(case)
+    c = case
+    lens = [c["lens"][0]] * len(c["lens"]) if c["lock_step"] else c["lens"]
+    nkv, ns, steps, bits = c["n_kv"], c["n_sink"], c["steps"], c["bits"]
+    B = len(lens)
+    final = [L + steps for L in lens]
+    MB = max(1, max((L - ns) // 128 for L in final) + 1)
+    gen = torch.Generator(device="cuda").manual_seed(c["seed"])
+    sc = torch.exp(torch.randn((1, nkv, 128), generator=gen, device="cuda"))
+    total = int(sum(lens))
+    k = (torch.randn((max(total, 1), nkv, 128), generator=gen, device="cuda") * sc).to(torch.bfloat16)
+    v = torch.randn((max(total, 1), nkv, 128), generator=gen, device="cuda").to(torch.bfloat16)
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    p = K.kvarn_params_init(bits, aux_format=c["aux"], n_sink=ns)
+    po = oracle.Params(bits=bits, aux=c["aux"])
+    cache = K.Cache(p, B, nkv, MB)
+    K.kvarn_prefill(p, cache, k, v, K.KVARN_BF16, torch.tensor(cu, device="cuda"), max(lens))
+    hc = oracle.HostCache(B, nkv, MB, bits=bits, n_sink=ns, aux=c["aux"])
+    kh, vh = q_to_host(k), q_to_host(v)
+    assert oracle.prefill(hc, kh, vh, cu, max(lens), po) == 0
+    hist = {0: [list(kh[cu[b]:cu[b + 1]]) for b in range(B)], 1: [list(vh[cu[b]:cu[b + 1]]) for b in range(B)]}
+    for t in range(steps):
+        kt = (torch.randn((B, nkv, 128), generator=gen, device="cuda") * sc).to(torch.bfloat16)
+        vt = torch.randn((B, nkv, 128), generator=gen, device="cuda").to(torch.bfloat16)
+        K.kvarn_append_token(p, cache, kt, vt, K.KVARN_BF16, lens[0] + t if c["lock_step"] else -1)
+        kth, vth = q_to_host(kt), q_to_host(vt)
+        assert oracle.append(hc, kth, vth, po) == 0
+        for b in range(B):
+            hist[0][b].append(kth[b])
+            hist[1][b].append(vth[b])
+    torch.cuda.synchronize()
+    assert int(cache.err_word[0]) == 0
+    gc = host_cache(cache)
+    np.testing.assert_array_equal(gc.seq_len, final)
+    np.testing.assert_array_equal(hc.seq_len, final)
+    cmp = compare_tiles if c["aux"] == 0 else compare_tiles_compact
+    for b, L in enumerate(final):
+        nb = (L - ns) // 128 if L > ns else 0
+        nr = (L - ns) % 128 if L > ns else 0
+        for f in ("k_resid", "v_resid"):
+            np.testing.assert_array_equal(getattr(gc, f)[b, :, :nr], getattr(hc, f)[b, :, :nr], err_msg=f)
+        for f in ("k_sink", "v_sink"):
+            np.testing.assert_array_equal(getattr(gc, f)[b, :, :min(L, ns)], getattr(hc, f)[b, :, :min(L, ns)])
+        for kind, body in ((0, gc.k_body), (1, gc.v_body)):
+            rows = np.stack(hist[kind][b])  # [L][n_kv][128] bf16 bits
+            for blk in range(nb):
+                X = oracle.bf16_bits_to_f64(rows[ns + blk * 128:ns + (blk + 1) * 128].transpose(1, 0, 2))
+                cmp(body[b, :, blk], X, kind, bits)
+    q = torch.randn((B, 4 * nkv, 128), generator=gen, device="cuda").to(torch.bfloat16)
+    out = _decode(K, p, cache, q, K.KVARN_BF16, torch.float32, max(final) + 1)
+    check_output(out.cpu().numpy(), oracle.decode(gc, q_to_host(q), SCALE), bf16_out=False)
