@@ -12,7 +12,7 @@ from hypothesis import strategies as st
 
 import oracle
 from gpu_util import check_output, compare_tiles, compare_tiles_compact, host_cache, q_to_host, tiles_to_host
-from test_oracle_properties import STRUCTURES, make_tile
+from tiles import STRUCTURES, make_tile
 
 pytestmark = pytest.mark.gpu
 
