@@ -753,21 +753,45 @@ constexpr float kPlaneMul = BITS == 2 ? 4.f : 1.f;
 
 // Query heads are taken in groups of four (NH groups, g <= 4 * NH): every group repeats the
 // per-head work on the same code operands, which are extracted once per tile.
-template <int NH>
+template <int NH, int X1>
 struct Smem4 {
-    float q[4 * NH][kD];       // rotated q (rows >= g zero); reused for the inverse rotation of the output
-    float aux[6][kD];          // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
-    uint4 qp[NH][4][2][4][4];  // q~ digit planes [group][digit slot][kappa][G][head]; slot 3 stays zero
-    float hv[4 * NH][4];       // per head: beta, q~ step, alpha, l
-    float p[4 * NH][kG];       // probabilities of a bf16 chunk (sink / residual)
+    float q[4 * NH + X1][kD];       // rotated q (rows >= g zero); reused for the inverse rotation of the output
+    float aux[6][kD];               // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
+    uint4 qp[NH][4][2][4][4];       // q~ digit planes [group][digit slot][kappa][G][head]; slot 3 stays zero
+    uint4 qp4[X1 ? 4 : 1][2][4];    // X1: the extra head's q~ digit planes [digit slot][kappa][G]; slot 3 zero
+    float hv[4 * NH + X1][4];       // per head: beta, q~ step, alpha, l
+    float p[4 * NH + X1][kG];       // probabilities of a bf16 chunk (sink / residual)
 };
 
-template <int BITS, int NH, int CMP, int PG>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 ? 3 : 2, 8)))
+// Max and sum over the whole wave (the four DPP rows, then row pairs): every lane ends with
+// the same value.
+template <class F>
+__device__ __forceinline__ float across_rows4(float v, F f) {
+    const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    v = f(__uint_as_float(x[0]), __uint_as_float(x[1]));
+    const auto y = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return f(__uint_as_float(y[0]), __uint_as_float(y[1]));
+}
+__device__ __forceinline__ float wave_max(float v) {
+    return across_rows4(row_max(v), [](float x, float y) { return fmaxf(x, y); });
+}
+__device__ __forceinline__ float wave_sum(float v) {
+    return across_rows4(row_sum(v), [](float x, float y) { return x + y; });
+}
+
+// X1 = 1 (group size 5, with NH = 1): a fifth query head spread over the whole wave instead of a
+// second head group of four slots.  Its logits for a token block land in one row group of the
+// MFMA output (its digits sit in that group's A rows, the other rows are zero), so lane (G, n)
+// holds it for tokens 64 sg + 16 G + n and output channels 16 (4 q + G) + n (sg, q = 0, 1): two
+// values per lane instead of eight, and no padded head slots.
+template <int BITS, int NH, int CMP, int PG, int X1>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
-    __shared__ Smem4<NH> sm;
+    static_assert(X1 == 0 || NH == 1, "the extra head is only for one head group");
+    __shared__ Smem4<NH, X1> sm;
     constexpr int WPU = BITS / 2;
-    constexpr int NHD = 4 * NH;  // head slots
+    constexpr int NHD = 4 * NH;   // head slots of the head groups
+    constexpr int NHX = NHD + X1;  // all head slots
     // Fixed point: q~ and p~ in even dwords of the A operand are scaled by MUL (the code planes
     // there are not shifted up), so every product term carries weight MUL.  The exact sum is
     // bounded by MUL * (2^BITS - 1) * 128 * QMAX < 2^31 and MUL * QMAX < 2^22 keeps the
@@ -798,6 +822,9 @@ void k_decode4(DecodeArgs a) {
 
     float m_run[NH], l_run[NH];  // head 4*hg + G; l_run is this lane's partial sum
     float orot[NH][8];           // head 4*hg + G, channel 16*mt + n (rotated domain)
+    // X1: the extra head's running max, this lane's partial sum, and its output channels
+    // 16 (4 q + G) + n, q = 0, 1
+    float m4 = -INFINITY, l4 = 0.f, orot4[2] = {0.f, 0.f};
 #pragma unroll
     for (int hg = 0; hg < NH; ++hg) {
         m_run[hg] = -INFINITY;
@@ -818,6 +845,24 @@ void k_decode4(DecodeArgs a) {
         float s = 0.f;
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
+            float p = __builtin_amdgcn_exp2f(lg[k] - m_new);
+            if (maybe_absent) p = lg[k] == -INFINITY ? 0.f : p;
+            lg[k] = p;
+            s += p;
+        }
+        lsum = lsum * alpha + s;
+        m = m_new;
+        return alpha;
+    };
+
+    // the same for the extra head, whose 128 logits are spread over the wave (two per lane)
+    auto softmax_wave = [](float (&lg)[2], bool maybe_absent, float& m, float& lsum) -> float {
+        const float mx = wave_max(fmaxf(lg[0], lg[1]));
+        const float m_new = fmaxf(m, mx);
+        const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
+        float s = 0.f;
+#pragma unroll
+        for (int k = 0; k < 2; ++k) {
             float p = __builtin_amdgcn_exp2f(lg[k] - m_new);
             if (maybe_absent) p = lg[k] == -INFINITY ? 0.f : p;
             lg[k] = p;
@@ -856,11 +901,12 @@ void k_decode4(DecodeArgs a) {
         load_codes(tile_v(id0), ra.v);
         load_aux(ra, id0);
 
-        q_to_lds<NHD>(sm.q, a, qrow, g, l);
+        q_to_lds<NHX>(sm.q, a, qrow, g, l);
         for (int idx = l; idx < NH * 32; idx += 64)
             sm.qp[idx >> 5][3][(idx >> 4) & 1][(idx >> 2) & 3][idx & 3] = make_uint4(0u, 0u, 0u, 0u);
+        if (X1 && l < 8) sm.qp4[X1 ? 3 : 0][l >> 2][l & 3] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
-        if (a.rotate) lds_hadamard<NHD>(sm.q, g);
+        if (a.rotate) lds_hadamard<NHX>(sm.q, g);
         // q~ role: head 4*hg + G, channels 8n .. 8n + 7 (rotated and normalized, or as given)
         const float qs = a.rotate ? kInvSqrt128 : 1.f;
         float qr[NH][8];
@@ -868,8 +914,12 @@ void k_decode4(DecodeArgs a) {
         for (int hg = 0; hg < NH; ++hg)
 #pragma unroll
             for (int k = 0; k < 8; ++k) qr[hg][k] = sm.q[4 * hg + G][8 * n + k] * qs;
-        // source lane of the PV operand permutation (see above), as a byte address
+        // extra head: channels 2l, 2l + 1
+        const float qr4[2] = {X1 ? sm.q[NHX - 1][2 * l] * qs : 0.f, X1 ? sm.q[NHX - 1][2 * l + 1] * qs : 0.f};
+        // source lane of the PV operand permutation (see above), as a byte address; for the
+        // extra head the source row is the token block (tau), not the head
         const int perm_addr = (16 * h + 4 * G + j) * 4;
+        const int perm4 = (4 * G + j) * 4;
 
         // One tile: consume cur, prefetch tile id_next into nxt.
         auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
@@ -937,6 +987,33 @@ void k_decode4(DecodeArgs a) {
                         sm.hv[4 * hg + G][1] = mx * (1.0f / (MUL * (float)QMAX));
                     }
                 }
+                if constexpr (X1) {
+                    // extra head: channels 2l, 2l + 1 = kappa l / 32, group (l / 8) % 4, bytes
+                    // 2 (l % 8) + {0, 1} of that group (an even dword when (l / 2) % 2 == 0);
+                    // grid, digits and beta as for the head groups, over the whole wave
+                    const float2 a2 = *reinterpret_cast<const float2*>(&sm.aux[0][2 * l]);
+                    const float2 r2 = *reinterpret_cast<const float2*>(&sm.aux[1][2 * l]);
+                    const float qt0 = qr4[0] * a2.x, qt1 = qr4[1] * a2.y;
+                    const float mx = wave_max(fmaxf(fabsf(qt0), fabsf(qt1)));
+                    const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
+                    const bool even = ((l >> 1) & 1) == 0;
+                    const float y0f = fmaf(qt0, even ? sc * MUL : sc, MAGIC);
+                    const float y1f = fmaf(qt1, even ? sc * MUL : sc, MAGIC);
+                    const float bsl = fmaf(y1f - MAGIC, r2.y, (y0f - MAGIC) * r2.x);
+                    const float bs = wave_sum(even ? bsl : bsl * MUL);
+                    const uint32_t y0 = __float_as_uint(y0f) + (0x808080u - MAGIC_BITS);
+                    const uint32_t y1 = __float_as_uint(y1f) + (0x808080u - MAGIC_BITS);
+                    const uint32_t d01 = perm(y1, y0, 0x05010400u) ^ 0x80808080u;  // digit 0 | digit 1 pairs
+                    const uint32_t d2 = perm(y1, y0, 0x0c0c0602u) ^ 0x8080u;       // digit 2 pair
+                    const int kp = l >> 5, gq = (l >> 3) & 3, e = l & 7;
+                    reinterpret_cast<uint16_t*>(&sm.qp4[0][kp][gq])[e] = (uint16_t)(d01 & 0xFFFFu);
+                    reinterpret_cast<uint16_t*>(&sm.qp4[X1 ? 1 : 0][kp][gq])[e] = (uint16_t)(d01 >> 16);
+                    reinterpret_cast<uint16_t*>(&sm.qp4[X1 ? 2 : 0][kp][gq])[e] = (uint16_t)d2;
+                    if (l == 0) {
+                        sm.hv[NHX - 1][0] = bs;
+                        sm.hv[NHX - 1][1] = mx * (1.0f / (MUL * (float)QMAX));
+                    }
+                }
             }
             __syncthreads();
 
@@ -955,6 +1032,17 @@ void k_decode4(DecodeArgs a) {
                 beta[hg] = sm.hv[4 * hg + G][0];
                 fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
             }
+            // extra head: its digits in the A rows of row group tau for token block tau, so that
+            // block tau's logits land in lanes G == tau; one accumulator per sg collects them
+            const v4i z4 = {0, 0, 0, 0};
+            v4i aq4[2] = {z4, z4}, c4[2] = {z4, z4};
+            if constexpr (X1) {
+#pragma unroll
+                for (int kap = 0; kap < 2; ++kap) {
+                    const uint4 u = sm.qp4[j][kap][G];
+                    aq4[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
+                }
+            }
 #pragma unroll
             for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
@@ -968,7 +1056,19 @@ void k_decode4(DecodeArgs a) {
                         c = mfma_i8(aq[hg][1], b1, c);
                         lg[hg][4 * sg + tau] = ((float)digit_sum(c) + beta[hg]) * (fqs[hg] * s2k);
                     }
+                    if constexpr (X1) {
+                        const bool mine = h == tau;
+                        c4[sg] = mfma_i8(mine ? aq4[0] : z4, b0, c4[sg]);
+                        c4[sg] = mfma_i8(mine ? aq4[1] : z4, b1, c4[sg]);
+                    }
                 }
+            float lg4[2] = {0.f, 0.f};  // extra head, tokens 64 sg + 16 G + n
+            if constexpr (X1) {
+                const float beta4 = sm.hv[NHX - 1][0], fqs4 = sm.hv[NHX - 1][1] * a.scale_log2;
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg)
+                    lg4[sg] = ((float)digit_sum(c4[sg]) + beta4) * (fqs4 * sm.aux[2][64 * sg + 16 * G + n]);
+            }
             load_codes(tile_k(id_next), nxt.k);
 
             v4i ap[NH][2];
@@ -1002,6 +1102,34 @@ void k_decode4(DecodeArgs a) {
                 gam[hg] = row_sum(fmaf(gam_o, MUL, gam_e));
                 fp[hg] = pmx * (1.0f / (MUL * (float)QMAX));
             }
+            // extra head: lane (G, n) holds token 64 sg + 16 G + n, i.e. token block tau = G of
+            // each sg, so the byte transpose and the operand permutation are those of the head
+            // groups with the source row taken from the token block instead of the head
+            v4i ap4[2] = {z4, z4}, acc4[2] = {z4, z4};
+            float alpha4 = 0.f, gam4 = 0.f, fp4 = 0.f;
+            if constexpr (X1) {
+                alpha4 = softmax_wave(lg4, false, m4, l4);
+                lg4[0] *= sm.aux[3][16 * G + n];
+                lg4[1] *= sm.aux[3][64 + 16 * G + n];
+                const float pmx = wave_max(fmaxf(lg4[0], lg4[1]));
+                const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
+                const float ps = (G & 1) ? psc : psc * MUL;
+                float gl = 0.f;
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg) {
+                    const float yf = fmaf(lg4[sg], ps, MAGIC);
+                    gl = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * G + n], gl);
+                    const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
+                    const uint32_t t = quad_transpose_bytes(y, j);
+                    uint32_t D[4];
+#pragma unroll
+                    for (int tau = 0; tau < 4; ++tau)
+                        D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm4 + 64 * tau, (int)t) ^ 0x80808080u;
+                    ap4[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
+                }
+                gam4 = wave_sum((G & 1) ? gl * MUL : gl);
+                fp4 = pmx * (1.0f / (MUL * (float)QMAX));
+            }
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) {
                 const v4i v0 = unit_planes<BITS>(&vw[0][mt * WPU]);
@@ -1013,6 +1141,18 @@ void k_decode4(DecodeArgs a) {
                     acc = mfma_i8(ap[hg][1], v1, acc);
                     orot[hg][mt] = fmaf((float)digit_sum(acc) + gam[hg], fp[hg] * s2v, orot[hg][mt] * alpha[hg]);
                 }
+                if constexpr (X1) {
+                    // channel block mt lands in lanes G == mt % 4 (A rows of that row group)
+                    const bool mine = h == (mt & 3);
+                    acc4[mt >> 2] = mfma_i8(mine ? ap4[0] : z4, v0, acc4[mt >> 2]);
+                    acc4[mt >> 2] = mfma_i8(mine ? ap4[1] : z4, v1, acc4[mt >> 2]);
+                }
+            }
+            if constexpr (X1) {
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    orot4[q] = fmaf((float)digit_sum(acc4[q]) + gam4, fp4 * sm.aux[5][16 * (4 * q + G) + n],
+                                    orot4[q] * alpha4);
             }
             load_codes(tile_v(id_next), nxt.v);
         };
@@ -1030,9 +1170,9 @@ void k_decode4(DecodeArgs a) {
     }
 
     // ---- sink and residual (bf16, unrotated): last split only ------------------------------
-    float oplain[NHD][2];  // head hh, channel 2*l + jj (unrotated)
+    float oplain[NHX][2];  // head hh, channel 2*l + jj (unrotated)
 #pragma unroll
-    for (int hh = 0; hh < NHD; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
+    for (int hh = 0; hh < NHX; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
     if (last && ns + nr > 0) {
         // A operand of group hg: row 4h holds q of head 4*hg + h rounded to bf16, row 4h + 1 the
         // remainder (zero for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds
@@ -1059,6 +1199,23 @@ void k_decode4(DecodeArgs a) {
                     }
             }
         }
+        // extra head: the same rows (hi, lo) of its q, placed in row group tau % 4 at use
+        v8bf aqs4[4];
+        if constexpr (X1) {
+            size_t qi[4];
+            float qv[4][8];
+#pragma unroll
+            for (int k = 0; k < 4; ++k) qi[k] = (qrow + NHX - 1) * kD + 32 * k + 8 * G;
+            load_q_runs<4>(a, qi, qv);
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const float v = j < 2 ? qv[k][e] : 0.f;
+                    const __bf16 hi = (__bf16)v;
+                    aqs4[k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
+                }
+        }
         const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
         for (int chunk = 0; chunk <= nsc; ++chunk) {
             const bool in_sink = chunk < nsc;
@@ -1073,6 +1230,7 @@ void k_decode4(DecodeArgs a) {
             // logits of head 4*hg + G, token 16*tau + n.  Rows past the chunk read its last row
             // (in bounds) and are masked, so no load waits behind a branch.
             float lg[NH][8];
+            v4f r4[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
             for (int tau = 0; tau < 8; ++tau) {
                 const int trow = 16 * tau + n;
@@ -1090,6 +1248,26 @@ void k_decode4(DecodeArgs a) {
                     for (int k = 0; k < 4; ++k) acc = mfma_bf16(aqs[hg][k], B[k], acc);
                     lg[hg][tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
                 }
+                if constexpr (X1) {
+                    // token block tau lands in lanes G == tau % 4 of accumulator tau / 4
+                    const bool mine = h == (tau & 3);
+                    const v8bf zb = {};
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) r4[tau >> 2] = mfma_bf16(mine ? aqs4[k] : zb, B[k], r4[tau >> 2]);
+                }
+            }
+            if constexpr (X1) {
+                // extra head, tokens 16 (4 q + G) + n
+                float lgx[2];
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+                    lgx[q] = 16 * (4 * q + G) + n < cn ? (r4[q][0] + r4[q][1]) * a.scale_log2 : -INFINITY;
+                const float alpha = softmax_wave(lgx, true, m4, l4);
+                orot4[0] *= alpha;
+                orot4[1] *= alpha;
+#pragma unroll
+                for (int q = 0; q < 2; ++q) sm.p[NHX - 1][16 * (4 * q + G) + n] = lgx[q];
+                if (l == 0) sm.hv[NHX - 1][2] = alpha;
             }
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
@@ -1105,12 +1283,12 @@ void k_decode4(DecodeArgs a) {
             }
             __syncthreads();
 #pragma unroll
-            for (int hh = 0; hh < NHD; ++hh) {
+            for (int hh = 0; hh < NHX; ++hh) {
                 const float al = sm.hv[hh][2];
                 oplain[hh][0] *= al;
                 oplain[hh][1] *= al;
             }
-            pv_plain<NHD>(oplain, sm.p, Vp, cn, l);
+            pv_plain<NHX>(oplain, sm.p, Vp, cn, l);
         }
     }
 
@@ -1118,6 +1296,7 @@ void k_decode4(DecodeArgs a) {
     float lt[NH];
 #pragma unroll
     for (int hg = 0; hg < NH; ++hg) lt[hg] = row_sum(l_run[hg]);
+    const float lt4 = X1 ? wave_sum(l4) : 0.f;
     if (a.n_split == 1) {
         __syncthreads();
 #pragma unroll
@@ -1128,11 +1307,16 @@ void k_decode4(DecodeArgs a) {
                 if (n == 0) sm.hv[4 * hg + G][3] = lt[hg];
             }
         }
+        if constexpr (X1) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) sm.q[NHX - 1][16 * (4 * q + G) + n] = orot4[q];
+            if (l == 0) sm.hv[NHX - 1][3] = lt4;
+        }
         __syncthreads();
-        if (a.rotate) lds_hadamard<NHD>(sm.q, g);
+        if (a.rotate) lds_hadamard<NHX>(sm.q, g);
         const float rs = a.rotate ? kInvSqrt128 : 1.f;
 #pragma unroll
-        for (int hh = 0; hh < NHD; ++hh) {
+        for (int hh = 0; hh < NHX; ++hh) {
             if (hh < g) {
                 const float L = sm.hv[hh][3];
                 float o0 = sm.q[hh][2 * l] * rs + oplain[hh][0];
@@ -1160,8 +1344,17 @@ void k_decode4(DecodeArgs a) {
                 }
             }
         }
+        if constexpr (X1) {
+            float* P = a.ws + ((qrow + NHX - 1) * a.n_split + split) * kPart;
 #pragma unroll
-        for (int hh = 0; hh < NHD; ++hh) {
+            for (int q = 0; q < 2; ++q) P[4 + 16 * (4 * q + G) + n] = orot4[q];
+            if (l == 0) {
+                P[0] = m4;
+                P[1] = lt4;
+            }
+        }
+#pragma unroll
+        for (int hh = 0; hh < NHX; ++hh) {
             if (hh < g) {
                 float* P = a.ws + ((qrow + hh) * a.n_split + split) * kPart;
                 *reinterpret_cast<float2*>(P + 132 + 2 * l) = make_float2(oplain[hh][0], oplain[hh][1]);
@@ -1247,11 +1440,14 @@ hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const dim3 grid((unsigned)(streams * a.n_split));
     const bool pg = a.block_table != nullptr;
     if constexpr (GQ == 4) {
-        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1>), grid, dim3(64), 0, stream, a);
-        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0>), grid, dim3(64), 0, stream, a);
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 0>), grid, dim3(64), 0, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0, 0>), grid, dim3(64), 0, stream, a);
+    } else if constexpr (GQ == 5) {
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 1>), grid, dim3(64), 0, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0, 1>), grid, dim3(64), 0, stream, a);
     } else if constexpr (GQ == 8) {
-        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 1>), grid, dim3(64), 0, stream, a);
-        else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0>), grid, dim3(64), 0, stream, a);
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 1, 0>), grid, dim3(64), 0, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0, 0>), grid, dim3(64), 0, stream, a);
     } else
         hipLaunchKernelGGL((k_decode<BITS, GQ, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
     hipError_t e = hipGetLastError();
@@ -1263,6 +1459,7 @@ hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
 template <int BITS, int CMP>
 hipError_t launch_bits(const DecodeArgs& a, int batch, hipStream_t stream) {
     if (a.g <= 4) return launch_cfg<BITS, 4, CMP>(a, batch, stream);
+    if (a.g == 5) return launch_cfg<BITS, 5, CMP>(a, batch, stream);
     if (a.g <= 8) return launch_cfg<BITS, 8, CMP>(a, batch, stream);
     return launch_cfg<BITS, 16, CMP>(a, batch, stream);
 }

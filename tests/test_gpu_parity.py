@@ -160,9 +160,9 @@ def test_decode_variants(K, bits, n_sink, name):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
-@pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (12, 2), (32, 2)])
+@pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (10, 2), (12, 2), (32, 2)])
 def test_decode_group_sizes(K, n_q, n_kv):
-    """Every query-group size class (1 .. 4, 5 .. 8, 9 .. 16 take different kernels), with a
+    """Every query-group size class (1 .. 4, 5, 6 .. 8, 9 .. 16 take different kernels), with a
     residual and enough body tiles for the plan to split every stream."""
     from paper_2606_03458_amd import workloads
     built, _ = workloads.build("llama", context=12 * 128 + 45, batch=2, n_q=n_q, n_kv=n_kv)

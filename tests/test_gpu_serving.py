@@ -121,9 +121,9 @@ def test_paged_equals_dense(K):
 
 @pytest.mark.parametrize("bits", [2, 4])
 @pytest.mark.parametrize("aux", [0, 1])
-@pytest.mark.parametrize("g", [4, 5, 12])
+@pytest.mark.parametrize("g", [4, 5, 6, 12])
 def test_paged_every_kernel(K, bits, aux, g):
-    """Every decode kernel (code width x aux format x query-group class 1-4, 5-8, 9-16) on a
+    """Every decode kernel (code width x aux format x query-group class 1-4, 5, 6-8, 9-16) on a
     permuted pool: bit-equal to the dense layout and within the output bar of the oracle, with
     ragged lengths (a residual, an exact block boundary, a sequence shorter than one block)."""
     lens = [9 * 128 + 77, 3 * 128, 90]  # 9 body tiles: the plan splits the longest stream in two
