@@ -112,6 +112,7 @@ def lib():
         L.kvo_quantize_tile.argtypes = [vp, ctypes.c_int, ctypes.POINTER(_Params), vp, vp, vp, vp, vp, vp, vp, vp,
                                         vp, vp, vp, vp]
         L.kvo_tile_bytes.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.kvo_set_threads.argtypes = [ctypes.c_int]
         L.kvo_tile_bytes.restype = ctypes.c_size_t
         L.kvo_pack_tile.argtypes = [vp, vp, vp, vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp]
         L.kvo_unpack_tile.argtypes = [vp, ctypes.c_int, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp]
@@ -236,6 +237,11 @@ def quantize_tile(X, kind: int, params: Params = Params()) -> TileResult:
     lib().kvo_quantize_tile(_p(X), kind, ctypes.byref(pc), _p(codes), _p(a), _p(b), _p(s2), _p(T), _p(B), _p(u),
                             _p(Sc), _p(Sr), _p(imb), ctypes.cast(ctypes.byref(best), ctypes.c_void_p), _p(pre))
     return TileResult(codes, a, b, s2, T, B, u, Sc, Sr, imb, best.value, pre)
+
+
+def set_threads(n: int) -> None:
+    """Threads of the oracle's parallel loops (timing only; results do not depend on it)."""
+    lib().kvo_set_threads(int(n))
 
 
 def tile_bytes(bits: int, aux: int = 0) -> int:

@@ -26,6 +26,9 @@
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 #define D 128   /* head_dim: channels per token                       (Sec. 2.1) */
 #define G 128   /* tokens per quantization group / block              (Sec. 2.1, App. D) */
@@ -814,4 +817,14 @@ int kvo_prefill(kvo_cache *cc, const void *k, const void *v, int dtype, const in
         cc->seq_len[bi] = L;
     }
     return ret;
+}
+
+/* Thread count of the parallel loops over tiles and streams (timing only; results do not
+ * depend on it: every tile and stream is computed by one thread in a fixed order). */
+void kvo_set_threads(int n) {
+#ifdef _OPENMP
+    omp_set_num_threads(n > 0 ? n : 1);
+#else
+    (void)n;
+#endif
 }
