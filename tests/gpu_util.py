@@ -57,13 +57,15 @@ def _tile_mismatch(codes, a, b, s2, r, qmax):
 
 
 def compare_tiles(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gpu_best=None, params=None,
-                  tie_fraction: float = TIE_FRACTION):
+                  tie_fraction: float = TIE_FRACTION, max_best_ties=None):
     """gpu_tiles [n, tile_bytes] uint8 (GPU output); X [n, 128, 128] float64 (exact input).
 
     A tile whose kept VarN iteration differs from the oracle's is still compared code by
     code; only if that comparison fails and the two iterations' imbalances agree to 1e-5
     (a tie at fp32 resolution) is it checked against the dequantization bound instead.
-    Returns a stats dict; raises AssertionError on any violation."""
+    max_best_ties bounds such tiles (default: 1 % of the tiles, at least one); degenerate tiles
+    (constant rows or columns, where clamped variances make Imb values tie systematically) may
+    pass a larger bound.  Returns a stats dict; raises AssertionError on any violation."""
     params = params or oracle.Params(bits=bits)
     qmax = (1 << bits) - 1
     n = gpu_tiles.shape[0]
@@ -90,7 +92,7 @@ def compare_tiles(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gp
         stats["excused"] += excused
         stats["max_aux_rel"] = max(stats["max_aux_rel"], aux)
     assert stats["excused"] <= tie_fraction * max(stats["codes"], 1) + 1, stats
-    assert stats["best_ties"] <= max(1, n // 100), stats
+    assert stats["best_ties"] <= (max(1, n // 100) if max_best_ties is None else max_best_ties), stats
     return stats
 
 
@@ -191,11 +193,11 @@ def _near_e4m3_boundary(x: float, upward: bool) -> bool:
     return bool(np.min(np.abs(bounds - x)) <= FORMAT_TIE * abs(x))
 
 
-def _near_fp16_midpoint(x: float) -> bool:
+def _near_fp16_midpoint(x: float, slack: float = 0.0) -> bool:
     h = np.float16(x)
     up, dn = np.nextafter(h, np.float16(np.inf)), np.nextafter(h, np.float16(-np.inf))
     mids = [(float(h) + float(up)) / 2, (float(h) + float(dn)) / 2]
-    return min(abs(m - x) for m in mids) <= FORMAT_TIE * abs(x)
+    return min(abs(m - x) for m in mids) <= FORMAT_TIE * abs(x) + slack
 
 
 def _near_shift_tie(r, kind) -> bool:
@@ -219,9 +221,12 @@ def _compact_tile_status(codes, a, b, s2, r, kind):
         tie = tie or _near_shift_tie(r, kind)
         return ("tie" if tie else "mismatch"), 0, 0
     b_bad = np.flatnonzero(b != r.b)
+    # the group minimum comes out of the rotation, a sum of 128 terms: in fp32 its absolute
+    # error scales with the tile's magnitude, not with the (possibly cancelled) value itself
+    slack = 2.0 ** -20 * float(np.abs(r.T).max()) / float(r.s2.astype(np.float64).min()) if b_bad.size else 0.0
     for k in b_bad:
         adjacent = np.nextafter(np.float16(r.b[k]), np.float16(b[k])) == np.float16(b[k])
-        if not (adjacent and _near_fp16_midpoint(r.pre[1][k])):
+        if not (adjacent and _near_fp16_midpoint(r.pre[1][k], slack)):
             return "mismatch", 0, 0
     mism = codes != r.codes
     if not mism.any():
@@ -236,7 +241,7 @@ def _compact_tile_status(codes, a, b, s2, r, kind):
 
 
 def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits: int, gpu_best=None,
-                          varn_iters: int = 8):
+                          varn_iters: int = 8, max_ties=None, tie_fraction: float = TIE_FRACTION):
     """compare_tiles for the compact aux format (see the comment above for the tie rules).  As
     there, a tile whose kept VarN iteration differs is still compared value by value first."""
     params = oracle.Params(bits=bits, aux=1, varn_iters=varn_iters)
@@ -278,8 +283,8 @@ def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits:
             assert status == "tie", (i, status)
         stats["ties"] += 1
         _check_dequant_bound_compact(gpu_tiles[i], X[i], kind, bits)
-    assert stats["excused"] <= TIE_FRACTION * max(stats["codes"], 1) + 1, stats
-    assert stats["ties"] <= max(1, n // 100), stats
+    assert stats["excused"] <= tie_fraction * max(stats["codes"], 1) + 1, stats
+    assert stats["ties"] <= (max(1, n // 100) if max_ties is None else max_ties), stats
     return stats
 
 

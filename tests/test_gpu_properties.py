@@ -4,6 +4,8 @@ magnitude, bit width, kind, aux format and input dtype, and decode attention ove
 caches of random batch, kv heads, query group size, sink size, ragged lengths, dense or paged
 body and query / output dtypes.  All through the C ABI against the oracle, to the same bars as
 the fixed-case parity tests (gpu_util)."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -11,13 +13,17 @@ from hypothesis import HealthCheck, Phase, given, settings
 from hypothesis import strategies as st
 
 import oracle
-from gpu_util import check_output, compare_tiles, compare_tiles_compact, host_cache, q_to_host, tiles_to_host
+from gpu_util import (TIE_FRACTION, check_output, compare_tiles, compare_tiles_compact, host_cache, q_to_host,
+                      tiles_to_host)
 from tiles import STRUCTURES, make_tile
 
 pytestmark = pytest.mark.gpu
 
 SETTINGS = dict(derandomize=True, database=None, deadline=None, phases=[Phase.explicit, Phase.generate],
                 suppress_health_check=[HealthCheck.too_slow, HealthCheck.function_scoped_fixture])
+# KVARN_PROPERTY_SCALE multiplies every example count (a longer run of the same derandomized
+# search; the default keeps the GPU suite short)
+SCALE_EXAMPLES = max(1, int(os.environ.get("KVARN_PROPERTY_SCALE", "1")))
 SCALE = 1.0 / np.sqrt(128.0)
 
 
@@ -40,7 +46,7 @@ quant_cases = st.fixed_dictionaries(dict(
     bf16=st.booleans(), varn_iters=st.sampled_from([0, 1, 8])))
 
 
-@settings(max_examples=40, **SETTINGS)
+@settings(max_examples=40 * SCALE_EXAMPLES, **SETTINGS)
 @given(case=quant_cases)
 def test_gpu_quantize_property(K, case):
     _announce(case)
@@ -59,11 +65,19 @@ def test_gpu_quantize_property(K, case):
     torch.cuda.synchronize()
     tiles, gbest = out.cpu().numpy(), best.cpu().numpy()
     assert np.all((gbest >= 0) & (gbest <= c["varn_iters"]))
+    # Degenerate tiles (constant rows or columns, zeros, one outlier) tie systematically: clamped
+    # variances make Algorithm 1's imbalances of different iterations agree to fp32 resolution,
+    # and a group of equal values has one RTN quotient, so one rounding tie moves all its codes
+    # at once.  Each such tile or code is still held to the tie rules and the dequantization
+    # bound; only their number is not bounded by the statistical limits meant for real data.
+    degenerate = c["structure"] in ("constant_rows", "constant_cols", "zeros", "single_outlier")
     if c["aux"] == 0:
         compare_tiles(tiles, Xh, c["kind"], c["bits"], gbest,
-                      params=oracle.Params(bits=c["bits"], varn_iters=c["varn_iters"]))
+                      params=oracle.Params(bits=c["bits"], varn_iters=c["varn_iters"]),
+                      max_best_ties=n if degenerate else None, tie_fraction=0.05 if degenerate else TIE_FRACTION)
     else:
-        compare_tiles_compact(tiles, Xh, c["kind"], c["bits"], gbest, varn_iters=c["varn_iters"])
+        compare_tiles_compact(tiles, Xh, c["kind"], c["bits"], gbest, varn_iters=c["varn_iters"],
+                              max_ties=n if degenerate else None, tie_fraction=0.05 if degenerate else TIE_FRACTION)
 
 
 decode_cases = st.fixed_dictionaries(dict(
@@ -83,7 +97,7 @@ def _decode(K, p, cache, q, q_dt, out_dtype, max_len):
     return out
 
 
-@settings(max_examples=30, **SETTINGS)
+@settings(max_examples=30 * SCALE_EXAMPLES, **SETTINGS)
 @given(case=decode_cases)
 def test_gpu_decode_property(K, case):
     _announce(case)
@@ -133,7 +147,7 @@ append_cases = st.fixed_dictionaries(dict(
     lens=st.lists(st.integers(0, 2 * 128 + 60), min_size=1, max_size=3)))
 
 
-@settings(max_examples=15, **SETTINGS)
+@settings(max_examples=15 * SCALE_EXAMPLES, **SETTINGS)
 @given(case=append_cases)
 def test_gpu_append_property(K, case):
     """Prefilled prompts of random lengths, then `steps` appends (with the lock-step length hint
