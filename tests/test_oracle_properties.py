@@ -5,6 +5,8 @@ the rotation, and random cache layouts.  Each property follows from the definiti
 three cache regions and the stored aux) and softmax attention; the expected values are computed
 here from independent routines (scipy's Hadamard matrix, numpy's softmax, torch's E4M3 and
 numpy's binary16 conversions)."""
+import os
+
 import numpy as np
 import pytest
 import scipy.linalg
@@ -17,6 +19,8 @@ from tiles import STRUCTURES, make_tile
 
 H = scipy.linalg.hadamard(128).astype(np.float64) / np.sqrt(128.0)
 SETTINGS = dict(derandomize=True, database=None, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+# KVARN_PROPERTY_SCALE multiplies every example count (a longer run of the same search)
+SCALE_EXAMPLES = max(1, int(os.environ.get("KVARN_PROPERTY_SCALE", "1")))
 
 
 def e4m3_grid(v: np.ndarray) -> np.ndarray:
@@ -29,7 +33,7 @@ tile_cases = st.fixed_dictionaries(dict(
     varn_iters=st.sampled_from([0, 1, 2, 8]), rotate=st.sampled_from([0, 1]), aux=st.sampled_from([0, 1])))
 
 
-@settings(max_examples=150, **SETTINGS)
+@settings(max_examples=150 * SCALE_EXAMPLES, **SETTINGS)
 @given(case=tile_cases)
 def test_quantize_tile_properties(case):
     c = case
@@ -103,7 +107,7 @@ def test_quantize_tile_properties(case):
     assert np.allclose(Xd, expect, rtol=0, atol=1e-12 * max(np.abs(dq).max(), 1e-300))
 
 
-@settings(max_examples=40, **SETTINGS)
+@settings(max_examples=40 * SCALE_EXAMPLES, **SETTINGS)
 @given(bits=st.sampled_from([2, 4]), kind=st.sampled_from([0, 1]), aux=st.sampled_from([0, 1]),
        seed=st.integers(0, 2 ** 31 - 1))
 def test_pack_roundtrip_and_coverage(bits, kind, aux, seed):
@@ -147,7 +151,7 @@ cache_cases = st.fixed_dictionaries(dict(
     lens=st.lists(st.integers(0, 2 * 128 + 140), min_size=1, max_size=3)))
 
 
-@settings(max_examples=12, **SETTINGS)
+@settings(max_examples=12 * SCALE_EXAMPLES, **SETTINGS)
 @given(case=cache_cases)
 def test_prefill_equals_appends_property(case):
     """Writing whole prompts equals appending the same tokens one by one (App. D's regions)."""
@@ -204,7 +208,7 @@ def _stream(hc: oracle.HostCache, b: int, kh: int, which: str) -> np.ndarray:
     return np.concatenate(parts, axis=0)
 
 
-@settings(max_examples=25, **SETTINGS)
+@settings(max_examples=25 * SCALE_EXAMPLES, **SETTINGS)
 @given(case=decode_cases)
 def test_decode_is_attention_over_the_dequantized_stream(case):
     """Decode of query head h of sequence b is softmax attention over kv head h // g's stream
