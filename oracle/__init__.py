@@ -16,7 +16,11 @@ Parity status of each function (pins are in ``tests/test_oracle_*.py``):
   append           pinned (region bookkeeping against a direct re-quantization)
   e4m3 / fp16      pinned (all E4M3 values enumerated from the format definition, brute-force
                    nearest / upward rounding; numpy's binary16 conversion)
-  compact aux      pinned through the conversions, the round trip and the error bound
+  compact aux      pinned through the conversions, the round trip and the error bound; the
+                   tile-wide power-of-two shift between its two scales (a reading of App. D)
+                   through its minimality and the bound at large magnitudes
+  prefill          pinned (equals appending the same tokens one by one)
+  properties       random tiles, layouts and caches (``tests/test_oracle_properties.py``)
   c_min, c_max     parity unpinned: the paper does not give their values.
 """
 from __future__ import annotations
