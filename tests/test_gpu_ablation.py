@@ -55,11 +55,13 @@ def test_ablation_quantize(K, name):
 
 
 @pytest.mark.parametrize("name", ["KIVI", "VarN"])
-def test_ablation_decode(K, name):
-    """Decode over an unrotated cache: q and the output skip the rotation."""
+@pytest.mark.parametrize("n_q", [32, 40])
+def test_ablation_decode(K, name, n_q):
+    """Decode over an unrotated cache: q and the output skip the rotation (query groups of 4 and
+    of 5, which take different kernels)."""
     from paper_2606_03458_amd import workloads
     rotate, iters = VARIANTS[name]
-    built, _ = workloads.build("llama", context=20 * 128 + 77, batch=2, rotate=rotate, varn_iters=iters)
+    built, _ = workloads.build("llama", context=20 * 128 + 77, batch=2, rotate=rotate, varn_iters=iters, n_q=n_q)
     q = workloads.decode_queries(built, seed=12)
     p, cache = built.params, built.cache
     max_len = built.length + 1
