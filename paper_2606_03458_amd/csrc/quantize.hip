@@ -191,7 +191,8 @@ __device__ __forceinline__ float imbalance(float rmax, float rmin, const float (
     // all 128 channels live in one 16-lane row
     cmax = row16<OpMax>(cmax);
     cmin = row16<OpMin>(cmin);
-    return rmax / fmaxf(rmin, 1e-8f) + cmax / fmaxf(cmin, 1e-8f);
+    // (hardware reciprocal, ~1 ulp: Imb only ranks iterations, and values that close are ties)
+    return rmax * __builtin_amdgcn_rcpf(fmaxf(rmin, 1e-8f)) + cmax * __builtin_amdgcn_rcpf(fmaxf(cmin, 1e-8f));
 }
 
 __device__ __forceinline__ float clampf(float v, float lo, float hi) { return fminf(fmaxf(v, lo), hi); }
