@@ -15,8 +15,9 @@
  *
  * Every floating-point step runs in double precision.  Values that the format stores in
  * fp32 (the three auxiliary vectors) are rounded once, to nearest-even, when stored.  The
- * compact format (App. D "Effective memory overhead": two FP8 scales and one FP16 zero point
- * per group) rounds them to OCP E4M3 and IEEE binary16 instead, see kvo_quantize_tile.
+ * compact format of App. D ("Effective memory overhead": per group of 128 values, the two
+ * scales in an 8-bit float format and the zero point in a 16-bit one) rounds them to OCP E4M3
+ * and IEEE binary16 instead, see kvo_quantize_tile.
  *
  * Parity pins for each function live in tests/test_oracle_*.py.  The constants c_min and
  * c_max of Algorithm 1 are not given numerically by the paper (parity unpinned; 1e-8 and
@@ -72,7 +73,8 @@ uint16_t kvo_double_to_bf16(double x) {
 }
 
 /* ------------------------------------------------------------------------------------------
- * Narrow formats of the compact aux (App. D: "two FP8 scales ... and one FP16 zero-point").
+ * Narrow formats of the compact aux (App. D, "Effective memory overhead": 8-bit float scales,
+ * a 16-bit float zero point).
  *   E4M3 (the OCP 8-bit floating-point format E4M3): sign, 4 exponent bits with bias 7, 3
  *   mantissa bits.  Exponent field 0 holds the subnormals m * 2^-9; there are no infinities and
  *   the pattern with all exponent and mantissa bits set is NaN, so the largest finite value is
@@ -153,19 +155,25 @@ void kvo_hadamard128(double *x) {
 }
 
 /* ------------------------------------------------------------------------------------------
- * Algorithm 1 (App. H): VarN on one tile T with R rows and C columns, stored row-major.
- * Rows are tokens and columns are channels of the cache tile.
+ * VarN (Sec. 3.3, App. H, Algorithm 1) on one tile T of R rows and C columns, row-major; rows
+ * are the tile's tokens, columns its channels.
  *
- * Notation of Algorithm 1:
- *   Var_row(X): variance across the row index  -> one value per column (length C)
- *   Var_col(X): variance across the column index -> one value per row (length R)
- *   Imb(X) = max(v)/max(min(v), floor) summed over both variance vectors
- *   L_c (1 x C), L_r (R x 1): log-scales; Cur = (T ./ exp(L_c)) ./ exp(L_r)
- *   each iteration: column update from Var_row(Cur), then row update from Var_col(Cur),
- *   then keep the scales if Imb(Cur) <= I_best.
+ * The method looks for a row scale S_r and a column scale S_c such that the balanced tile
+ * T[r][c] / (S_c[c] S_r[r]) has lines of equal spread along both axes.  The scales are kept as
+ * logarithms L_c, L_r (zero at the start).  One iteration balances the columns and then the
+ * rows (the column scales come first, reading A1): a line's variance v in the current balanced
+ * tile is clamped to [c_min, c_max] and the line's log-scale moves by log(sqrt(v)), i.e. by half
+ * of log v, then is clamped to [log_lo, log_hi].  Dividing the line by sqrt(v) gives it unit
+ * variance, so without the clamps every line of the axis just balanced has variance exactly 1.
+ * After both axes the imbalance Imb of the current tile is measured (the ratio of the largest
+ * to the smallest line variance of each axis, summed over the two axes, the smallest floored
+ * at imb_floor), and the scales of the best state seen so far are kept; the start state counts
+ * as iteration 0 and a later iteration displaces an earlier one of equal Imb.
  * ------------------------------------------------------------------------------------------ */
 
-/* Two-pass (mean-centred) variance of n values spaced `stride` apart. */
+enum { AXIS_COLUMNS = 0, AXIS_ROWS = 1 };
+
+/* Two-pass (mean-centred) variance of n values spaced `stride` apart, divisor n - ddof. */
 static double variance(const double *v, int n, int stride, int ddof) {
     double mean = 0.0;
     for (int i = 0; i < n; ++i) mean += v[(size_t)i * stride];
@@ -178,93 +186,118 @@ static double variance(const double *v, int n, int stride, int ddof) {
     return ss / (double)(n - ddof);
 }
 
-static double clampd(double x, double lo, double hi) { return x < lo ? lo : (x > hi ? hi : x); }
-
-/* Cur = (T ./ exp(L_c)) ./ exp(L_r): two divisions, as written. */
-static void current_tile(const double *T, int R, int C, const double *Lc, const double *Lr, double *Cur) {
-    for (int r = 0; r < R; ++r)
-        for (int c = 0; c < C; ++c)
-            Cur[(size_t)r * C + c] = (T[(size_t)r * C + c] / exp(Lc[c])) / exp(Lr[r]);
+/* Variance of line i of the axis: column i taken over the R rows, or row i over the C columns. */
+static double line_variance(const double *X, int R, int C, int axis, int i, int ddof) {
+    return axis == AXIS_COLUMNS ? variance(X + i, R, C, ddof) : variance(X + (size_t)i * C, C, 1, ddof);
 }
 
-/* Imb(X) of Algorithm 1. */
+static double clampd(double x, double lo, double hi) { return x < lo ? lo : (x > hi ? hi : x); }
+
+/* Largest over smallest line variance of one axis (the smallest floored); 1 when balanced. */
+static double spread_ratio(const double *X, int R, int C, int axis, int ddof, double floor_) {
+    const int n = axis == AXIS_COLUMNS ? C : R;
+    double vmax = -INFINITY, vmin = INFINITY;
+    for (int i = 0; i < n; ++i) {
+        const double v = line_variance(X, R, C, axis, i, ddof);
+        vmax = fmax(vmax, v);
+        vmin = fmin(vmin, v);
+    }
+    return vmax / fmax(vmin, floor_);
+}
+
+/* Imb(X) of Algorithm 1: the spread ratio of the rows plus that of the columns. */
 double kvo_imbalance(const double *X, int R, int C, int ddof, double floor_) {
-    double vmax_r = -INFINITY, vmin_r = INFINITY, vmax_c = -INFINITY, vmin_c = INFINITY;
-    for (int r = 0; r < R; ++r) { /* variance along each row, over its C columns */
-        double v = variance(X + (size_t)r * C, C, 1, ddof);
-        vmax_r = fmax(vmax_r, v);
-        vmin_r = fmin(vmin_r, v);
+    return spread_ratio(X, R, C, AXIS_ROWS, ddof, floor_) + spread_ratio(X, R, C, AXIS_COLUMNS, ddof, floor_);
+}
+
+/* The tile and its current log-scales. */
+typedef struct {
+    const double *T;
+    int R, C;
+    double *Lc, *Lr; /* log-scale of every column and of every row */
+    double *Cur;     /* current balanced tile */
+} varn_state;
+
+/* Cur[r][c] = T[r][c] divided by e^{Lc[c]}, and the quotient divided by e^{Lr[r]}. */
+static void rebalance(varn_state *s) {
+    for (int r = 0; r < s->R; ++r)
+        for (int c = 0; c < s->C; ++c)
+            s->Cur[(size_t)r * s->C + c] = (s->T[(size_t)r * s->C + c] / exp(s->Lc[c])) / exp(s->Lr[r]);
+}
+
+/* One half-iteration: every line of the axis takes half the log of its clamped variance into
+ * its log-scale (clamped), measured on the tile before any of them moves; then Cur is redone. */
+static void balance_axis(varn_state *s, int axis, const kvo_params *p) {
+    const int n = axis == AXIS_COLUMNS ? s->C : s->R;
+    double *L = axis == AXIS_COLUMNS ? s->Lc : s->Lr;
+    for (int i = 0; i < n; ++i) {
+        const double v = clampd(line_variance(s->Cur, s->R, s->C, axis, i, p->ddof), p->c_min, p->c_max);
+        L[i] = clampd(L[i] + 0.5 * log(v), p->log_lo, p->log_hi);
     }
-    for (int c = 0; c < C; ++c) { /* variance along each column, over its R rows */
-        double v = variance(X + c, R, C, ddof);
-        vmax_c = fmax(vmax_c, v);
-        vmin_c = fmin(vmin_c, v);
-    }
-    return vmax_r / fmax(vmin_r, floor_) + vmax_c / fmax(vmin_c, floor_);
+    rebalance(s);
+}
+
+/* The scales of the best state so far: S_c*, S_r* (linear), its Imb and iteration. */
+typedef struct {
+    double *Sc, *Sr;
+    double I;
+    int k;
+} varn_best;
+
+/* Keep iteration k's scales if its imbalance I is no larger than the best so far (the later
+ * one wins a tie), or, with force_best >= 0, exactly when k is that iteration (test use). */
+static void keep_if_best(varn_best *b, const varn_state *s, double I, int k, const kvo_params *p) {
+    const int take = k == 0 || (p->force_best >= 0 ? k == p->force_best : I <= b->I);
+    if (!take) return;
+    b->I = I;
+    b->k = k;
+    for (int c = 0; c < s->C; ++c) b->Sc[c] = exp(s->Lc[c]);
+    for (int r = 0; r < s->R; ++r) b->Sr[r] = exp(s->Lr[r]);
 }
 
 /*
- * Run Algorithm 1 on one tile.
- *   T[R*C] (row-major) in; Sc[C], Sr[R] out (the best linear scales S_c*, S_r*);
- *   Bal[R*C] out (optional): (T ./ S_c*) ./ S_r*.
- * Optional histories, each indexed by iteration k = 0..K (k = 0 is the initial state):
+ * VarN on one tile.
+ *   T[R*C] (row-major) in; Sc[C], Sr[R] out: the kept scales S_c*, S_r*;
+ *   Bal[R*C] out (optional): T with column c divided by Sc[c], then row r by Sr[r].
+ * Optional histories, indexed by iteration k = 0..K (0 = the start state):
  *   imb_hist[K+1], Lc_hist[(K+1)*C], Lr_hist[(K+1)*R].
- * *best_iter (optional) receives the iteration whose scales were kept (0 = initial).
+ * *best_iter (optional) receives the iteration whose scales were kept.
  */
 void kvo_varn(const double *T, int R, int C, const kvo_params *p, double *Sc, double *Sr, double *Bal,
               double *imb_hist, double *Lc_hist, double *Lr_hist, int *best_iter) {
-    double *Lc = calloc((size_t)C, sizeof(double));
-    double *Lr = calloc((size_t)R, sizeof(double));
-    double *Cur = malloc((size_t)R * C * sizeof(double));
-    double *v = malloc((size_t)(R > C ? R : C) * sizeof(double));
-
-    current_tile(T, R, C, Lc, Lr, Cur);
-    double I_best = kvo_imbalance(Cur, R, C, p->ddof, p->imb_floor);
-    for (int c = 0; c < C; ++c) Sc[c] = exp(Lc[c]);
-    for (int r = 0; r < R; ++r) Sr[r] = exp(Lr[r]);
-    int best = 0;
-    if (imb_hist) imb_hist[0] = I_best;
-    if (Lc_hist) memcpy(Lc_hist, Lc, (size_t)C * sizeof(double));
-    if (Lr_hist) memcpy(Lr_hist, Lr, (size_t)R * sizeof(double));
-
-    for (int k = 1; k <= p->varn_iters; ++k) {
-        /* column scales from the variance of every column (taken across rows) */
-        for (int c = 0; c < C; ++c) v[c] = clampd(variance(Cur + c, R, C, p->ddof), p->c_min, p->c_max);
-        for (int c = 0; c < C; ++c) Lc[c] = clampd(Lc[c] + 0.5 * log(v[c]), p->log_lo, p->log_hi);
-        current_tile(T, R, C, Lc, Lr, Cur);
-        /* row scales from the variance of every row (taken across columns) */
-        for (int r = 0; r < R; ++r) v[r] = clampd(variance(Cur + (size_t)r * C, C, 1, p->ddof), p->c_min, p->c_max);
-        for (int r = 0; r < R; ++r) Lr[r] = clampd(Lr[r] + 0.5 * log(v[r]), p->log_lo, p->log_hi);
-        current_tile(T, R, C, Lc, Lr, Cur);
-
-        double I_curr = kvo_imbalance(Cur, R, C, p->ddof, p->imb_floor);
-        const int take = p->force_best >= 0 ? k == p->force_best : I_curr <= I_best;
-        if (take) { /* "<=": a later iteration wins a tie */
-            I_best = I_curr;
-            for (int c = 0; c < C; ++c) Sc[c] = exp(Lc[c]);
-            for (int r = 0; r < R; ++r) Sr[r] = exp(Lr[r]);
-            best = k;
+    varn_state s = {T, R, C, calloc((size_t)C, sizeof(double)), calloc((size_t)R, sizeof(double)),
+                    malloc((size_t)R * C * sizeof(double))};
+    varn_best best = {Sc, Sr, INFINITY, -1};
+    rebalance(&s);
+    for (int k = 0; k <= p->varn_iters; ++k) {
+        if (k > 0) {
+            balance_axis(&s, AXIS_COLUMNS, p);
+            balance_axis(&s, AXIS_ROWS, p);
         }
-        if (imb_hist) imb_hist[k] = I_curr;
-        if (Lc_hist) memcpy(Lc_hist + (size_t)k * C, Lc, (size_t)C * sizeof(double));
-        if (Lr_hist) memcpy(Lr_hist + (size_t)k * R, Lr, (size_t)R * sizeof(double));
+        const double I = kvo_imbalance(s.Cur, R, C, p->ddof, p->imb_floor);
+        keep_if_best(&best, &s, I, k, p);
+        if (imb_hist) imb_hist[k] = I;
+        if (Lc_hist) memcpy(Lc_hist + (size_t)k * C, s.Lc, (size_t)C * sizeof(double));
+        if (Lr_hist) memcpy(Lr_hist + (size_t)k * R, s.Lr, (size_t)R * sizeof(double));
     }
     if (Bal)
         for (int r = 0; r < R; ++r)
             for (int c = 0; c < C; ++c) Bal[(size_t)r * C + c] = (T[(size_t)r * C + c] / Sc[c]) / Sr[r];
-    if (best_iter) *best_iter = best;
-    free(Lc);
-    free(Lr);
-    free(Cur);
-    free(v);
+    if (best_iter) *best_iter = best.k;
+    free(s.Lc);
+    free(s.Lr);
+    free(s.Cur);
 }
 
 /* ------------------------------------------------------------------------------------------
  * Asymmetric round-to-nearest over one group of n values (Sec. 2.1, Eq. 1):
  *   mn = min, mx = max, s = (mx - mn) / (2^bits - 1)   (s := 1 when mx == mn)
  *   u = (x - mn) / s, code = clamp(round-half-even(u), 0, 2^bits - 1)
- * Eq. 1 writes the dequantized value as (code + z) * s with z = mn / s; the stored form here is
- * the equivalent code * s + mn.  u_out (optional) receives the unrounded quotients.
+ * The quotient u is evaluated as (2^bits - 1)(x - mn) / (mx - mn), the same real number with a
+ * single rounding at the end, so a value that lies exactly halfway between two levels gives an
+ * exact half-integer u and is rounded half to even.  Eq. 1 writes the dequantized value as
+ * (code + z) * s with z = mn / s; the stored form here is the equivalent code * s + mn.
+ * u_out (optional) receives the unrounded quotients.
  * ------------------------------------------------------------------------------------------ */
 void kvo_rtn_group(const double *x, int n, int stride, int bits, uint8_t *codes, int code_stride,
                    double *mn_out, double *s_out, double *u_out, int u_stride) {
@@ -274,10 +307,10 @@ void kvo_rtn_group(const double *x, int n, int stride, int bits, uint8_t *codes,
         mx = fmax(mx, x[(size_t)i * stride]);
     }
     const double qmax = (double)((1 << bits) - 1);
-    double s = (mx - mn) / qmax;
-    if (s == 0.0) s = 1.0;
+    const double range = mx - mn;
     for (int i = 0; i < n; ++i) {
-        double u = (x[(size_t)i * stride] - mn) / s;
+        const double d = x[(size_t)i * stride] - mn;
+        double u = range > 0.0 ? (qmax * d) / range : d; /* d = 0 for a constant group */
         double q = nearbyint(u); /* default rounding mode: to nearest, ties to even */
         if (q < 0.0) q = 0.0;
         if (q > qmax) q = qmax;
@@ -285,7 +318,7 @@ void kvo_rtn_group(const double *x, int n, int stride, int bits, uint8_t *codes,
         if (u_out) u_out[(size_t)i * u_stride] = u;
     }
     *mn_out = mn;
-    *s_out = s;
+    *s_out = range > 0.0 ? range / qmax : 1.0;
 }
 
 /* ------------------------------------------------------------------------------------------
@@ -783,17 +816,18 @@ void kvo_error_decomposition(const double *K, const double *Kdq, int32_t n, doub
  */
 int kvo_prefill(kvo_cache *cc, const void *k, const void *v, int dtype, const int32_t *cu, int32_t max_len,
                 const kvo_params *p) {
-    int ret = 0;
-    for (int32_t bi = 0; bi < cc->batch; ++bi) {
-        const int32_t L = cu[bi + 1] - cu[bi];
-        int32_t ns, nb, nr;
-        region_sizes(cc, L, &ns, &nb, &nr);
-        if (L < 0 || L > max_len || nb > cc->max_blocks) {
-            cc->seq_len[bi] = 0;
-            ret = -3;
-            continue;
-        }
+    int too_long = 0, bad_id = 0;
+    /* (sequence, kv head) streams are independent; OpenMP spreads them over the host's threads */
+#pragma omp parallel for collapse(2) schedule(dynamic) reduction(|| : too_long, bad_id)
+    for (int32_t bi = 0; bi < cc->batch; ++bi)
         for (int32_t kh = 0; kh < cc->n_kv; ++kh) {
+            const int32_t L = cu[bi + 1] - cu[bi];
+            int32_t ns, nb, nr;
+            region_sizes(cc, L, &ns, &nb, &nr);
+            if (L < 0 || L > max_len || nb > cc->max_blocks) {
+                too_long = 1;
+                continue;
+            }
             const size_t stream = (size_t)bi * cc->n_kv + kh;
             for (int32_t t = 0; t < ns + nr; ++t) { /* sink rows, then residual rows */
                 const int32_t row = t < ns ? t : L - nr + (t - ns);
@@ -808,15 +842,22 @@ int kvo_prefill(kvo_cache *cc, const void *k, const void *v, int dtype, const in
             const size_t esz = dtype == 0 ? 4 : 2;
             for (int32_t blk = 0; blk < nb; ++blk) {
                 uint8_t *kt = body_tile(cc, cc->k_body, bi, kh, blk), *vt = body_tile(cc, cc->v_body, bi, kh, blk);
-                if (!kt || !vt) return -4;
+                if (!kt || !vt) {
+                    bad_id = 1;
+                    continue;
+                }
                 const size_t at = ((size_t)(cu[bi] + ns + blk * G) * cc->n_kv + kh) * D;
                 kvo_quantize_pack((const uint8_t *)k + at * esz, dtype, (int64_t)cc->n_kv * D, KVO_KEYS, p, kt);
                 kvo_quantize_pack((const uint8_t *)v + at * esz, dtype, (int64_t)cc->n_kv * D, KVO_VALUES, p, vt);
             }
         }
-        cc->seq_len[bi] = L;
+    for (int32_t bi = 0; bi < cc->batch; ++bi) {
+        const int32_t L = cu[bi + 1] - cu[bi];
+        int32_t ns, nb, nr;
+        region_sizes(cc, L, &ns, &nb, &nr);
+        cc->seq_len[bi] = (L < 0 || L > max_len || nb > cc->max_blocks) ? 0 : L;
     }
-    return ret;
+    return bad_id ? -4 : (too_long ? -3 : 0);
 }
 
 /* Thread count of the parallel loops over tiles and streams (timing only; results do not

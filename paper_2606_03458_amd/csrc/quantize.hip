@@ -6,6 +6,8 @@
 // tr = 4*wave + lane / 16.  Row (per-token) reductions stay inside a 16-lane row; column
 // (per-channel) reductions cross the four 16-lane groups of a wave and then the four waves
 // through LDS, in a fixed order so that every thread sees bit-identical results.
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace kvarn {
@@ -507,30 +509,46 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         }
         inv_s[m] = 1.0f / s[m];
     }
-    // codes -> LDS (keys [t][c], values [c][t]), 8 bytes per thread per token / channel
-    if (kind == KVARN_KEYS) {
+    // codes -> LDS (keys [t][c], values [c][t]), 8 bytes per thread per token / channel.
+    // Unrotated and unbalanced tiles (the KIVI-style ablation) hold the inputs themselves, and a
+    // bf16 value can lie exactly halfway between two levels; there the quotient is formed as
+    // qmax (x - mn) / (mx - mn) with one correctly rounded division, which keeps such a value an
+    // exact half-integer, rounded half to even.  Elsewhere the reciprocal step is used.
+    auto write_codes = [&](auto exact) {
+        constexpr bool kExact = decltype(exact)::value;
+        float den[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            uint32_t lo = 0, hi = 0;
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - off[j]) * inv_s[j]), 0.f, qmax);
-                if (j < 4) lo |= q << (8 * j); else hi |= q << (8 * (j - 4));
-            }
-            *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tr + i) * kD + 8 * L.tc]) = make_uint2(lo, hi);
-        }
-    } else {
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            uint32_t lo = 0, hi = 0;
+        for (int m = 0; m < 8; ++m) den[m] = mx[m] > mn[m] ? mx[m] - mn[m] : 1.f;
+        auto code = [&](float v, int m) -> uint32_t {
+            const float u = kExact ? ((v - off[m]) * qmax) / den[m] : (v - off[m]) * inv_s[m];
+            return (uint32_t)clampf(rintf(u), 0.f, qmax);
+        };
+        if (kind == KVARN_KEYS) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const uint32_t q = (uint32_t)clampf(rintf((x[i][j] - off[i]) * inv_s[i]), 0.f, qmax);
-                if (i < 4) lo |= q << (8 * i); else hi |= q << (8 * (i - 4));
+                uint32_t lo = 0, hi = 0;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const uint32_t q = code(x[i][j], j);
+                    if (j < 4) lo |= q << (8 * j); else hi |= q << (8 * (j - 4));
+                }
+                *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tr + i) * kD + 8 * L.tc]) = make_uint2(lo, hi);
             }
-            *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tc + j) * kG + 8 * L.tr]) = make_uint2(lo, hi);
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                uint32_t lo = 0, hi = 0;
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    const uint32_t q = code(x[i][j], i);
+                    if (i < 4) lo |= q << (8 * i); else hi |= q << (8 * (i - 4));
+                }
+                *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tc + j) * kG + 8 * L.tr]) = make_uint2(lo, hi);
+            }
         }
-    }
+    };
+    if (!COMPACT && P.iters == 0 && !P.rotate) write_codes(std::true_type{});
+    else write_codes(std::false_type{});
 
     // ---- a7: aux (absorbed scales) --------------------------------------------------------
     float* aux = reinterpret_cast<float*>(dst + code_bytes(P.bits));

@@ -79,9 +79,12 @@ def reference(st: dict):
     return xs, outs
 
 
-def run(st: dict, ref, quantizer: str, bits: int = 2) -> dict:
+def run(st: dict, ref, quantizer: str, bits: int = 2, keep_outputs: bool = False):
     """Relative error ||o - o_ref|| / ||o_ref|| of every layer's attention output, per token,
-    averaged over the batch: {"static": [layers, T], "dynamic": [layers, T]} (fp32, device)."""
+    averaged over the batch: {"static": [layers, T], "dynamic": [layers, T]} (fp32, device).
+    With keep_outputs, also returns the attention outputs themselves,
+    {"static" | "dynamic": [layers, T, B, n_q, 128]} (fp32, host), and the caches
+    {"static" | "dynamic": [one kvarn.Cache per layer]}."""
     xs, o_ref = ref
     x0, nq, nkv, D, layers = st["x0"], st["n_q"], st["n_kv"], 128, st["layers"]
     B, T, _ = x0.shape
@@ -89,6 +92,7 @@ def run(st: dict, ref, quantizer: str, bits: int = 2) -> dict:
     p = K.kvarn_params_init(bits, **QUANTIZERS[quantizer])
     caches = {m: [K.Cache(p, B, nkv, T // 128 + 1, device=dev) for _ in range(layers)] for m in ("static", "dynamic")}
     err = {m: torch.zeros((layers, T), device=dev) for m in caches}
+    outs = {m: torch.zeros((layers, T, B, nq, D)) for m in caches} if keep_outputs else None
     ws_bytes = K.kvarn_decode_workspace_bytes(p, caches["static"][0], nq, T)
     ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device=dev)
     out = torch.empty((B, nq, D), dtype=torch.float32, device=dev)
@@ -107,10 +111,12 @@ def run(st: dict, ref, quantizer: str, bits: int = 2) -> dict:
                 K.kvarn_decode_attention(p, c, nq, qt, K.KVARN_F32, out, K.KVARN_F32, scale, T, ws, ws_bytes)
                 r = o_ref[l][:, t]
                 err[m][l, t] = ((out - r).norm(dim=(1, 2)) / r.norm(dim=(1, 2))).mean()
+                if keep_outputs:
+                    outs[m][l, t] = out.cpu()
                 if m == "dynamic":
                     xd = xd + out.reshape(B, nq * D) @ st["WO"][l]
     for m in caches:
         for c in caches[m]:
             if int(c.err_word.item()) != 0:
                 raise RuntimeError(f"cache error word {int(c.err_word.item())}")
-    return err
+    return (err, outs, caches) if keep_outputs else err

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import check_output, compare_tiles_compact, host_cache, q_to_host, tiles_to_host
+from gpu_util import check_end_to_end, check_output, compare_tiles_compact, host_cache, q_to_host, tiles_to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -122,3 +122,5 @@ def test_compact_append_stream(K):
     K.kvarn_decode_attention(p, cache, 4 * H, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE, steps + 1, ws, ws_bytes)
     torch.cuda.synchronize()
     check_output(out.cpu().numpy(), oracle.decode(gc, q_to_host(q), SCALE), bf16_out=False)
+    raw = lambda b, h, blk, kind: oracle.bf16_bits_to_f64(toks[kind][blk * 128:(blk + 1) * 128, b, h])
+    check_end_to_end(out.cpu().numpy(), hc, gc, raw, q_to_host(q), False, SCALE)  # end to end

@@ -5,7 +5,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import (check_output, compare_tiles, host_cache, q_to_host, tiles_to_host)
+from gpu_util import (check_end_to_end, check_output, compare_tiles, host_cache, oracle_cache_from_inputs,
+                      q_to_host, tiles_to_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -123,12 +124,21 @@ def _ref(built, q):
     return oracle.decode(host_cache(built.cache), q_to_host(q), SCALE)
 
 
+def _raw_tile(inputs):
+    """Raw tokens of body tile blk of (sequence b, kv head kh) of a one-layer workload."""
+    return lambda b, kh, blk, kind: tiles_to_host((inputs["K"], inputs["V"])[kind][0][b, kh, blk * 128:(blk + 1) * 128])
+
+
 def test_decode_tiny(K):
+    """Tiny workload: decode over the GPU's cache, and end to end against the oracle's own cache
+    of the same fp32 K/V (its own quantization of both tiles of K and of V)."""
     from paper_2606_03458_amd import workloads
-    built, _ = workloads.build("tiny")
+    built, inputs = workloads.build("tiny", keep_inputs=True)
     q = workloads.decode_queries(built, seed=0)
     out = _decode(K, built, q)
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+    hc = oracle_cache_from_inputs(built, inputs)
+    check_end_to_end(out.cpu().numpy(), hc, host_cache(built.cache), _raw_tile(inputs), q_to_host(q), False, SCALE)
 
 
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
@@ -136,14 +146,19 @@ def test_decode_llama_layer(K, out_dtype):
     """Llama-3-8B-shaped layer: 32 q / 8 kv heads, 8192-token prefill, then one appended
     token (residual = 1), bf16 q."""
     from paper_2606_03458_amd import workloads
-    built, _ = workloads.build("llama")
+    built, inputs = workloads.build("llama", keep_inputs=True)
     kt, vt = workloads.step_tokens(built, seed=1, step=0)
     K.kvarn_append_token(built.params, built.cache, kt, vt, K.KVARN_BF16, built.length)
     built.length += 1
     q = workloads.decode_queries(built, seed=1)
     out = _decode(K, built, q, out_dtype)
     assert int(built.cache.seq_len[0]) == 8193
-    check_output(out.float().cpu().numpy(), _ref(built, q), bf16_out=out_dtype == torch.bfloat16)
+    got = out.float().cpu().numpy()
+    check_output(got, _ref(built, q), bf16_out=out_dtype == torch.bfloat16)
+    # end to end, all 8 kv-head streams: the oracle's own cache of the same K/V and token
+    hc = oracle_cache_from_inputs(built, inputs, appended=[(kt, vt)])
+    check_end_to_end(got, hc, host_cache(built.cache), _raw_tile(inputs), q_to_host(q),
+                     out_dtype == torch.bfloat16, SCALE)
 
 
 @pytest.mark.parametrize("bits,n_sink,name", [(2, 128, "llama"), (4, 0, "llama"), (2, 0, "stress"),
@@ -250,11 +265,16 @@ def test_append_stream(K, bits, n_sink, hint):
                     compare_tiles(body[b, h, blk][None], X[None], kind, bits)
     assert not gc.k_body[:, :, 2].any() and not gc.v_body[:, :, 2].any()
     assert int(cache.err_word[0]) == 0
-    # the oracle's own flushes agree with the GPU's codes up to ties as well
-    for kind, gb, ob in ((0, gc.k_body, hc.k_body), (1, gc.v_body, hc.v_body)):
-        g_codes = oracle.unpack_tile(gb[0, 0, 0], kind, bits)[0]
-        o_codes = oracle.unpack_tile(ob[0, 0, 0], kind, bits)[0]
-        assert (g_codes != o_codes).mean() <= 1e-3
+    # decode over the GPU's cache, and end to end over the oracle's own (its own flushes)
+    q = torch.randn((B, 4 * H, 128), generator=g, device="cuda").to(torch.bfloat16)
+    ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, 4 * H, steps + 1)
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+    K.kvarn_decode_attention(p, cache, 4 * H, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE, steps + 1, ws, ws_bytes)
+    torch.cuda.synchronize()
+    check_output(out.cpu().numpy(), oracle.decode(gc, q_to_host(q), SCALE), bf16_out=False)
+    raw = lambda b, h, blk, kind: oracle.bf16_bits_to_f64(toks[kind][n_sink + blk * 128:n_sink + (blk + 1) * 128, b, h])
+    check_end_to_end(out.cpu().numpy(), hc, gc, raw, q_to_host(q), False, SCALE)
 
 
 def test_append_overflow_flag(K):

@@ -5,7 +5,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_util import check_output, compare_tiles, host_cache, q_to_host
+from gpu_util import check_end_to_end, check_output, compare_tiles, host_cache, q_to_host
 
 pytestmark = pytest.mark.gpu
 
@@ -78,6 +78,14 @@ def test_prefill_matches_oracle(K, bits, n_sink, dtype):
     q = torch.randn((B, 4 * H, 128), device="cuda").to(torch.bfloat16)
     out = _decode(K, p, cache, q, max(lens) + 1)
     check_output(out.cpu().numpy(), oracle.decode(gc, q_to_host(q), SCALE), bf16_out=False)
+    # end to end: the oracle's own prefill of the same prompts
+
+    def raw(b, h, blk, kind):
+        r0 = cun[b] + n_sink + blk * 128
+        X = (kk, vv)[kind][r0:r0 + 128, h]
+        return X.astype(np.float64) if dtype == torch.float32 else oracle.bf16_bits_to_f64(X)
+
+    check_end_to_end(out.cpu().numpy(), hc, gc, raw, q_to_host(q), False, SCALE)
 
 
 def test_paged_equals_dense(K):
