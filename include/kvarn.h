@@ -36,8 +36,8 @@
  *     512 bytes   s2[128] fp32   second scale: keys per token, values per channel (the other
  *                                Sinkhorn scale)
  *     Tile size 5632 bytes at 2 bits (2.75 bits/element), 9728 at 4 bits.
- *   KVARN_AUX_COMPACT (App. D, "Effective memory overhead": two FP8 scales and one FP16 zero
- *   point per group of 128 elements):
+ *   KVARN_AUX_COMPACT (App. D, "Effective memory overhead": per group of 128 values, both
+ *   scales in an 8-bit float format and the zero point in a 16-bit one):
  *     256 bytes   b[128]  IEEE binary16, little-endian
  *     128 bytes   a[128]  OCP E4M3 (4-bit exponent, bias 7, 3-bit mantissa, largest 448)
  *     128 bytes   s2[128] OCP E4M3

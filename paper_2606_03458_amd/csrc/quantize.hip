@@ -241,7 +241,7 @@ __device__ __forceinline__ float pick_col(const float (&v)[8], int q) {
     return __uint_as_float(__builtin_amdgcn_permlane32_swap(__float_as_uint(lo), __float_as_uint(hi), false, false)[0]);
 }
 
-// ---- narrow formats of the compact aux (App. D: two FP8 scales and one FP16 zero point) -----
+// ---- narrow formats of the compact aux (App. D: 8-bit float scales, 16-bit float offset) ----
 // OCP E4M3: 4-bit exponent with bias 7, 3-bit mantissa, subnormals m * 2^-9, largest 448.
 // Grid value of x > 0 on the E4M3 grid of its binade (spacing 2^(e-3), 2^-9 below 2^-6),
 // nearest with ties to even or upward, saturating at 448.  Scaling by powers of two is exact.

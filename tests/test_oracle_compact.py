@@ -1,8 +1,9 @@
-"""Pins of the compact aux format (App. D "Effective memory overhead": two FP8 scales and one
-FP16 zero point per group of 128 elements): the narrow-format conversions against independent
-library implementations (torch's float8_e4m3fn for OCP E4M3, numpy's float16 for binary16),
-brute force over the E4M3 value set, the code choice given the stored aux, the stated error
-bound, the packed round trip and the paper's printed 2.25 bits/element."""
+"""Pins of the compact aux format (App. D "Effective memory overhead": per group of 128 values,
+both scales in an 8-bit float format and the zero point in a 16-bit one): the narrow-format
+conversions against independent library implementations (torch's float8_e4m3fn for OCP E4M3,
+numpy's float16 for binary16), brute force over the E4M3 value set, the code choice given the
+stored aux, the stated error bound, the packed round trip and the paper's printed 2.25
+bits/element."""
 import os
 
 import numpy as np
