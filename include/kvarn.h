@@ -17,7 +17,9 @@
  *
  * Conventions for every entry point:
  *   - All pointers to tensors are DEVICE pointers, owned by the caller, and must stay valid
- *     until the work queued on `stream` has run.  The library allocates no device memory.
+ *     until the work queued on `stream` has run.  The library allocates no device memory at
+ *     run time; its code object holds one static scratch array per device, used only by
+ *     kvarn_decode_attention_noalloc.
  *   - Every call only enqueues work on `stream` (asynchronous); none synchronizes.
  *   - Arguments are validated on the host before anything is enqueued.  A failed check
  *     returns a negative kvarn_status and enqueues nothing.  KVARN_EHIP reports a failed
@@ -229,6 +231,25 @@ KVARN_API size_t kvarn_decode_workspace_bytes(const kvarn_params *p, const kvarn
 KVARN_API int kvarn_decode_attention(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q, const void *q,
                            int32_t q_dtype, void *out, int32_t out_dtype, float sm_scale, int32_t max_len_hint,
                            void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * Decode attention that allocates nothing, for callers that cannot allocate device memory:
+ * code under HIP graph capture, tight serving loops, harnesses that forbid allocation.
+ * Arguments and results are those of kvarn_decode_attention without the workspace: the split
+ * partials go to a scratch array of KVARN_NOALLOC_SCRATCH_BYTES (32 MiB) that the library
+ * holds in static device memory, one array per device, kept until the process ends.  Its
+ * device address is looked up once per device (hipGetSymbolAddress, on the first call with
+ * that device current, guarded by a mutex); no call allocates or frees anything.
+ *   - Plans whose partials need more than KVARN_NOALLOC_SCRATCH_BYTES (as
+ *     kvarn_decode_workspace_bytes reports) return KVARN_EWORKSPACE and enqueue nothing.
+ *   - Every call on one device shares that device's array: calls that may overlap on one
+ *     device (other streams, other host threads) race on it and must be ordered by the
+ *     caller.  The array keeps the last call's partials; no call relies on its contents.
+ */
+#define KVARN_NOALLOC_SCRATCH_BYTES (32u << 20)
+KVARN_API int kvarn_decode_attention_noalloc(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q,
+                                             const void *q, int32_t q_dtype, void *out, int32_t out_dtype,
+                                             float sm_scale, int32_t max_len_hint, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -2,12 +2,40 @@
 // planning and kernel launches.  No device memory is allocated here.
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "common.hpp"
 
 using namespace kvarn;
 
+// Split partials of kvarn_decode_attention_noalloc: one array per device, held until the
+// process ends.  In host code `scratch` only names the symbol; its device address on the
+// current device comes from hipGetSymbolAddress (scratch_ptr below) and is the only form
+// passed to kernels.
+static __device__ __align__(256) uint8_t scratch[KVARN_NOALLOC_SCRATCH_BYTES];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, looked up once per device.
+hipError_t scratch_ptr(void** out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* ptr = nullptr;
+        e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        g_scratch[dev] = ptr;
+    }
+    *out = g_scratch[dev];
+    return hipSuccess;
+}
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
@@ -158,9 +186,15 @@ size_t kvarn_decode_workspace_bytes(const kvarn_params* p, const kvarn_cache* ca
     return decode_workspace_bytes(cache->batch, n_q, plan);
 }
 
-int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q,
-                           int32_t q_dtype, void* out, int32_t out_dtype, float sm_scale, int32_t max_len_hint,
-                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation, planning and launch shared by both decode entry points.  ws == nullptr with
+// use_scratch: the partials go to the library's per-device scratch array.
+int decode_impl(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q, int32_t q_dtype,
+                void* out, int32_t out_dtype, float sm_scale, int32_t max_len_hint, void* workspace,
+                size_t workspace_bytes, bool use_scratch, hipStream_t stream) {
     int st = check_params(p);
     if (st) return st;
     st = check_cache(p, cache);
@@ -171,11 +205,34 @@ int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int3
     if (!aligned(q, 4) || !aligned(out, 8)) return KVARN_EINVAL;
     const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
     const size_t need = decode_workspace_bytes(cache->batch, n_q, plan);
-    if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) return KVARN_EWORKSPACE;
+    if (use_scratch) {
+        if (need > KVARN_NOALLOC_SCRATCH_BYTES) return KVARN_EWORKSPACE;
+        workspace = nullptr;
+        if (need > 0 && scratch_ptr(&workspace) != hipSuccess) return KVARN_EHIP;
+    } else if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) {
+        return KVARN_EWORKSPACE;
+    }
     hipError_t e = launch_decode(*cache, p->bits, p->aux_format == KVARN_AUX_COMPACT, p->rotate, p->n_sink, n_q, q,
                                  q_dtype == KVARN_BF16, out, out_dtype == KVARN_BF16, sm_scale, plan,
                                  static_cast<float*>(workspace), stream);
     return e == hipSuccess ? KVARN_OK : KVARN_EHIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvarn_decode_attention(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q,
+                           int32_t q_dtype, void* out, int32_t out_dtype, float sm_scale, int32_t max_len_hint,
+                           void* workspace, size_t workspace_bytes, hipStream_t stream) {
+    return decode_impl(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, max_len_hint, workspace, workspace_bytes,
+                       false, stream);
+}
+
+int kvarn_decode_attention_noalloc(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q,
+                                   int32_t q_dtype, void* out, int32_t out_dtype, float sm_scale,
+                                   int32_t max_len_hint, hipStream_t stream) {
+    return decode_impl(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, max_len_hint, nullptr, 0, true, stream);
 }
 
 }  // extern "C"

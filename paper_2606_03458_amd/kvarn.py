@@ -19,7 +19,9 @@ KVARN_AUX_F32, KVARN_AUX_COMPACT = 0, 1
 STATUS = {0: "KVARN_OK", -1: "KVARN_EINVAL", -2: "KVARN_EUNSUPPORTED", -3: "KVARN_ECAPACITY", -4: "KVARN_EHIP",
           -5: "KVARN_EWORKSPACE"}
 EXPORTS = ("kvarn_params_init", "kvarn_tile_bytes", "kvarn_cache_sizes", "kvarn_quantize_block", "kvarn_prefill",
-           "kvarn_append_token", "kvarn_decode_workspace_bytes", "kvarn_decode_attention")
+           "kvarn_append_token", "kvarn_decode_workspace_bytes", "kvarn_decode_attention",
+           "kvarn_decode_attention_noalloc")
+NOALLOC_SCRATCH_BYTES = 32 << 20  # KVARN_NOALLOC_SCRATCH_BYTES
 
 
 class KVarNError(RuntimeError):
@@ -75,6 +77,8 @@ def lib():
         L.kvarn_decode_workspace_bytes.restype = sz
         L.kvarn_decode_attention.argtypes = [P, C, i32, vp, i32, vp, i32, ctypes.c_float, i32, vp, sz, vp]
         L.kvarn_decode_attention.restype = ctypes.c_int
+        L.kvarn_decode_attention_noalloc.argtypes = [P, C, i32, vp, i32, vp, i32, ctypes.c_float, i32, vp]
+        L.kvarn_decode_attention_noalloc.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -164,6 +168,14 @@ def kvarn_decode_attention(p: kvarn_params, cache: "Cache", n_q: int, q, q_dtype
     st = lib().kvarn_decode_attention(ctypes.byref(p), ctypes.byref(d), n_q, _ptr(q), q_dtype, _ptr(out), out_dtype,
                                       sm_scale, max_len_hint, _ptr(workspace), workspace_bytes, _stream(stream))
     _check("kvarn_decode_attention", st)
+
+
+def kvarn_decode_attention_noalloc(p: kvarn_params, cache: "Cache", n_q: int, q, q_dtype: int, out, out_dtype: int,
+                                   sm_scale: float, max_len_hint: int, stream=None) -> None:
+    d = cache.desc()
+    st = lib().kvarn_decode_attention_noalloc(ctypes.byref(p), ctypes.byref(d), n_q, _ptr(q), q_dtype, _ptr(out),
+                                              out_dtype, sm_scale, max_len_hint, _stream(stream))
+    _check("kvarn_decode_attention_noalloc", st)
 
 
 # ------------------------------------------------------------------------------------------

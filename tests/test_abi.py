@@ -28,6 +28,9 @@ def test_exports_every_declared_symbol(K):
     L = ctypes.CDLL(K.library_path())
     for n in names:
         assert hasattr(L, n), n
+    text = open(os.path.join(ROOT, "include", "kvarn.h")).read()
+    m = re.search(r"#define KVARN_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == K.NOALLOC_SCRATCH_BYTES
 
 
 def test_params_and_sizes(K):
@@ -160,6 +163,27 @@ def test_decode_validation(K):
     # the workspace grows with the split plan and the number of query heads
     assert K.kvarn_decode_workspace_bytes(p, c, 16, 4096) == 2 * need
     assert K.kvarn_decode_workspace_bytes(p, c, 8, -1) == 0
+
+
+def test_decode_noalloc_validation(K):
+    """The allocation-free decode validates like kvarn_decode_attention, and rejects a plan whose
+    split partials exceed its scratch array, all before any HIP call."""
+    p = K.kvarn_params_init(2)
+    c = _HostCache(K, batch=2, n_kv=2, max_blocks=32)
+    keep, buf = _fake(1 << 20)
+    good = dict(n_q=8, q=buf, q_dtype=1, out=buf, out_dtype=1, sm_scale=0.088, max_len_hint=4096)
+    for kw, code in [(dict(n_q=7), -1), (dict(q=None), -1), (dict(out=buf + 2), -1), (dict(q_dtype=9), -1),
+                     (dict(sm_scale=float("nan")), -1), (dict(max_len_hint=-1), -1)]:
+        with pytest.raises(K.KVarNError) as e:
+            K.kvarn_decode_attention_noalloc(p, c, **{**good, **kw}, stream=0)
+        assert e.value.status == code, kw
+    # 1023 streams of 16 query heads over 2048 tiles: the largest split plan, 32.5 MiB of partials
+    big = _HostCache(K, batch=1023, n_kv=1, max_blocks=2049)
+    need = K.kvarn_decode_workspace_bytes(p, big, 16, 2048 * 128)
+    assert need > K.NOALLOC_SCRATCH_BYTES
+    with pytest.raises(K.KVarNError) as e:
+        K.kvarn_decode_attention_noalloc(p, big, **{**good, "n_q": 16, "max_len_hint": 2048 * 128}, stream=0)
+    assert e.value.status == -5
 
 
 def test_no_cpu_fallback(K, monkeypatch, tmp_path):
