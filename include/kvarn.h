@@ -202,7 +202,8 @@ KVARN_API int kvarn_prefill(const kvarn_params *p, const kvarn_cache *cache, con
  *   host_len_before  the common length of all sequences before this call (lock-step decode),
  *           used to check capacity on the host and to launch the flush only when one is due;
  *           pass -1 if lengths differ or are unknown: the flush kernel then runs every call
- *           and each sequence decides on the device, and overflow is caught by err_word only.
+ *           on a grid of resident size (768 workgroups) whose workgroups check the tiles in
+ *           turn, each sequence deciding on the device, and overflow is caught by err_word only.
  * Returns KVARN_ECAPACITY (enqueuing nothing) if the hint shows that a flush would need body
  * tile max_blocks.
  */

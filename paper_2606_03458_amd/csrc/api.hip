@@ -159,7 +159,7 @@ int kvarn_append_token(const kvarn_params* p, const kvarn_cache* cache, const vo
     hipError_t e = launch_append(*cache, p->n_sink, k_new, v_new, dtype == KVARN_BF16, stream);
     if (e != hipSuccess) return KVARN_EHIP;
     if (flush) {
-        e = launch_flush(qparams(p), *cache, p->n_sink, stream);
+        e = launch_flush(qparams(p), *cache, p->n_sink, host_len_before >= 0, stream);
         if (e != hipSuccess) return KVARN_EHIP;
     }
     return KVARN_OK;

@@ -44,7 +44,9 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
                                  int64_t n_inner, int64_t x_outer, int64_t x_inner, int64_t x_token, void* out,
                                  int64_t out_outer, int64_t out_inner, int32_t* best_iter, hipStream_t stream);
 
-hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream);
+// all_due: the caller knows every sequence completes a group with this token (lock-step
+// decode): one workgroup per tile.  Otherwise a resident-size grid checks the tiles.
+hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, bool all_due, hipStream_t stream);
 
 hipError_t launch_prefill(const QParams& qp, const kvarn_cache& c, int n_sink, const void* k, const void* v,
                           bool x_bf16, const int32_t* cu_seqlens, int max_len, hipStream_t stream);

@@ -268,7 +268,7 @@ __device__ __forceinline__ float fp16_round(float x, uint32_t& bits) {
 
 // Quantize one tile.  src: token t at src + t*tstride elements, channels contiguous (16-byte
 // aligned rows).  dst: the packed tile (16-byte aligned).
-template <bool COMPACT>
+template <bool COMPACT, bool EXACT>
 __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int kind, const QParams& P, uint8_t* dst,
                               int32_t* best_out, QuantSmem& sm) {
     const Lane L;
@@ -510,10 +510,11 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         inv_s[m] = 1.0f / s[m];
     }
     // codes -> LDS (keys [t][c], values [c][t]), 8 bytes per thread per token / channel.
-    // Unrotated and unbalanced tiles (the KIVI-style ablation) hold the inputs themselves, and a
-    // bf16 value can lie exactly halfway between two levels; there the quotient is formed as
-    // qmax (x - mn) / (mx - mn) with one correctly rounded division, which keeps such a value an
-    // exact half-integer, rounded half to even.  Elsewhere the reciprocal step is used.
+    // EXACT (unrotated and unbalanced tiles, the KIVI-style ablation, fp32 aux): the tile holds
+    // the inputs themselves and a bf16 value can lie exactly halfway between two levels; the
+    // quotient is then formed as qmax (x - mn) / (mx - mn) with one correctly rounded division,
+    // which keeps such a value an exact half-integer, rounded half to even.  Otherwise the
+    // reciprocal step is used.
     auto write_codes = [&](auto exact) {
         constexpr bool kExact = decltype(exact)::value;
         float den[8];
@@ -547,8 +548,7 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
             }
         }
     };
-    if (!COMPACT && P.iters == 0 && !P.rotate) write_codes(std::true_type{});
-    else write_codes(std::false_type{});
+    write_codes(std::integral_constant<bool, EXACT>{});
 
     // ---- a7: aux (absorbed scales) --------------------------------------------------------
     float* aux = reinterpret_cast<float*>(dst + code_bytes(P.bits));
@@ -681,7 +681,7 @@ struct TileArgs {
     int32_t* best_iter;
 };
 
-template <bool COMPACT>
+template <bool COMPACT, bool EXACT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_quantize_tiles(TileArgs a) {
     __shared__ QuantSmem sm;
     const int64_t tile = a.tile0 + blockIdx.x;
@@ -689,7 +689,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
     const size_t esz = a.x_bf16 ? 2 : 4;
     const char* src = static_cast<const char*>(a.x) + (size_t)(i * a.x_outer + j * a.x_inner) * esz;
     uint8_t* dst = a.out + (size_t)(i * a.out_outer + j * a.out_inner) * tile_bytes(a.P.bits, COMPACT);
-    quantize_tile<COMPACT>(src, a.x_bf16 != 0, a.x_token, a.kind, a.P, dst, a.best_iter ? a.best_iter + tile : nullptr,
+    quantize_tile<COMPACT, EXACT>(src, a.x_bf16 != 0, a.x_token, a.kind, a.P, dst, a.best_iter ? a.best_iter + tile : nullptr,
                            sm);
 }
 
@@ -699,24 +699,57 @@ struct FlushArgs {
     int n_sink;
 };
 
-// One workgroup per (sequence, kv head, K|V).  Runs after the append kernel has incremented
-// seq_len: a sequence whose residual just reached 128 tokens quantizes it into body tile
-// (len - n_sink)/128 - 1; every other workgroup exits at once.
-template <bool COMPACT>
+// Runs after the append kernel has incremented seq_len: the tile (sequence, kv head, K|V) of a
+// sequence whose residual just reached 128 tokens is quantized into body tile
+// (len - n_sink)/128 - 1; nothing else is written.  Workgroup w owns tiles w, w + gridDim.x,
+// ...: with one workgroup per tile (a flush known to be due for every sequence) that is one
+// tile, and with a grid of resident size (due tiles unknown on the host) its 256 threads check
+// up to 256 of its tiles at once and the workgroup quantizes the due ones, so that a call with
+// few or no due tiles costs one round of short workgroups.
+template <bool COMPACT, bool EXACT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_flush(FlushArgs a) {
     __shared__ QuantSmem sm;
-    const int kind = blockIdx.x & 1;
-    const int64_t stream = blockIdx.x >> 1;
-    const int b = (int)(stream / a.c.n_kv);
-    const int len = a.c.seq_len[b];
-    if (len <= a.n_sink || (len - a.n_sink) % kG != 0) return;
-    const int nb = (len - a.n_sink) / kG - 1;
-    if (nb >= a.c.max_blocks) return;  // the append kernel refused the token and flagged it
-    const int64_t ti = body_tile(a.c, b, (int)(stream % a.c.n_kv), nb);
-    if (ti < 0) return;
-    const uint16_t* src = static_cast<const uint16_t*>(kind ? a.c.v_resid : a.c.k_resid) + (size_t)stream * kG * kD;
-    uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) + (size_t)ti * tile_bytes(a.P.bits, COMPACT);
-    quantize_tile<COMPACT>(src, true, kD, kind, a.P, dst, nullptr, sm);
+    __shared__ uint64_t due_mask[kThreads / 64];
+    const int64_t n = (int64_t)a.c.batch * a.c.n_kv * 2;
+    const int64_t step = gridDim.x;
+    // the body tile a due tile goes to, or -1 when it is not due (or the append refused it)
+    auto target_block = [&](int64_t t) -> int {
+        const int b = (int)((t >> 1) / a.c.n_kv);
+        const int len = a.c.seq_len[b];
+        if (len <= a.n_sink || (len - a.n_sink) % kG != 0) return -1;
+        const int nb = (len - a.n_sink) / kG - 1;
+        return nb < a.c.max_blocks ? nb : -1;
+    };
+    for (int64_t base = blockIdx.x; base < n; base += step * kThreads) {
+        const int64_t mine = base + (int64_t)threadIdx.x * step;
+        const bool due = mine < n && target_block(mine) >= 0;
+        const uint64_t m = __ballot(due);
+        __syncthreads();  // the previous round is done with due_mask and the tile state in sm
+        if ((threadIdx.x & 63) == 0) due_mask[threadIdx.x >> 6] = m;
+        __syncthreads();
+        bool first = true;
+        for (int w = 0; w < kThreads / 64; ++w) {
+            // uniform across the workgroup: kept in scalar registers
+            const uint64_t dm = due_mask[w];
+            uint64_t mm = (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)dm) |
+                          (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(dm >> 32)) << 32;
+            for (; mm; mm &= mm - 1) {
+                const int64_t t = base + (int64_t)(64 * w + __builtin_ctzll(mm)) * step;
+                const int kind = (int)(t & 1);
+                const int64_t stream = t >> 1;
+                const int b = (int)(stream / a.c.n_kv);
+                const int64_t ti = body_tile(a.c, b, (int)(stream % a.c.n_kv), target_block(t));
+                if (ti < 0) continue;
+                if (!first) __syncthreads();  // every thread is done with the previous tile's LDS
+                first = false;
+                const uint16_t* src =
+                    static_cast<const uint16_t*>(kind ? a.c.v_resid : a.c.k_resid) + (size_t)stream * kG * kD;
+                uint8_t* dst =
+                    static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) + (size_t)ti * tile_bytes(a.P.bits, COMPACT);
+                quantize_tile<COMPACT, EXACT>(src, true, kD, kind, a.P, dst, nullptr, sm);
+            }
+        }
+    }
 }
 
 struct PrefillArgs {
@@ -741,7 +774,7 @@ __device__ __forceinline__ int prefill_len(const PrefillArgs& a, int b) {
 
 // One workgroup per (sequence, kv head, K|V, body tile): quantizes the prompt's tile straight
 // from the packed rows (token stride n_kv * 128 elements).
-template <bool COMPACT>
+template <bool COMPACT, bool EXACT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_prefill_tiles(PrefillArgs a) {
     __shared__ QuantSmem sm;
     const int blk = (int)(blockIdx.x % a.groups);
@@ -757,7 +790,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
     const int64_t row = (int64_t)a.cu[b] + a.n_sink + (int64_t)blk * kG;
     const char* src = static_cast<const char*>(kind ? a.v : a.k) + (size_t)((row * a.c.n_kv + kh) * kD) * esz;
     uint8_t* dst = static_cast<uint8_t*>(kind ? a.c.v_body : a.c.k_body) + (size_t)ti * tile_bytes(a.P.bits, COMPACT);
-    quantize_tile<COMPACT>(src, a.x_bf16 != 0, (int64_t)a.c.n_kv * kD, kind, a.P, dst, nullptr, sm);
+    quantize_tile<COMPACT, EXACT>(src, a.x_bf16 != 0, (int64_t)a.c.n_kv * kD, kind, a.P, dst, nullptr, sm);
 }
 
 // One workgroup per (sequence, kv head): sink and residual rows as bf16, then seq_len.
@@ -801,9 +834,14 @@ __global__ __launch_bounds__(kThreads) void k_prefill_copy(PrefillArgs a) {
 
 }  // namespace
 
+// Unrotated, unbalanced tiles with fp32 aux (the KIVI-style ablation) take the quantizer variant
+// whose RTN quotient keeps exact ties exact.
+bool exact_quotient(const QParams& qp) { return !qp.compact && qp.iters == 0 && !qp.rotate; }
+
 hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, bool x_bf16, int64_t n_outer,
                                  int64_t n_inner, int64_t x_outer, int64_t x_inner, int64_t x_token, void* out,
                                  int64_t out_outer, int64_t out_inner, int32_t* best_iter, hipStream_t stream) {
+    const bool exact = exact_quotient(qp);
     const int64_t total = n_outer * n_inner;
     const int64_t kMaxGrid = 1 << 30;
     for (int64_t t0 = 0; t0 < total; t0 += kMaxGrid) {
@@ -811,9 +849,11 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
         TileArgs a{qp, kind, x_bf16 ? 1 : 0, x, t0, n_inner, x_outer, x_inner, x_token,
                    static_cast<uint8_t*>(out), out_outer, out_inner, best_iter};
         if (qp.compact)
-            hipLaunchKernelGGL(k_quantize_tiles<true>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+            hipLaunchKernelGGL((k_quantize_tiles<true, false>), dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        else if (exact)
+            hipLaunchKernelGGL((k_quantize_tiles<false, true>), dim3((unsigned)n), dim3(kThreads), 0, stream, a);
         else
-            hipLaunchKernelGGL(k_quantize_tiles<false>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+            hipLaunchKernelGGL((k_quantize_tiles<false, false>), dim3((unsigned)n), dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -822,6 +862,7 @@ hipError_t launch_quantize_tiles(const QParams& qp, int kind, const void* x, boo
 
 hipError_t launch_prefill(const QParams& qp, const kvarn_cache& c, int n_sink, const void* k, const void* v,
                           bool x_bf16, const int32_t* cu_seqlens, int max_len, hipStream_t stream) {
+    const bool exact = exact_quotient(qp);
     int groups = max_len > n_sink ? (max_len - n_sink) / kG : 0;
     if (groups > c.max_blocks) groups = c.max_blocks;
     PrefillArgs a{qp, c, n_sink, k, v, x_bf16 ? 1 : 0, cu_seqlens, max_len, groups > 0 ? groups : 1};
@@ -830,9 +871,11 @@ hipError_t launch_prefill(const QParams& qp, const kvarn_cache& c, int n_sink, c
         const int64_t n = streams * 2 * groups;
         if (n >= (int64_t)1 << 31) return hipErrorInvalidValue;
         if (qp.compact)
-            hipLaunchKernelGGL(k_prefill_tiles<true>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+            hipLaunchKernelGGL((k_prefill_tiles<true, false>), dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        else if (exact)
+            hipLaunchKernelGGL((k_prefill_tiles<false, true>), dim3((unsigned)n), dim3(kThreads), 0, stream, a);
         else
-            hipLaunchKernelGGL(k_prefill_tiles<false>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+            hipLaunchKernelGGL((k_prefill_tiles<false, false>), dim3((unsigned)n), dim3(kThreads), 0, stream, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -840,13 +883,19 @@ hipError_t launch_prefill(const QParams& qp, const kvarn_cache& c, int n_sink, c
     return hipGetLastError();
 }
 
-hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, hipStream_t stream) {
+hipError_t launch_flush(const QParams& qp, const kvarn_cache& c, int n_sink, bool all_due, hipStream_t stream) {
+    const bool exact = exact_quotient(qp);
     FlushArgs a{qp, c, n_sink};
+    // resident grid: 256 CUs x 3 workgroups of 256 threads (the quantizer's occupancy)
+    constexpr int64_t kResidentGrid = 768;
     const int64_t n = (int64_t)c.batch * c.n_kv * 2;
+    const unsigned grid = (unsigned)(all_due ? n : (n < kResidentGrid ? n : kResidentGrid));
     if (qp.compact)
-        hipLaunchKernelGGL(k_flush<true>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((k_flush<true, false>), dim3(grid), dim3(kThreads), 0, stream, a);
+    else if (exact)
+        hipLaunchKernelGGL((k_flush<false, true>), dim3(grid), dim3(kThreads), 0, stream, a);
     else
-        hipLaunchKernelGGL(k_flush<false>, dim3((unsigned)n), dim3(kThreads), 0, stream, a);
+        hipLaunchKernelGGL((k_flush<false, false>), dim3(grid), dim3(kThreads), 0, stream, a);
     return hipGetLastError();
 }
 

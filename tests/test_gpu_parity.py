@@ -277,6 +277,54 @@ def test_append_stream(K, bits, n_sink, hint):
     check_end_to_end(out.cpu().numpy(), hc, gc, raw, q_to_host(q), False, SCALE)
 
 
+def test_append_no_hint_many_tiles(K):
+    """Without the length hint the flush runs on a resident-size grid whose workgroups check
+    several tiles each (here 1536 tiles): sequences of staggered lengths, 130 appends each, must
+    leave exactly the cache that a prefill of the whole final sequences writes (the same
+    quantizer on the same bf16 rows), and then decode identically."""
+    B, H, steps = 384, 2, 130
+    g = torch.Generator(device="cuda").manual_seed(9)
+    lens = torch.randint(0, 300, (B,), generator=g, device="cuda").cpu().numpy()
+    final = lens + steps
+    MB = int(final.max()) // 128 + 1
+    total = int(final.sum())
+    k = (torch.randn((total, H, 128), generator=g, device="cuda") * 3).to(torch.bfloat16)
+    v = torch.randn((total, H, 128), generator=g, device="cuda").to(torch.bfloat16)
+    cu_f = np.concatenate([[0], np.cumsum(final)]).astype(np.int32)
+    p = K.kvarn_params_init(2)
+    full = K.Cache(p, B, H, MB)
+    K.kvarn_prefill(p, full, k, v, K.KVARN_BF16, torch.tensor(cu_f, device="cuda"), int(final.max()))
+    # the prompts (first lens[b] rows of each sequence), then the rest one token per call
+    idx = np.concatenate([np.arange(cu_f[b], cu_f[b] + lens[b]) for b in range(B)]).astype(np.int64)
+    idx_t = torch.tensor(idx, device="cuda")
+    cu_p = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    inc = K.Cache(p, B, H, MB)
+    K.kvarn_prefill(p, inc, k[idx_t].contiguous(), v[idx_t].contiguous(), K.KVARN_BF16,
+                    torch.tensor(cu_p, device="cuda"), int(lens.max()))
+    starts = torch.tensor(cu_f[:-1] + lens, device="cuda", dtype=torch.int64)
+    for t in range(steps):
+        K.kvarn_append_token(p, inc, k[starts + t].contiguous(), v[starts + t].contiguous(), K.KVARN_BF16, -1)
+    torch.cuda.synchronize()
+    assert int(inc.err_word[0]) == 0 and int(full.err_word[0]) == 0
+    assert torch.equal(inc.seq_len, full.seq_len)
+    for b in range(B):
+        nb, nr = int(final[b]) // 128, int(final[b]) % 128
+        assert torch.equal(inc.k_body[b, :, :nb], full.k_body[b, :, :nb]), b
+        assert torch.equal(inc.v_body[b, :, :nb], full.v_body[b, :, :nb]), b
+        assert torch.equal(inc.k_resid[b, :, :nr], full.k_resid[b, :, :nr]), b
+        assert torch.equal(inc.v_resid[b, :, :nr], full.v_resid[b, :, :nr]), b
+    q = torch.randn((B, 4 * H, 128), generator=g, device="cuda").to(torch.bfloat16)
+    outs = []
+    for c in (inc, full):
+        ws_bytes = K.kvarn_decode_workspace_bytes(p, c, 4 * H, int(final.max()))
+        ws = torch.zeros(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+        out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+        K.kvarn_decode_attention(p, c, 4 * H, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE, int(final.max()), ws, ws_bytes)
+        outs.append(out)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0], outs[1])
+
+
 def test_append_overflow_flag(K):
     """With no length hint, a flush that has no body tile left is refused on the device: the
     token is dropped, err_word is set, and nothing is written out of bounds."""
