@@ -779,11 +779,28 @@ __device__ __forceinline__ float wave_sum(float v) {
     return across_rows4(row_sum(v), [](float x, float y) { return x + y; });
 }
 
+// Sum over the four row groups of a wave (lanes n, 16 + n, 32 + n, 48 + n), scattered: row group G
+// receives the sum of x_G.  permlane32_swap(a, b) returns {a's rows 0-1, b's rows 0-1} and
+// {a's rows 2-3, b's rows 2-3}, so the first two swaps leave in rows 0-1 the sums of x0, x1 over
+// rows {G, G ^ 2} and in rows 2-3 those of x2, x3; permlane16_swap(a, b) returns {a's even rows
+// in even rows, b's even rows in odd rows} and {a's odd rows in even rows, b's odd rows in odd
+// rows}, which completes each row group's sum over all four.  Integer adds wrap exactly.
+__device__ __forceinline__ uint32_t rows_reduce_scatter4(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3) {
+    const auto a = __builtin_amdgcn_permlane32_swap(x0, x2, false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(x1, x3, false, false);
+    const auto c = __builtin_amdgcn_permlane16_swap(a[0] + a[1], b[0] + b[1], false, false);
+    return c[0] + c[1];
+}
+
 // X1 = 1 (group size 5, with NH = 1): a fifth query head spread over the whole wave instead of a
-// second head group of four slots.  Its logits for a token block land in one row group of the
-// MFMA output (its digits sit in that group's A rows, the other rows are zero), so lane (G, n)
-// holds it for tokens 64 sg + 16 G + n and output channels 16 (4 q + G) + n (sg, q = 0, 1): two
-// values per lane instead of eight, and no padded head slots.
+// second head group of four slots, carried by the head group's own products in the digit slot
+// the group leaves empty: q~ and p~ have three digits, so A row 4 h + 3 (slot 3 of head h) is
+// zero, and rows 3, 7 and 11 take the extra head's digits 0, 1 and 2.  Accumulator 3 of lane
+// (G, n) then holds its digit-G partial sum for column n (a token in QK, a channel in PV; row
+// group 3 gets zero from row 15), and a reduce-scatter over the row groups combines the digits
+// so that lane (G, n) holds the head's logits for tokens 64 sg + 16 G + n and its outputs for
+// channels 16 (4 q + G) + n (sg, q = 0, 1): two values per lane, no padded head slots and no
+// MFMA of its own.
 template <int BITS, int NH, int CMP, int PG, int X1>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
@@ -919,7 +936,9 @@ void k_decode4(DecodeArgs a) {
         // source lane of the PV operand permutation (see above), as a byte address; for the
         // extra head the source row is the token block (tau), not the head
         const int perm_addr = (16 * h + 4 * G + j) * 4;
-        const int perm4 = (4 * G + j) * 4;
+        // extra head: A row 4 h + 3 (h < 3) takes digit h from lane 4 G + h of token block tau
+        const bool x1_row = X1 && j == 3 && h < 3;
+        const int perm4 = (4 * G + h) * 4;
 
         // One tile: consume cur, prefetch tile id_next into nxt.
         auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
@@ -1026,23 +1045,15 @@ void k_decode4(DecodeArgs a) {
             for (int hg = 0; hg < NH; ++hg) {
 #pragma unroll
                 for (int kap = 0; kap < 2; ++kap) {
-                    const uint4 u = sm.qp[hg][j][kap][G][h];
+                    // X1: rows 3, 7, 11 (slot 3 of heads 0-2) take the extra head's digits 0-2
+                    const uint4 u = X1 && j == 3 && h < 3 ? sm.qp4[X1 ? h : 0][kap][G] : sm.qp[hg][j][kap][G][h];
                     aq[hg][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
                 beta[hg] = sm.hv[4 * hg + G][0];
                 fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
             }
-            // extra head: its digits in the A rows of row group tau for token block tau, so that
-            // block tau's logits land in lanes G == tau; one accumulator per sg collects them
-            const v4i z4 = {0, 0, 0, 0};
-            v4i aq4[2] = {z4, z4}, c4[2] = {z4, z4};
-            if constexpr (X1) {
-#pragma unroll
-                for (int kap = 0; kap < 2; ++kap) {
-                    const uint4 u = sm.qp4[j][kap][G];
-                    aq4[kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
-                }
-            }
+            // X1: accumulator 3 holds the extra head's digit-G partial (row group 3: zero)
+            uint32_t x4[2][4];
 #pragma unroll
             for (int sg = 0; sg < 2; ++sg)
 #pragma unroll
@@ -1055,22 +1066,42 @@ void k_decode4(DecodeArgs a) {
                         v4i c = mfma_i8(aq[hg][0], b0, v4i{0, 0, 0, 0});
                         c = mfma_i8(aq[hg][1], b1, c);
                         lg[hg][4 * sg + tau] = ((float)digit_sum(c) + beta[hg]) * (fqs[hg] * s2k);
-                    }
-                    if constexpr (X1) {
-                        const bool mine = h == tau;
-                        c4[sg] = mfma_i8(mine ? aq4[0] : z4, b0, c4[sg]);
-                        c4[sg] = mfma_i8(mine ? aq4[1] : z4, b1, c4[sg]);
+                        if (X1 && hg == 0) x4[sg][tau] = (uint32_t)c[3] << (8 * G);
                     }
                 }
             float lg4[2] = {0.f, 0.f};  // extra head, tokens 64 sg + 16 G + n
             if constexpr (X1) {
                 const float beta4 = sm.hv[NHX - 1][0], fqs4 = sm.hv[NHX - 1][1] * a.scale_log2;
 #pragma unroll
-                for (int sg = 0; sg < 2; ++sg)
-                    lg4[sg] = ((float)digit_sum(c4[sg]) + beta4) * (fqs4 * sm.aux[2][64 * sg + 16 * G + n]);
+                for (int sg = 0; sg < 2; ++sg) {
+                    const uint32_t raw = rows_reduce_scatter4(x4[sg][0], x4[sg][1], x4[sg][2], x4[sg][3]);
+                    lg4[sg] = ((float)(int)raw + beta4) * (fqs4 * sm.aux[2][64 * sg + 16 * G + n]);
+                }
             }
             load_codes(tile_k(id_next), nxt.k);
 
+            // extra head: lane (G, n) holds token 64 sg + 16 G + n, i.e. token block tau = G of
+            // each sg; its digit words are byte-transposed like the head groups' and reach A rows
+            // 3, 7, 11 (digit h in row 4 h + 3) from the lanes of token block tau
+            float alpha4 = 0.f, gam4 = 0.f, fp4 = 0.f;
+            uint32_t t4[2] = {0u, 0u};
+            if constexpr (X1) {
+                alpha4 = softmax_wave(lg4, false, m4, l4);
+                lg4[0] *= sm.aux[3][16 * G + n];
+                lg4[1] *= sm.aux[3][64 + 16 * G + n];
+                const float pmx = wave_max(fmaxf(lg4[0], lg4[1]));
+                const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
+                const float ps = (G & 1) ? psc : psc * MUL;
+                float gl = 0.f;
+#pragma unroll
+                for (int sg = 0; sg < 2; ++sg) {
+                    const float yf = fmaf(lg4[sg], ps, MAGIC);
+                    gl = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * G + n], gl);
+                    t4[sg] = quad_transpose_bytes(__float_as_uint(yf) + (0x80808080u - MAGIC_BITS), j);
+                }
+                gam4 = wave_sum((G & 1) ? gl * MUL : gl);
+                fp4 = pmx * (1.0f / (MUL * (float)QMAX));
+            }
             v4i ap[NH][2];
             float alpha[NH], gam[NH], fp[NH];
 #pragma unroll
@@ -1095,41 +1126,19 @@ void k_decode4(DecodeArgs a) {
                         else gam_e = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_e);
                         const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
                         const uint32_t t = quad_transpose_bytes(y, j);
-                        D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t) ^ 0x80808080u;
+                        uint32_t d = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t);
+                        if (X1 && hg == 0) {
+                            const uint32_t d4 = (uint32_t)__builtin_amdgcn_ds_bpermute(perm4 + 64 * tau, (int)t4[sg]);
+                            d = x1_row ? d4 : d;
+                        }
+                        D[tau] = d ^ 0x80808080u;
                     }
                     ap[hg][sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
                 }
                 gam[hg] = row_sum(fmaf(gam_o, MUL, gam_e));
                 fp[hg] = pmx * (1.0f / (MUL * (float)QMAX));
             }
-            // extra head: lane (G, n) holds token 64 sg + 16 G + n, i.e. token block tau = G of
-            // each sg, so the byte transpose and the operand permutation are those of the head
-            // groups with the source row taken from the token block instead of the head
-            v4i ap4[2] = {z4, z4}, acc4[2] = {z4, z4};
-            float alpha4 = 0.f, gam4 = 0.f, fp4 = 0.f;
-            if constexpr (X1) {
-                alpha4 = softmax_wave(lg4, false, m4, l4);
-                lg4[0] *= sm.aux[3][16 * G + n];
-                lg4[1] *= sm.aux[3][64 + 16 * G + n];
-                const float pmx = wave_max(fmaxf(lg4[0], lg4[1]));
-                const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
-                const float ps = (G & 1) ? psc : psc * MUL;
-                float gl = 0.f;
-#pragma unroll
-                for (int sg = 0; sg < 2; ++sg) {
-                    const float yf = fmaf(lg4[sg], ps, MAGIC);
-                    gl = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * G + n], gl);
-                    const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
-                    const uint32_t t = quad_transpose_bytes(y, j);
-                    uint32_t D[4];
-#pragma unroll
-                    for (int tau = 0; tau < 4; ++tau)
-                        D[tau] = (uint32_t)__builtin_amdgcn_ds_bpermute(perm4 + 64 * tau, (int)t) ^ 0x80808080u;
-                    ap4[sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
-                }
-                gam4 = wave_sum((G & 1) ? gl * MUL : gl);
-                fp4 = pmx * (1.0f / (MUL * (float)QMAX));
-            }
+            uint32_t x5[8];  // X1: accumulator 3, the extra head's digit-G partial of channel block mt
 #pragma unroll
             for (int mt = 0; mt < 8; ++mt) {
                 const v4i v0 = unit_planes<BITS>(&vw[0][mt * WPU]);
@@ -1140,19 +1149,15 @@ void k_decode4(DecodeArgs a) {
                     v4i acc = mfma_i8(ap[hg][0], v0, v4i{0, 0, 0, 0});
                     acc = mfma_i8(ap[hg][1], v1, acc);
                     orot[hg][mt] = fmaf((float)digit_sum(acc) + gam[hg], fp[hg] * s2v, orot[hg][mt] * alpha[hg]);
-                }
-                if constexpr (X1) {
-                    // channel block mt lands in lanes G == mt % 4 (A rows of that row group)
-                    const bool mine = h == (mt & 3);
-                    acc4[mt >> 2] = mfma_i8(mine ? ap4[0] : z4, v0, acc4[mt >> 2]);
-                    acc4[mt >> 2] = mfma_i8(mine ? ap4[1] : z4, v1, acc4[mt >> 2]);
+                    if (X1 && hg == 0) x5[mt] = (uint32_t)acc[3] << (8 * G);
                 }
             }
             if constexpr (X1) {
 #pragma unroll
-                for (int q = 0; q < 2; ++q)
-                    orot4[q] = fmaf((float)digit_sum(acc4[q]) + gam4, fp4 * sm.aux[5][16 * (4 * q + G) + n],
-                                    orot4[q] * alpha4);
+                for (int q = 0; q < 2; ++q) {
+                    const uint32_t raw = rows_reduce_scatter4(x5[4 * q], x5[4 * q + 1], x5[4 * q + 2], x5[4 * q + 3]);
+                    orot4[q] = fmaf((float)(int)raw + gam4, fp4 * sm.aux[5][16 * (4 * q + G) + n], orot4[q] * alpha4);
+                }
             }
             load_codes(tile_v(id_next), nxt.v);
         };
