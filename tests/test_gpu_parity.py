@@ -111,7 +111,7 @@ def _decode(K, built, q, out_dtype=torch.float32, max_len=None):
     p, cache = built.params, built.cache
     max_len = built.length + 1 if max_len is None else max_len
     ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, built.n_q, max_len)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
     out = torch.empty(q.shape, dtype=out_dtype, device="cuda")
     qd = K.KVARN_F32 if q.dtype == torch.float32 else K.KVARN_BF16
     od = K.KVARN_F32 if out_dtype == torch.float32 else K.KVARN_BF16
@@ -197,7 +197,7 @@ def test_decode_peaked_softmax(K, mult):
     out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
     max_len = built.length + 1
     ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, built.n_q, max_len)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
     K.kvarn_decode_attention(p, cache, built.n_q, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE * mult, max_len, ws,
                              ws_bytes)
     torch.cuda.synchronize()
@@ -213,6 +213,34 @@ def test_decode_length_above_hint(K):
     q = workloads.decode_queries(built, seed=4)
     out = _decode(K, built, q, max_len=300)
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
+def test_decode_workspace_reuse(K):
+    """One workspace serves consecutive calls on caches of different shapes and split plans (more
+    streams after fewer, many splits after few; every kernel family): each call rewrites what it
+    reads, so every output equals that of a call with a fresh workspace."""
+    from paper_2606_03458_amd import workloads
+    cases = []
+    for i, (batch, n_q, n_kv, ctx) in enumerate([(1, 32, 8, 64 * 128 + 40), (6, 40, 8, 24 * 128 + 5),
+                                                  (2, 64, 4, 40 * 128 + 99), (1, 8, 1, 96 * 128 + 1)]):
+        built, _ = workloads.build("llama", context=ctx, batch=batch, n_q=n_q, n_kv=n_kv)
+        cases.append((built, workloads.decode_queries(built, seed=40 + i)))
+    sizes = [K.kvarn_decode_workspace_bytes(b.params, b.cache, b.n_q, b.length) for b, _ in cases]
+    assert all(n > 0 for n in sizes)
+    shared = torch.zeros(max(sizes), dtype=torch.uint8, device="cuda")
+    for rep in range(2):
+        for (built, q), n in zip(cases, sizes):
+            p, cache = built.params, built.cache
+            got = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+            ref = torch.empty(q.shape, dtype=torch.float32, device="cuda")
+            K.kvarn_decode_attention(p, cache, built.n_q, q, K.KVARN_BF16, got, K.KVARN_F32, SCALE, built.length,
+                                     shared, shared.numel())
+            fresh = torch.zeros(n, dtype=torch.uint8, device="cuda")
+            K.kvarn_decode_attention(p, cache, built.n_q, q, K.KVARN_BF16, ref, K.KVARN_F32, SCALE, built.length,
+                                     fresh, n)
+            torch.cuda.synchronize()
+            assert torch.equal(got, ref), (rep, n)
+    check_output(got.cpu().numpy(), _ref(cases[-1][0], cases[-1][1]), bf16_out=False)
 
 
 def test_decode_deterministic(K):
@@ -268,7 +296,7 @@ def test_append_stream(K, bits, n_sink, hint):
     # decode over the GPU's cache, and end to end over the oracle's own (its own flushes)
     q = torch.randn((B, 4 * H, 128), generator=g, device="cuda").to(torch.bfloat16)
     ws_bytes = K.kvarn_decode_workspace_bytes(p, cache, 4 * H, steps + 1)
-    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
     out = torch.empty(q.shape, dtype=torch.float32, device="cuda")
     K.kvarn_decode_attention(p, cache, 4 * H, q, K.KVARN_BF16, out, K.KVARN_F32, SCALE, steps + 1, ws, ws_bytes)
     torch.cuda.synchronize()
