@@ -93,7 +93,10 @@ __device__ __forceinline__ v4i unit_i8(const uint32_t* w) {
     }
 }
 
-__device__ __forceinline__ float xor_max(float v, int m) { return fmaxf(v, __shfl_xor(v, m)); }
+// Max in the NaN-propagating form: no operand of the reductions here is a NaN, and fmaxf would
+// first quiet every operand that comes from another lane (one more instruction per step).
+__device__ __forceinline__ float fmax_any(float x, float y) { return __builtin_elementwise_maximum(x, y); }
+__device__ __forceinline__ float xor_max(float v, int m) { return fmax_any(v, __shfl_xor(v, m)); }
 __device__ __forceinline__ float xor_sum(float v, int m) { return v + __shfl_xor(v, m); }
 
 // Four values y0..y3, each a fixed-point integer plus 0x808080 (0x8080 for two digits), to
@@ -708,10 +711,19 @@ __device__ __forceinline__ float fdpp_mirror(float v) { return __int_as_float(dp
 // the other quad of the half (mirror within 8), then the other half (mirror within 16).  Every
 // step combines two equal-shaped partial results, so all 16 lanes end with identical values.
 __device__ __forceinline__ float row_max(float v) {
-    v = fmaxf(v, fdpp_x1(v));
-    v = fmaxf(v, fdpp_x2(v));
-    v = fmaxf(v, fdpp_half_mirror(v));
-    return fmaxf(v, fdpp_mirror(v));
+    v = fmax_any(v, fdpp_x1(v));
+    v = fmax_any(v, fdpp_x2(v));
+    v = fmax_any(v, fdpp_half_mirror(v));
+    return fmax_any(v, fdpp_mirror(v));
+}
+// The same for values >= 0: their bit patterns order as signed integers, so the steps run as
+// integer max instructions with the lane move folded in.
+__device__ __forceinline__ float row_max_nonneg(float v) {
+    int b = __float_as_int(v);
+    b = max(b, dpp_x1(b));
+    b = max(b, dpp_x2(b));
+    b = max(b, dpp_half_mirror(b));
+    return __int_as_float(max(b, dpp_mirror(b)));
 }
 __device__ __forceinline__ float row_sum(float v) {
     v += fdpp_x1(v);
@@ -721,9 +733,10 @@ __device__ __forceinline__ float row_sum(float v) {
 }
 
 // The digit-weighted sum of one output lane: register i holds the partial sum of digit i.  The
-// true sum fits int32, so the wrapping arithmetic below is exact.
+// true sum fits int32, so the wrapping arithmetic below is exact.  Horner form: two
+// shift-and-add instructions.
 __device__ __forceinline__ int digit_sum(v4i c) {
-    return (int)(((uint32_t)c[2] << 16) + ((uint32_t)c[1] << 8) + (uint32_t)c[0]);
+    return (int)(((((uint32_t)c[2] << 8) + (uint32_t)c[1]) << 8) + (uint32_t)c[0]);
 }
 
 // Lane j of a quad holds y (row j of a 4 x 4 byte matrix); returns column j: byte i of the
@@ -773,7 +786,12 @@ __device__ __forceinline__ float across_rows4(float v, F f) {
     return f(__uint_as_float(y[0]), __uint_as_float(y[1]));
 }
 __device__ __forceinline__ float wave_max(float v) {
-    return across_rows4(row_max(v), [](float x, float y) { return fmaxf(x, y); });
+    return across_rows4(row_max(v), [](float x, float y) { return fmax_any(x, y); });
+}
+__device__ __forceinline__ float wave_max_nonneg(float v) {
+    return across_rows4(row_max_nonneg(v), [](float x, float y) {
+        return __int_as_float(max(__float_as_int(x), __float_as_int(y)));
+    });
 }
 __device__ __forceinline__ float wave_sum(float v) {
     return across_rows4(row_sum(v), [](float x, float y) { return x + y; });
@@ -981,7 +999,7 @@ void k_decode4(DecodeArgs a) {
                         qt[k] = qr[hg][k] * av[k];
                         mx = fmaxf(mx, fabsf(qt[k]));
                     }
-                    mx = row_max(mx);
+                    mx = row_max_nonneg(mx);
                     const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
                     // channels 8n .. 8n + 3 sit in an even dword of the A operand, 8n + 4 ..
                     // 8n + 7 in an odd one; beta is kept in units of MUL grid steps
@@ -1013,7 +1031,7 @@ void k_decode4(DecodeArgs a) {
                     const float2 a2 = *reinterpret_cast<const float2*>(&sm.aux[0][2 * l]);
                     const float2 r2 = *reinterpret_cast<const float2*>(&sm.aux[1][2 * l]);
                     const float qt0 = qr4[0] * a2.x, qt1 = qr4[1] * a2.y;
-                    const float mx = wave_max(fmaxf(fabsf(qt0), fabsf(qt1)));
+                    const float mx = wave_max_nonneg(fmaxf(fabsf(qt0), fabsf(qt1)));
                     const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
                     const bool even = ((l >> 1) & 1) == 0;
                     const float y0f = fmaf(qt0, even ? sc * MUL : sc, MAGIC);
@@ -1040,7 +1058,7 @@ void k_decode4(DecodeArgs a) {
             // inner: the code planes of a token block are extracted once and used at once.
             float lg[NH][8];
             v4i aq[NH][2];
-            float beta[NH], fqs[NH];
+            float bq[NH], fqs[NH];  // beta and the grid step in logit units (log2, scaled)
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
 #pragma unroll
@@ -1049,8 +1067,8 @@ void k_decode4(DecodeArgs a) {
                     const uint4 u = X1 && j == 3 && h < 3 ? sm.qp4[X1 ? h : 0][kap][G] : sm.qp[hg][j][kap][G][h];
                     aq[hg][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
-                beta[hg] = sm.hv[4 * hg + G][0];
                 fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
+                bq[hg] = sm.hv[4 * hg + G][0] * fqs[hg];
             }
             // X1: accumulator 3 holds the extra head's digit-G partial (row group 3: zero)
             uint32_t x4[2][4];
@@ -1065,17 +1083,17 @@ void k_decode4(DecodeArgs a) {
                     for (int hg = 0; hg < NH; ++hg) {
                         v4i c = mfma_i8(aq[hg][0], b0, v4i{0, 0, 0, 0});
                         c = mfma_i8(aq[hg][1], b1, c);
-                        lg[hg][4 * sg + tau] = ((float)digit_sum(c) + beta[hg]) * (fqs[hg] * s2k);
+                        lg[hg][4 * sg + tau] = fmaf((float)digit_sum(c), fqs[hg], bq[hg]) * s2k;
                         if (X1 && hg == 0) x4[sg][tau] = (uint32_t)c[3] << (8 * G);
                     }
                 }
             float lg4[2] = {0.f, 0.f};  // extra head, tokens 64 sg + 16 G + n
             if constexpr (X1) {
-                const float beta4 = sm.hv[NHX - 1][0], fqs4 = sm.hv[NHX - 1][1] * a.scale_log2;
+                const float fqs4 = sm.hv[NHX - 1][1] * a.scale_log2, bq4 = sm.hv[NHX - 1][0] * fqs4;
 #pragma unroll
                 for (int sg = 0; sg < 2; ++sg) {
                     const uint32_t raw = rows_reduce_scatter4(x4[sg][0], x4[sg][1], x4[sg][2], x4[sg][3]);
-                    lg4[sg] = ((float)(int)raw + beta4) * (fqs4 * sm.aux[2][64 * sg + 16 * G + n]);
+                    lg4[sg] = fmaf((float)(int)raw, fqs4, bq4) * sm.aux[2][64 * sg + 16 * G + n];
                 }
             }
             load_codes(tile_k(id_next), nxt.k);
@@ -1089,7 +1107,7 @@ void k_decode4(DecodeArgs a) {
                 alpha4 = softmax_wave(lg4, false, m4, l4);
                 lg4[0] *= sm.aux[3][16 * G + n];
                 lg4[1] *= sm.aux[3][64 + 16 * G + n];
-                const float pmx = wave_max(fmaxf(lg4[0], lg4[1]));
+                const float pmx = wave_max_nonneg(fmaxf(lg4[0], lg4[1]));
                 const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
                 const float ps = (G & 1) ? psc : psc * MUL;
                 float gl = 0.f;
@@ -1099,11 +1117,11 @@ void k_decode4(DecodeArgs a) {
                     gl = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * G + n], gl);
                     t4[sg] = quad_transpose_bytes(__float_as_uint(yf) + (0x80808080u - MAGIC_BITS), j);
                 }
-                gam4 = wave_sum((G & 1) ? gl * MUL : gl);
                 fp4 = pmx * (1.0f / (MUL * (float)QMAX));
+                gam4 = wave_sum((G & 1) ? gl * MUL : gl) * fp4;
             }
             v4i ap[NH][2];
-            float alpha[NH], gam[NH], fp[NH];
+            float alpha[NH], gam[NH], fp[NH];  // gam: the offset term in output units
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
                 alpha[hg] = softmax_update(lg[hg], false, m_run[hg], l_run[hg]);
@@ -1113,7 +1131,7 @@ void k_decode4(DecodeArgs a) {
                     lg[hg][k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + n];
                     pmx = fmaxf(pmx, lg[hg][k]);
                 }
-                pmx = row_max(pmx);
+                pmx = row_max_nonneg(pmx);
                 const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
                 float gam_e = 0.f, gam_o = 0.f;
 #pragma unroll
@@ -1135,8 +1153,8 @@ void k_decode4(DecodeArgs a) {
                     }
                     ap[hg][sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
                 }
-                gam[hg] = row_sum(fmaf(gam_o, MUL, gam_e));
                 fp[hg] = pmx * (1.0f / (MUL * (float)QMAX));
+                gam[hg] = row_sum(fmaf(gam_o, MUL, gam_e)) * fp[hg];
             }
             uint32_t x5[8];  // X1: accumulator 3, the extra head's digit-G partial of channel block mt
 #pragma unroll
@@ -1148,7 +1166,7 @@ void k_decode4(DecodeArgs a) {
                 for (int hg = 0; hg < NH; ++hg) {
                     v4i acc = mfma_i8(ap[hg][0], v0, v4i{0, 0, 0, 0});
                     acc = mfma_i8(ap[hg][1], v1, acc);
-                    orot[hg][mt] = fmaf((float)digit_sum(acc) + gam[hg], fp[hg] * s2v, orot[hg][mt] * alpha[hg]);
+                    orot[hg][mt] = fmaf(fmaf((float)digit_sum(acc), fp[hg], gam[hg]), s2v, orot[hg][mt] * alpha[hg]);
                     if (X1 && hg == 0) x5[mt] = (uint32_t)acc[3] << (8 * G);
                 }
             }
@@ -1156,7 +1174,7 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
                 for (int q = 0; q < 2; ++q) {
                     const uint32_t raw = rows_reduce_scatter4(x5[4 * q], x5[4 * q + 1], x5[4 * q + 2], x5[4 * q + 3]);
-                    orot4[q] = fmaf((float)(int)raw + gam4, fp4 * sm.aux[5][16 * (4 * q + G) + n], orot4[q] * alpha4);
+                    orot4[q] = fmaf(fmaf((float)(int)raw, fp4, gam4), sm.aux[5][16 * (4 * q + G) + n], orot4[q] * alpha4);
                 }
             }
             load_codes(tile_v(id_next), nxt.v);

@@ -37,11 +37,16 @@ struct Lane {
 struct OpSum {
     __device__ static float f(float a, float b) { return a + b; }
 };
+// Max and min in the NaN-propagating forms: no operand here is a NaN (the input is finite), and
+// fmaxf / fminf would first quiet every operand that comes from another lane or from LDS (one
+// more instruction each).
+__device__ __forceinline__ float fmax_any(float a, float b) { return __builtin_elementwise_maximum(a, b); }
+__device__ __forceinline__ float fmin_any(float a, float b) { return __builtin_elementwise_minimum(a, b); }
 struct OpMax {
-    __device__ static float f(float a, float b) { return fmaxf(a, b); }
+    __device__ static float f(float a, float b) { return fmax_any(a, b); }
 };
 struct OpMin {
-    __device__ static float f(float a, float b) { return fminf(a, b); }
+    __device__ static float f(float a, float b) { return fmin_any(a, b); }
 };
 
 template <int CTRL>
@@ -91,8 +96,8 @@ __device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& b
     }
     __syncthreads();
     if (STAT) {
-        *xmax = fmaxf(fmaxf(sm.rstat[buf][0][0], sm.rstat[buf][1][0]), fmaxf(sm.rstat[buf][2][0], sm.rstat[buf][3][0]));
-        *xmin = fminf(fminf(sm.rstat[buf][0][1], sm.rstat[buf][1][1]), fminf(sm.rstat[buf][2][1], sm.rstat[buf][3][1]));
+        *xmax = fmax_any(fmax_any(sm.rstat[buf][0][0], sm.rstat[buf][1][0]), fmax_any(sm.rstat[buf][2][0], sm.rstat[buf][3][0]));
+        *xmin = fmin_any(fmin_any(sm.rstat[buf][0][1], sm.rstat[buf][1][1]), fmin_any(sm.rstat[buf][2][1], sm.rstat[buf][3][1]));
     }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -471,7 +476,7 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         __syncthreads();
 #pragma unroll
         for (int k = 0; k < 3; ++k)
-            st[k] = fmaxf(fmaxf(sm.red[buf][0][k], sm.red[buf][1][k]), fmaxf(sm.red[buf][2][k], sm.red[buf][3][k]));
+            st[k] = fmax_any(fmax_any(sm.red[buf][0][k], sm.red[buf][1][k]), fmax_any(sm.red[buf][2][k], sm.red[buf][3][k]));
         buf ^= 1;
         int e = 0;
         if (-st[2] >= 0.015625f)
