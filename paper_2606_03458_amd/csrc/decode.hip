@@ -37,6 +37,7 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef unsigned v4u __attribute__((ext_vector_type(4)));
+typedef unsigned v2u __attribute__((ext_vector_type(2)));
 
 constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
 
@@ -199,6 +200,62 @@ __device__ __forceinline__ void stage_aux(float (&aux)[6][kD], const AuxRegs& r,
             row[k] = make_float4(lo[0], lo[1], hi[0], hi[1]);
         }
     }
+}
+
+// The aux of one K tile and one V tile as loaded for the row-digit kernels: lane l holds entries
+// 2l and 2l + 1 of each row (a, b, s2 of the K tile's channels, of the V tile's tokens), so that
+// it forms the offset ratios b / a of its own entries.  fp32: three 8-byte loads per tile;
+// compact: the two binary16 offsets (4 bytes) and the two E4M3 values of each scale row
+// (2 bytes each).
+template <int CMP>
+struct HalfAux {
+    uint2 a, b, s;
+};
+template <>
+struct HalfAux<1> {
+    uint32_t b, a, s;
+};
+__device__ __forceinline__ uint2 load_stream2(const uint8_t* p) {
+    return __builtin_bit_cast(uint2, __builtin_nontemporal_load(reinterpret_cast<const v2u*>(p)));
+}
+template <int CMP>
+__device__ __forceinline__ void load_half_aux(HalfAux<CMP>& r, const uint8_t* t, size_t cb, int l) {
+    if constexpr (CMP) {
+        r.b = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(t + cb + 4 * l));
+        r.a = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(t + cb + 256 + 2 * l));
+        r.s = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(t + cb + 384 + 2 * l));
+    } else {
+        r.a = load_stream2(t + cb + 8 * l);
+        r.b = load_stream2(t + cb + 512 + 8 * l);
+        r.s = load_stream2(t + cb + 1024 + 8 * l);
+    }
+}
+// -> fp32 rows a, b / a, s2 (rows r0, r0 + 1, r0 + 2 of aux), entries 2l and 2l + 1; both
+// compact conversions are exact
+template <int CMP>
+__device__ __forceinline__ void stage_half_aux(float (&aux)[6][kD], int r0, const HalfAux<CMP>& r, int l) {
+    float a0, a1, b0, b1, s0, s1;
+    if constexpr (CMP) {
+        const auto ap = __builtin_amdgcn_cvt_pk_f32_fp8((int)r.a, false);
+        const auto sp = __builtin_amdgcn_cvt_pk_f32_fp8((int)r.s, false);
+        a0 = ap[0];
+        a1 = ap[1];
+        s0 = sp[0];
+        s1 = sp[1];
+        b0 = (float)__builtin_bit_cast(_Float16, (uint16_t)(r.b & 0xFFFFu));
+        b1 = (float)__builtin_bit_cast(_Float16, (uint16_t)(r.b >> 16));
+    } else {
+        a0 = __uint_as_float(r.a.x);
+        a1 = __uint_as_float(r.a.y);
+        b0 = __uint_as_float(r.b.x);
+        b1 = __uint_as_float(r.b.y);
+        s0 = __uint_as_float(r.s.x);
+        s1 = __uint_as_float(r.s.y);
+    }
+    *reinterpret_cast<float2*>(&aux[r0][2 * l]) = make_float2(a0, a1);
+    *reinterpret_cast<float2*>(&aux[r0 + 1][2 * l]) =
+        make_float2(b0 * __builtin_amdgcn_rcpf(a0), b1 * __builtin_amdgcn_rcpf(a1));
+    *reinterpret_cast<float2*>(&aux[r0 + 2][2 * l]) = make_float2(s0, s1);
 }
 
 template <int GQ>
@@ -917,14 +974,17 @@ void k_decode4(DecodeArgs a) {
         // each wait counts exactly the loads it needs.
         struct TileRegs {
             uint4 k[2][2 * WPU], v[2][2 * WPU];
-            AuxRegs ar;
+            HalfAux<CMP> ak, av;
         };
         TileRegs ra, rb;
         // tiles by block_id (pool id when paged); the id of the next tile is read a tile ahead
         auto tile_of = [&](int id) { return PG ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id; };
         auto tile_k = [&](int id) { return a.k_body + tile_of(id) * tb; };
         auto tile_v = [&](int id) { return a.v_body + tile_of(id) * tb; };
-        auto load_aux = [&](TileRegs& r, int id) { load_aux_regs<CMP>(r.ar, tile_k(id), tile_v(id), cb, l); };
+        auto load_aux = [&](TileRegs& r, int id) {
+            load_half_aux<CMP>(r.ak, tile_k(id), cb, l);
+            load_half_aux<CMP>(r.av, tile_v(id), cb, l);
+        };
         auto load_codes = [&](const uint8_t* t, uint4 (&c)[2][2 * WPU]) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -961,14 +1021,11 @@ void k_decode4(DecodeArgs a) {
         // One tile: consume cur, prefetch tile id_next into nxt.
         auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
-            stage_aux<CMP>(sm.aux, cur.ar, l);
-            __syncthreads();
+            // aux rows a_K, b_K / a_K, s2_K, a_V, b_V / a_V, s2_V (offsets as ratios: keys per
+            // channel, values per token)
+            stage_half_aux<CMP>(sm.aux, 0, cur.ak, l);
+            stage_half_aux<CMP>(sm.aux, 3, cur.av, l);
             load_aux(nxt, id_next);
-            // offsets as ratios b / a: keys per channel, values per token
-            sm.aux[1][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l]);
-            sm.aux[1][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[0][2 * l + 1]);
-            sm.aux[4][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l]);
-            sm.aux[4][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l + 1]);
             __syncthreads();
             uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
 #pragma unroll

@@ -22,7 +22,7 @@ import torch
 D = 128
 
 # Seeds of the five workloads (the tiny case's seed is 0).
-SEEDS = {"tiny": 0, "llama": 1, "throughput": 2, "streaming": 3, "stress": 4}
+SEEDS = {"tiny": 0, "llama": 1, "throughput": 2, "streaming": 3, "stress": 4, "gqa8": 5}
 
 
 def _gen(seed: int, device) -> torch.Generator:
@@ -80,4 +80,6 @@ WORKLOADS = {
     "throughput": dict(layers=32, batch=32, n_q=32, n_kv=8, context=32768, dtype="bf16", dist="llama", bits=2),
     "streaming": dict(layers=1, batch=64, n_q=32, n_kv=8, context=32768, dtype="bf16", dist="llama", bits=2),
     "stress": dict(layers=1, batch=128, n_q=40, n_kv=8, context=16384, dtype="bf16", dist="stress", bits=2),
+    # query groups of 8 (64 q / 8 kv heads, the layout of 70B-class models), batch 128, 16k
+    "gqa8": dict(layers=1, batch=128, n_q=64, n_kv=8, context=16384, dtype="bf16", dist="llama", bits=2),
 }
