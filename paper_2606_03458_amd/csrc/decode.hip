@@ -203,10 +203,9 @@ __device__ __forceinline__ void stage_aux(float (&aux)[6][kD], const AuxRegs& r,
 }
 
 // The aux of one K tile and one V tile as loaded for the row-digit kernels: lane l holds entries
-// 2l and 2l + 1 of each row (a, b, s2 of the K tile's channels, of the V tile's tokens), so that
-// it forms the offset ratios b / a of its own entries.  fp32: three 8-byte loads per tile;
-// compact: the two binary16 offsets (4 bytes) and the two E4M3 values of each scale row
-// (2 bytes each).
+// 2l and 2l + 1 of each row (a, b, s2 of the K tile's channels, of the V tile's tokens).  fp32:
+// three 8-byte loads per tile; compact: the two binary16 offsets (4 bytes) and the two E4M3
+// values of each scale row (2 bytes each).
 template <int CMP>
 struct HalfAux {
     uint2 a, b, s;
@@ -230,8 +229,8 @@ __device__ __forceinline__ void load_half_aux(HalfAux<CMP>& r, const uint8_t* t,
         r.s = load_stream2(t + cb + 1024 + 8 * l);
     }
 }
-// -> fp32 rows a, b / a, s2 (rows r0, r0 + 1, r0 + 2 of aux), entries 2l and 2l + 1; both
-// compact conversions are exact
+// -> fp32 rows a, b, s2 (rows r0, r0 + 1, r0 + 2 of aux), entries 2l and 2l + 1; both compact
+// conversions are exact
 template <int CMP>
 __device__ __forceinline__ void stage_half_aux(float (&aux)[6][kD], int r0, const HalfAux<CMP>& r, int l) {
     float a0, a1, b0, b1, s0, s1;
@@ -253,8 +252,7 @@ __device__ __forceinline__ void stage_half_aux(float (&aux)[6][kD], int r0, cons
         s1 = __uint_as_float(r.s.y);
     }
     *reinterpret_cast<float2*>(&aux[r0][2 * l]) = make_float2(a0, a1);
-    *reinterpret_cast<float2*>(&aux[r0 + 1][2 * l]) =
-        make_float2(b0 * __builtin_amdgcn_rcpf(a0), b1 * __builtin_amdgcn_rcpf(a1));
+    *reinterpret_cast<float2*>(&aux[r0 + 1][2 * l]) = make_float2(b0, b1);
     *reinterpret_cast<float2*>(&aux[r0 + 2][2 * l]) = make_float2(s0, s1);
 }
 
@@ -854,17 +852,20 @@ __device__ __forceinline__ float wave_sum(float v) {
     return across_rows4(row_sum(v), [](float x, float y) { return x + y; });
 }
 
-// Sum over the four row groups of a wave (lanes n, 16 + n, 32 + n, 48 + n), scattered: row group G
-// receives the sum of x_G.  permlane32_swap(a, b) returns {a's rows 0-1, b's rows 0-1} and
-// {a's rows 2-3, b's rows 2-3}, so the first two swaps leave in rows 0-1 the sums of x0, x1 over
-// rows {G, G ^ 2} and in rows 2-3 those of x2, x3; permlane16_swap(a, b) returns {a's even rows
-// in even rows, b's even rows in odd rows} and {a's odd rows in even rows, b's odd rows in odd
-// rows}, which completes each row group's sum over all four.  Integer adds wrap exactly.
-__device__ __forceinline__ uint32_t rows_reduce_scatter4(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3) {
+// Digit-weighted sum over the four row groups of a wave (lanes n, 16 + n, 32 + n, 48 + n),
+// scattered: row group G receives the sum over r of x_G(row group r) * 256^r.
+// permlane32_swap(a, b) returns {a's rows 0-1, b's rows 0-1} and {a's rows 2-3, b's rows 2-3}, so
+// after the first two swaps a lane of row group R holds x(R mod 2) and x(R mod 2 + 2) of x0, x1
+// (rows 0-1) or x2, x3 (rows 2-3); their weights differ by 256^2, so the lane adds the second
+// times 2^16 and keeps the common factor 256^(R mod 2) for later.  permlane16_swap(a, b) returns
+// {a's even rows in even rows, b's even rows in odd rows} and {a's odd rows in even rows, b's odd
+// rows in odd rows}: the even-row partial (factor 1) plus 2^8 times the odd-row partial (factor
+// 256) completes each row group's sum.  Integer arithmetic wraps exactly.
+__device__ __forceinline__ uint32_t rows_digit_reduce_scatter4(uint32_t x0, uint32_t x1, uint32_t x2, uint32_t x3) {
     const auto a = __builtin_amdgcn_permlane32_swap(x0, x2, false, false);
     const auto b = __builtin_amdgcn_permlane32_swap(x1, x3, false, false);
-    const auto c = __builtin_amdgcn_permlane16_swap(a[0] + a[1], b[0] + b[1], false, false);
-    return c[0] + c[1];
+    const auto c = __builtin_amdgcn_permlane16_swap(a[0] + (a[1] << 16), b[0] + (b[1] << 16), false, false);
+    return c[0] + (c[1] << 8);
 }
 
 // X1 = 1 (group size 5, with NH = 1): a fifth query head spread over the whole wave instead of a
@@ -1021,8 +1022,7 @@ void k_decode4(DecodeArgs a) {
         // One tile: consume cur, prefetch tile id_next into nxt.
         auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
             __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
-            // aux rows a_K, b_K / a_K, s2_K, a_V, b_V / a_V, s2_V (offsets as ratios: keys per
-            // channel, values per token)
+            // aux rows a_K, b_K, s2_K (keys: per channel), a_V, b_V, s2_V (values: per token)
             stage_half_aux<CMP>(sm.aux, 0, cur.ak, l);
             stage_half_aux<CMP>(sm.aux, 3, cur.av, l);
             load_aux(nxt, id_next);
@@ -1037,15 +1037,15 @@ void k_decode4(DecodeArgs a) {
                     vw[s][4 * k] = cur.v[s][k].x; vw[s][4 * k + 1] = cur.v[s][k].y;
                     vw[s][4 * k + 2] = cur.v[s][k].z; vw[s][4 * k + 3] = cur.v[s][k].w;
                 }
-            // q~ = q_rot * a_K as fixed point on a per-head grid, then three digit planes; beta
-            // in grid units from the same rounded integers times b_K / a_K
+            // q~ = q_rot * a_K as fixed point on a per-head grid, then three digit planes; beta =
+            // sum over channels of q_rot * b_K, the offsets' part of the logit (unscaled)
             {
                 const float4 a0 = *reinterpret_cast<const float4*>(&sm.aux[0][8 * n]);
                 const float4 a1 = *reinterpret_cast<const float4*>(&sm.aux[0][8 * n + 4]);
-                const float4 r0 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n]);
-                const float4 r1 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n + 4]);
+                const float4 b0 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n]);
+                const float4 b1 = *reinterpret_cast<const float4*>(&sm.aux[1][8 * n + 4]);
                 const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-                const float rk[8] = {r0.x, r0.y, r0.z, r0.w, r1.x, r1.y, r1.z, r1.w};
+                const float bk[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
                 // channels 8n .. 8n + 7 = kappa n / 8, group (n % 8) / 2, components 2 (n % 2) + {0, 1}
                 const int kap = n >> 3, Gq = (n >> 1) & 3, half = n & 1;
 #pragma unroll
@@ -1059,17 +1059,16 @@ void k_decode4(DecodeArgs a) {
                     mx = row_max_nonneg(mx);
                     const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
                     // channels 8n .. 8n + 3 sit in an even dword of the A operand, 8n + 4 ..
-                    // 8n + 7 in an odd one; beta is kept in units of MUL grid steps
-                    float bs_e = 0.f, bs_o = 0.f;
+                    // 8n + 7 in an odd one
+                    float bsum = 0.f;
                     uint32_t y[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
                         const float yf = fmaf(qt[k], k < 4 ? sc * MUL : sc, MAGIC);
-                        if (k < 4) bs_e = fmaf(yf - MAGIC, rk[k], bs_e);
-                        else bs_o = fmaf(yf - MAGIC, rk[k], bs_o);
+                        bsum = fmaf(qr[hg][k], bk[k], bsum);
                         y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
                     }
-                    const float bs = row_sum(fmaf(bs_o, MUL, bs_e));
+                    const float bs = row_sum(bsum);
                     uint32_t d0, d1, d2, e0, e1, e2;
                     digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
                     digits4(y[4], y[5], y[6], y[7], e0, e1, e2);
@@ -1086,15 +1085,14 @@ void k_decode4(DecodeArgs a) {
                     // 2 (l % 8) + {0, 1} of that group (an even dword when (l / 2) % 2 == 0);
                     // grid, digits and beta as for the head groups, over the whole wave
                     const float2 a2 = *reinterpret_cast<const float2*>(&sm.aux[0][2 * l]);
-                    const float2 r2 = *reinterpret_cast<const float2*>(&sm.aux[1][2 * l]);
+                    const float2 b2 = *reinterpret_cast<const float2*>(&sm.aux[1][2 * l]);
                     const float qt0 = qr4[0] * a2.x, qt1 = qr4[1] * a2.y;
                     const float mx = wave_max_nonneg(fmaxf(fabsf(qt0), fabsf(qt1)));
                     const float sc = mx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(mx) : 0.f;
                     const bool even = ((l >> 1) & 1) == 0;
                     const float y0f = fmaf(qt0, even ? sc * MUL : sc, MAGIC);
                     const float y1f = fmaf(qt1, even ? sc * MUL : sc, MAGIC);
-                    const float bsl = fmaf(y1f - MAGIC, r2.y, (y0f - MAGIC) * r2.x);
-                    const float bs = wave_sum(even ? bsl : bsl * MUL);
+                    const float bs = wave_sum(fmaf(qr4[1], b2.y, qr4[0] * b2.x));
                     const uint32_t y0 = __float_as_uint(y0f) + (0x808080u - MAGIC_BITS);
                     const uint32_t y1 = __float_as_uint(y1f) + (0x808080u - MAGIC_BITS);
                     const uint32_t d01 = perm(y1, y0, 0x05010400u) ^ 0x80808080u;  // digit 0 | digit 1 pairs
@@ -1115,7 +1113,7 @@ void k_decode4(DecodeArgs a) {
             // inner: the code planes of a token block are extracted once and used at once.
             float lg[NH][8];
             v4i aq[NH][2];
-            float bq[NH], fqs[NH];  // beta and the grid step in logit units (log2, scaled)
+            float bq[NH], fqs[NH];  // beta and the q~ grid step in logit units (log2, scaled)
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
 #pragma unroll
@@ -1125,7 +1123,7 @@ void k_decode4(DecodeArgs a) {
                     aq[hg][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
                 fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
-                bq[hg] = sm.hv[4 * hg + G][0] * fqs[hg];
+                bq[hg] = sm.hv[4 * hg + G][0] * a.scale_log2;
             }
             // X1: accumulator 3 holds the extra head's digit-G partial (row group 3: zero)
             uint32_t x4[2][4];
@@ -1141,15 +1139,15 @@ void k_decode4(DecodeArgs a) {
                         v4i c = mfma_i8(aq[hg][0], b0, v4i{0, 0, 0, 0});
                         c = mfma_i8(aq[hg][1], b1, c);
                         lg[hg][4 * sg + tau] = fmaf((float)digit_sum(c), fqs[hg], bq[hg]) * s2k;
-                        if (X1 && hg == 0) x4[sg][tau] = (uint32_t)c[3] << (8 * G);
+                        if (X1 && hg == 0) x4[sg][tau] = (uint32_t)c[3];
                     }
                 }
             float lg4[2] = {0.f, 0.f};  // extra head, tokens 64 sg + 16 G + n
             if constexpr (X1) {
-                const float fqs4 = sm.hv[NHX - 1][1] * a.scale_log2, bq4 = sm.hv[NHX - 1][0] * fqs4;
+                const float fqs4 = sm.hv[NHX - 1][1] * a.scale_log2, bq4 = sm.hv[NHX - 1][0] * a.scale_log2;
 #pragma unroll
                 for (int sg = 0; sg < 2; ++sg) {
-                    const uint32_t raw = rows_reduce_scatter4(x4[sg][0], x4[sg][1], x4[sg][2], x4[sg][3]);
+                    const uint32_t raw = rows_digit_reduce_scatter4(x4[sg][0], x4[sg][1], x4[sg][2], x4[sg][3]);
                     lg4[sg] = fmaf((float)(int)raw, fqs4, bq4) * sm.aux[2][64 * sg + 16 * G + n];
                 }
             }
@@ -1162,43 +1160,43 @@ void k_decode4(DecodeArgs a) {
             uint32_t t4[2] = {0u, 0u};
             if constexpr (X1) {
                 alpha4 = softmax_wave(lg4, false, m4, l4);
+                // the offsets' part of the output: sum over tokens of p * b_V
+                gam4 = wave_sum(fmaf(lg4[1], sm.aux[4][64 + 16 * G + n], lg4[0] * sm.aux[4][16 * G + n]));
                 lg4[0] *= sm.aux[3][16 * G + n];
                 lg4[1] *= sm.aux[3][64 + 16 * G + n];
                 const float pmx = wave_max_nonneg(fmaxf(lg4[0], lg4[1]));
                 const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
                 const float ps = (G & 1) ? psc : psc * MUL;
-                float gl = 0.f;
 #pragma unroll
                 for (int sg = 0; sg < 2; ++sg) {
                     const float yf = fmaf(lg4[sg], ps, MAGIC);
-                    gl = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * G + n], gl);
                     t4[sg] = quad_transpose_bytes(__float_as_uint(yf) + (0x80808080u - MAGIC_BITS), j);
                 }
                 fp4 = pmx * (1.0f / (MUL * (float)QMAX));
-                gam4 = wave_sum((G & 1) ? gl * MUL : gl) * fp4;
             }
             v4i ap[NH][2];
             float alpha[NH], gam[NH], fp[NH];  // gam: the offset term in output units
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
                 alpha[hg] = softmax_update(lg[hg], false, m_run[hg], l_run[hg]);
-                float pmx = 0.f;
+                // the offsets' part of the output, sum over tokens of p * b_V; then p * a_V, the
+                // real-valued side of the code products
+                float pmx = 0.f, gsum = 0.f;
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
-                    lg[hg][k] *= sm.aux[3][64 * (k >> 2) + 16 * (k & 3) + n];
+                    const int tok = 64 * (k >> 2) + 16 * (k & 3) + n;
+                    gsum = fmaf(lg[hg][k], sm.aux[4][tok], gsum);
+                    lg[hg][k] *= sm.aux[3][tok];
                     pmx = fmaxf(pmx, lg[hg][k]);
                 }
                 pmx = row_max_nonneg(pmx);
                 const float psc = pmx > kTinyMax ? (float)QMAX * __builtin_amdgcn_rcpf(pmx) : 0.f;
-                float gam_e = 0.f, gam_o = 0.f;
 #pragma unroll
                 for (int sg = 0; sg < 2; ++sg) {
                     uint32_t D[4];
 #pragma unroll
                     for (int tau = 0; tau < 4; ++tau) {
                         const float yf = fmaf(lg[hg][4 * sg + tau], (tau & 1) ? psc : psc * MUL, MAGIC);
-                        if (tau & 1) gam_o = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_o);
-                        else gam_e = fmaf(yf - MAGIC, sm.aux[4][64 * sg + 16 * tau + n], gam_e);
                         const uint32_t y = __float_as_uint(yf) + (0x80808080u - MAGIC_BITS);
                         const uint32_t t = quad_transpose_bytes(y, j);
                         uint32_t d = (uint32_t)__builtin_amdgcn_ds_bpermute(perm_addr, (int)t);
@@ -1211,7 +1209,7 @@ void k_decode4(DecodeArgs a) {
                     ap[hg][sg] = v4i{(int)D[0], (int)D[1], (int)D[2], (int)D[3]};
                 }
                 fp[hg] = pmx * (1.0f / (MUL * (float)QMAX));
-                gam[hg] = row_sum(fmaf(gam_o, MUL, gam_e)) * fp[hg];
+                gam[hg] = row_sum(gsum);
             }
             uint32_t x5[8];  // X1: accumulator 3, the extra head's digit-G partial of channel block mt
 #pragma unroll
@@ -1224,13 +1222,13 @@ void k_decode4(DecodeArgs a) {
                     v4i acc = mfma_i8(ap[hg][0], v0, v4i{0, 0, 0, 0});
                     acc = mfma_i8(ap[hg][1], v1, acc);
                     orot[hg][mt] = fmaf(fmaf((float)digit_sum(acc), fp[hg], gam[hg]), s2v, orot[hg][mt] * alpha[hg]);
-                    if (X1 && hg == 0) x5[mt] = (uint32_t)acc[3] << (8 * G);
+                    if (X1 && hg == 0) x5[mt] = (uint32_t)acc[3];
                 }
             }
             if constexpr (X1) {
 #pragma unroll
                 for (int q = 0; q < 2; ++q) {
-                    const uint32_t raw = rows_reduce_scatter4(x5[4 * q], x5[4 * q + 1], x5[4 * q + 2], x5[4 * q + 3]);
+                    const uint32_t raw = rows_digit_reduce_scatter4(x5[4 * q], x5[4 * q + 1], x5[4 * q + 2], x5[4 * q + 3]);
                     orot4[q] = fmaf(fmaf((float)(int)raw, fp4, gam4), sm.aux[5][16 * (4 * q + G) + n], orot4[q] * alpha4);
                 }
             }
