@@ -825,11 +825,17 @@ template <int NH, int X1>
 struct Smem4 {
     float q[4 * NH + X1][kD];       // rotated q (rows >= g zero); reused for the inverse rotation of the output
     float aux[6][kD];               // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
-    uint4 qp[NH][4][2][4][4];       // q~ digit planes [group][digit slot][kappa][G][head]; slot 3 stays zero
+    uint4 qp[NH][4][2][16];         // q~ digit planes [group][digit slot][kappa][qslot(slot, G, head)]; slot 3 stays zero
     uint4 qp4[X1 ? 4 : 1][2][4];    // X1: the extra head's q~ digit planes [digit slot][kappa][G]; slot 3 zero
     float hv[4 * NH + X1][4];       // per head: beta, q~ step, alpha, l
     float p[4 * NH + X1][kG];       // probabilities of a bf16 chunk (sink / residual)
 };
+
+// Position of the 16-byte piece (K group G, head h) in a digit slot's row of the q~ planes.  The
+// QK operand read has lane (G, 4h + j) fetch piece (G, h) of slot j; the slot-dependent swizzle
+// gives the 16 lanes of a row 16 different bank groups (unswizzled, the four slots of one (G, h)
+// share a bank group).
+__device__ __forceinline__ int qslot(int slot, int G, int h) { return (4 * G + h) ^ (4 * slot); }
 
 // Max and sum over the whole wave (the four DPP rows, then row pairs): every lane ends with
 // the same value.
@@ -999,7 +1005,7 @@ void k_decode4(DecodeArgs a) {
 
         q_to_lds<NHX>(sm.q, a, qrow, g, l);
         for (int idx = l; idx < NH * 32; idx += 64)
-            sm.qp[idx >> 5][3][(idx >> 4) & 1][(idx >> 2) & 3][idx & 3] = make_uint4(0u, 0u, 0u, 0u);
+            sm.qp[idx >> 5][3][(idx >> 4) & 1][idx & 15] = make_uint4(0u, 0u, 0u, 0u);
         if (X1 && l < 8) sm.qp4[X1 ? 3 : 0][l >> 2][l & 3] = make_uint4(0u, 0u, 0u, 0u);
         __syncthreads();
         if (a.rotate) lds_hadamard<NHX>(sm.q, g);
@@ -1072,9 +1078,9 @@ void k_decode4(DecodeArgs a) {
                     uint32_t d0, d1, d2, e0, e1, e2;
                     digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
                     digits4(y[4], y[5], y[6], y[7], e0, e1, e2);
-                    reinterpret_cast<uint2*>(&sm.qp[hg][0][kap][Gq][G])[half] = make_uint2(d0, e0);
-                    reinterpret_cast<uint2*>(&sm.qp[hg][1][kap][Gq][G])[half] = make_uint2(d1, e1);
-                    reinterpret_cast<uint2*>(&sm.qp[hg][2][kap][Gq][G])[half] = make_uint2(d2, e2);
+                    reinterpret_cast<uint2*>(&sm.qp[hg][0][kap][qslot(0, Gq, G)])[half] = make_uint2(d0, e0);
+                    reinterpret_cast<uint2*>(&sm.qp[hg][1][kap][qslot(1, Gq, G)])[half] = make_uint2(d1, e1);
+                    reinterpret_cast<uint2*>(&sm.qp[hg][2][kap][qslot(2, Gq, G)])[half] = make_uint2(d2, e2);
                     if (n == 0) {
                         sm.hv[4 * hg + G][0] = bs;
                         sm.hv[4 * hg + G][1] = mx * (1.0f / (MUL * (float)QMAX));
@@ -1119,7 +1125,7 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
                 for (int kap = 0; kap < 2; ++kap) {
                     // X1: rows 3, 7, 11 (slot 3 of heads 0-2) take the extra head's digits 0-2
-                    const uint4 u = X1 && j == 3 && h < 3 ? sm.qp4[X1 ? h : 0][kap][G] : sm.qp[hg][j][kap][G][h];
+                    const uint4 u = X1 && j == 3 && h < 3 ? sm.qp4[X1 ? h : 0][kap][G] : sm.qp[hg][j][kap][qslot(j, G, h)];
                     aq[hg][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
                 fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
