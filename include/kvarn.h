@@ -113,7 +113,8 @@ typedef enum { KVARN_AUX_F32 = 0, KVARN_AUX_COMPACT = 1 } kvarn_aux_format;
  * variance inside the normal fp32 range. */
 
 /* The cache of `batch` sequences with n_kv kv heads each (a model's layers may be folded
- * into batch).  Device buffers, all caller-allocated (sizes from kvarn_cache_sizes):
+ * into batch; batch * n_kv at most 2^26, else KVARN_EINVAL).  Device buffers, all
+ * caller-allocated (sizes from kvarn_cache_sizes):
  *   k_body, v_body   [batch][n_kv][max_blocks] packed tiles of kvarn_tile_bytes(p)
  *   k_resid, v_resid [batch][n_kv][128][128]    bf16, tokens as given (unrotated)
  *   k_sink, v_sink   [batch][n_kv][n_sink][128] bf16, or NULL when n_sink == 0

@@ -60,6 +60,8 @@ QParams qparams(const kvarn_params* p) {
 int check_cache(const kvarn_params* p, const kvarn_cache* c) {
     if (!c) return KVARN_EINVAL;
     if (c->batch <= 0 || c->n_kv <= 0 || c->max_blocks < 0) return KVARN_EINVAL;
+    // kernels index (sequence, kv head, K|V) in 32 bits
+    if ((int64_t)c->batch * c->n_kv > kMaxStreams) return KVARN_EINVAL;
     if (!c->k_body || !c->v_body || !c->k_resid || !c->v_resid || !c->seq_len) return KVARN_EINVAL;
     if (p->n_sink > 0 && (!c->k_sink || !c->v_sink)) return KVARN_EINVAL;
     if (!aligned(c->k_body, 16) || !aligned(c->v_body, 16) || !aligned(c->k_resid, 16) || !aligned(c->v_resid, 16))
@@ -99,6 +101,7 @@ int kvarn_cache_sizes(const kvarn_params* p, int32_t batch, int32_t n_kv, int32_
     int st = check_params(p);
     if (st) return st;
     if (!sizes || batch <= 0 || n_kv <= 0 || max_blocks < 0) return KVARN_EINVAL;
+    if ((int64_t)batch * n_kv > kMaxStreams) return KVARN_EINVAL;
     const size_t streams = (size_t)batch * n_kv;
     sizes[0] = sizes[1] = streams * max_blocks * tile_bytes(p->bits, p->aux_format == KVARN_AUX_COMPACT);
     sizes[2] = sizes[3] = streams * kG * kD * sizeof(uint16_t);

@@ -10,6 +10,7 @@ namespace kvarn {
 
 constexpr int kD = 128;  // head_dim (channels per token)
 constexpr int kG = 128;  // tokens per quantization group / body tile
+constexpr int64_t kMaxStreams = int64_t(1) << 26;  // (sequence, kv head) pairs a cache may hold
 
 // 1/sqrt(128), rounded to fp32.
 constexpr float kInvSqrt128 = 0.08838834764831845f;

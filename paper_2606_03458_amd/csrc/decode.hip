@@ -1011,11 +1011,17 @@ void k_decode4(DecodeArgs a) {
         if (a.rotate) lds_hadamard<NHX>(sm.q, g);
         // q~ role: head 4*hg + G, channels 8n .. 8n + 7 (rotated and normalized, or as given)
         const float qs = a.rotate ? kInvSqrt128 : 1.f;
-        float qr[NH][8];
+        // two head groups: q stays in LDS (each lane scales, and later reads, only its own
+        // elements), which keeps 16 registers free for the tile loop
+        constexpr bool QLDS = NH == 2;
+        float qr[QLDS ? 1 : NH][8];
 #pragma unroll
         for (int hg = 0; hg < NH; ++hg)
 #pragma unroll
-            for (int k = 0; k < 8; ++k) qr[hg][k] = sm.q[4 * hg + G][8 * n + k] * qs;
+            for (int k = 0; k < 8; ++k) {
+                if constexpr (QLDS) sm.q[4 * hg + G][8 * n + k] *= qs;
+                else qr[hg][k] = sm.q[4 * hg + G][8 * n + k] * qs;
+            }
         // extra head: channels 2l, 2l + 1
         const float qr4[2] = {X1 ? sm.q[NHX - 1][2 * l] * qs : 0.f, X1 ? sm.q[NHX - 1][2 * l + 1] * qs : 0.f};
         // source lane of the PV operand permutation (see above), as a byte address; for the
@@ -1056,10 +1062,19 @@ void k_decode4(DecodeArgs a) {
                 const int kap = n >> 3, Gq = (n >> 1) & 3, half = n & 1;
 #pragma unroll
                 for (int hg = 0; hg < NH; ++hg) {
-                    float qt[8], mx = 0.f;
+                    float qv[8], qt[8], mx = 0.f;
+                    if constexpr (QLDS) {
+                        const float4 x0 = *reinterpret_cast<const float4*>(&sm.q[4 * hg + G][8 * n]);
+                        const float4 x1 = *reinterpret_cast<const float4*>(&sm.q[4 * hg + G][8 * n + 4]);
+                        qv[0] = x0.x; qv[1] = x0.y; qv[2] = x0.z; qv[3] = x0.w;
+                        qv[4] = x1.x; qv[5] = x1.y; qv[6] = x1.z; qv[7] = x1.w;
+                    } else {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) qv[k] = qr[QLDS ? 0 : hg][k];
+                    }
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        qt[k] = qr[hg][k] * av[k];
+                        qt[k] = qv[k] * av[k];
                         mx = fmaxf(mx, fabsf(qt[k]));
                     }
                     mx = row_max_nonneg(mx);
@@ -1071,7 +1086,7 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
                         const float yf = fmaf(qt[k], k < 4 ? sc * MUL : sc, MAGIC);
-                        bsum = fmaf(qr[hg][k], bk[k], bsum);
+                        bsum = fmaf(qv[k], bk[k], bsum);
                         y[k] = __float_as_uint(yf) + (0x808080u - MAGIC_BITS);
                     }
                     const float bs = row_sum(bsum);

@@ -715,18 +715,19 @@ template <bool COMPACT, bool EXACT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))) void k_flush(FlushArgs a) {
     __shared__ QuantSmem sm;
     __shared__ uint64_t due_mask[kThreads / 64];
-    const int64_t n = (int64_t)a.c.batch * a.c.n_kv * 2;
-    const int64_t step = gridDim.x;
+    // tile indices fit 32 bits: the host bounds batch * n_kv
+    const int n = a.c.batch * a.c.n_kv * 2;
+    const int step = (int)gridDim.x;
     // the body tile a due tile goes to, or -1 when it is not due (or the append refused it)
-    auto target_block = [&](int64_t t) -> int {
-        const int b = (int)((t >> 1) / a.c.n_kv);
+    auto target_block = [&](int t) -> int {
+        const int b = (t >> 1) / a.c.n_kv;
         const int len = a.c.seq_len[b];
         if (len <= a.n_sink || (len - a.n_sink) % kG != 0) return -1;
         const int nb = (len - a.n_sink) / kG - 1;
         return nb < a.c.max_blocks ? nb : -1;
     };
-    for (int64_t base = blockIdx.x; base < n; base += step * kThreads) {
-        const int64_t mine = base + (int64_t)threadIdx.x * step;
+    for (int base = (int)blockIdx.x; base < n; base += step * kThreads) {
+        const int mine = base + (int)threadIdx.x * step;
         const bool due = mine < n && target_block(mine) >= 0;
         const uint64_t m = __ballot(due);
         __syncthreads();  // the previous round is done with due_mask and the tile state in sm
@@ -739,11 +740,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3, 8))
             uint64_t mm = (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)dm) |
                           (uint64_t)__builtin_amdgcn_readfirstlane((uint32_t)(dm >> 32)) << 32;
             for (; mm; mm &= mm - 1) {
-                const int64_t t = base + (int64_t)(64 * w + __builtin_ctzll(mm)) * step;
-                const int kind = (int)(t & 1);
-                const int64_t stream = t >> 1;
-                const int b = (int)(stream / a.c.n_kv);
-                const int64_t ti = body_tile(a.c, b, (int)(stream % a.c.n_kv), target_block(t));
+                const int t = base + (64 * w + __builtin_ctzll(mm)) * step;
+                const int kind = t & 1;
+                const int stream = t >> 1;
+                const int b = stream / a.c.n_kv;
+                const int64_t ti = body_tile(a.c, b, stream % a.c.n_kv, target_block(t));
                 if (ti < 0) continue;
                 if (!first) __syncthreads();  // every thread is done with the previous tile's LDS
                 first = false;

@@ -53,6 +53,11 @@ def test_params_and_sizes(K):
     assert s == [3 * 8 * 10 * 5632] * 2 + [3 * 8 * 128 * 128 * 2] * 2 + [3 * 8 * 128 * 128 * 2] * 2 + [12]
     with pytest.raises(K.KVarNError):
         K.kvarn_cache_sizes(p, 0, 8, 10)
+    # at most 2^26 (sequence, kv head) pairs: the kernels index them in 32 bits
+    assert K.kvarn_cache_sizes(p, 1 << 13, 1 << 13, 0)[6] == 4 << 13
+    with pytest.raises(K.KVarNError) as e:
+        K.kvarn_cache_sizes(p, (1 << 13) + 1, 1 << 13, 0)
+    assert e.value.status == -1
 
 
 def _fake(n, align=256):
@@ -136,6 +141,10 @@ def test_append_validation(K):
     p.n_sink = 128
     with pytest.raises(K.KVarNError) as e:  # sink buffers required when n_sink > 0
         K.kvarn_append_token(p, c, tok, tok, 1, 0, stream=0)
+    assert e.value.status == -1
+    big = _HostCache(K, batch=(1 << 13) + 1, n_kv=1 << 13)
+    with pytest.raises(K.KVarNError) as e:  # more (sequence, kv head) pairs than the kernels index
+        K.kvarn_append_token(K.kvarn_params_init(2), big, tok, tok, 1, 0, stream=0)
     assert e.value.status == -1
 
 
