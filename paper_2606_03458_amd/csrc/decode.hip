@@ -9,18 +9,20 @@
 // The two sums over codes are matrix products on the int8 matrix cores
 // (v_mfma_i32_16x16x64_i8).  The codes are exact int8 operands taken straight from the packed
 // words (the tile format stores them in the MFMA register order).  The real-valued side is
-// written as a fixed-point integer split into signed base-256 digits, one MFMA per digit,
-// recombined exactly in int32: q~ uses three digits (22 bits at 2-bit codes, 20 at 4-bit),
-// p~ two (15 bits).  Integer accumulation is exact, so the only rounding is that of q~ and p~
-// to their fixed-point grids.  beta and gamma are formed from the same rounded integers (with
-// the per-element offset ratios b / a), so code term and offset term of every dequantized
-// value carry identical weights and the rounding cannot leave a common-mode offset behind.
+// written as a fixed-point integer split into signed base-256 digits, recombined exactly in
+// int32.  Integer accumulation is exact, so the only rounding in the code terms is that of q~
+// and p~ to their fixed-point grids.
 //
-// Layout per wave (64 lanes, lane = 16*G + n): QK computes S^T = codes x q~^T with rows =
-// 16 tokens and columns = query heads of the kv head's group, so lane (G, n) receives tokens
-// 16*tau + 4*G + i of head n.  Those are exactly the K-slice of lane (G, n) in the PV product
-// O^T = codes_V^T x p~^T, so probabilities never leave their lane between the two products.
-// Columns n >= g (the group size) carry unused values.
+// Two kernel families.  k_decode (group sizes 9-16): one MFMA per digit; q~ uses three digits
+// (22 bits at 2-bit codes, 20 at 4-bit), p~ two (15 bits); beta and gamma are formed from the
+// same rounded integers (with the per-element offset ratios b / a).  Layout per wave (64 lanes,
+// lane = 16*G + n): QK computes S^T = codes x q~^T with rows = 16 tokens and columns = query
+// heads of the kv head's group, so lane (G, n) receives tokens 16*tau + 4*G + i of head n.
+// Those are exactly the K-slice of lane (G, n) in the PV product O^T = codes_V^T x p~^T, so
+// probabilities never leave their lane between the two products.  Columns n >= g (the group
+// size) carry unused values.  k_decode4 (group sizes up to 8, below): the digits of a head are
+// rows of one MFMA operand (three digits for both q~ and p~), and beta, gamma are plain fp32
+// dot products of the unrounded q_rot and p with the offsets.
 //
 // Sink and residual tokens (bf16, unrotated) use the bf16 matrix cores for q . k (q as a bf16
 // pair hi + lo when it is fp32) and plain FMAs for p . v.  One wave owns a (split, sequence,
@@ -824,7 +826,7 @@ constexpr float kPlaneMul = BITS == 2 ? 4.f : 1.f;
 template <int NH, int X1>
 struct Smem4 {
     float q[4 * NH + X1][kD];       // rotated q (rows >= g zero); reused for the inverse rotation of the output
-    float aux[6][kD];               // a_K b_K s2_K a_V b_V s2_V of the current tile (b becomes b / a)
+    float aux[6][kD];               // a_K b_K s2_K a_V b_V s2_V of the current tile
     uint4 qp[NH][4][2][16];         // q~ digit planes [group][digit slot][kappa][qslot(slot, G, head)]; slot 3 stays zero
     uint4 qp4[X1 ? 4 : 1][2][4];    // X1: the extra head's q~ digit planes [digit slot][kappa][G]; slot 3 zero
     float hv[4 * NH + X1][4];       // per head: beta, q~ step, alpha, l
