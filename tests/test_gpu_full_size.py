@@ -140,6 +140,12 @@ def test_full_size_stress(K):
     _run(K, "stress", n_append=130, n_streams=64, n_tiles=12, out_dtype=torch.float32)
 
 
+def test_full_size_gqa8(K):
+    """Query groups of 8 (64 q / 8 kv heads, two head groups per wave), batch 128, 16384-token
+    2-bit cache."""
+    _run(K, "gqa8", n_append=130, n_streams=64, n_tiles=12, out_dtype=torch.bfloat16)
+
+
 def test_full_size_throughput_compact(K):
     """The throughput workload with the compact aux format (2.25 bits/element)."""
     _run(K, "throughput", n_append=130, n_streams=64, n_tiles=12, out_dtype=torch.bfloat16, aux=1)
