@@ -13,20 +13,15 @@
 // int32.  Integer accumulation is exact, so the only rounding in the code terms is that of q~
 // and p~ to their fixed-point grids.
 //
-// Two kernel families.  k_decode (group sizes 9-16): one MFMA per digit; q~ uses three digits
-// (22 bits at 2-bit codes, 20 at 4-bit), p~ two (15 bits); beta and gamma are formed from the
-// same rounded integers (with the per-element offset ratios b / a).  Layout per wave (64 lanes,
-// lane = 16*G + n): QK computes S^T = codes x q~^T with rows = 16 tokens and columns = query
-// heads of the kv head's group, so lane (G, n) receives tokens 16*tau + 4*G + i of head n.
-// Those are exactly the K-slice of lane (G, n) in the PV product O^T = codes_V^T x p~^T, so
-// probabilities never leave their lane between the two products.  Columns n >= g (the group
-// size) carry unused values.  k_decode4 (group sizes up to 8, below): the digits of a head are
-// rows of one MFMA operand (three digits for both q~ and p~), and beta, gamma are plain fp32
-// dot products of the unrounded q_rot and p with the offsets.
+// The digits of a head are rows of one MFMA operand (three digits for both q~ and p~: 22 bits
+// at 2-bit codes, 20 at 4-bit), and beta, gamma are plain fp32 dot products of the unrounded
+// q_rot and p with the offsets.  A wave takes up to eight query heads of a kv head's group (one
+// or two head groups of four, or four plus a fifth carried in the empty digit slots); larger
+// groups are taken in chunks of at most eight heads, one wave per chunk.
 //
 // Sink and residual tokens (bf16, unrotated) use the bf16 matrix cores for q . k (q as a bf16
 // pair hi + lo when it is fp32) and plain FMAs for p . v.  One wave owns a (split, sequence,
-// kv head); the last split also takes sink + residual (or only those when the stream is split:
+// kv head, head chunk); the last split also takes sink + residual (or only those when the stream is split:
 // then they run beside the body splits instead of after one of them).  A single split writes the final
 // output directly (inverse rotation in LDS); several splits write partials that the merge
 // kernel combines by log-sum-exp.
@@ -70,6 +65,8 @@ struct DecodeArgs {
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
     int n_split, bps;  // splits per stream and body tiles per body split
     int res_split;     // 1: the last split holds only sink + residual (n_split - 1 body splits)
+    int n_streams;     // batch * n_kv
+    int n_chunk, g_chunk;  // head chunks per stream and heads per chunk (row-digit kernels)
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
 };
 
@@ -99,11 +96,9 @@ __device__ __forceinline__ v4i unit_i8(const uint32_t* w) {
 // Max in the NaN-propagating form: no operand of the reductions here is a NaN, and fmaxf would
 // first quiet every operand that comes from another lane (one more instruction per step).
 __device__ __forceinline__ float fmax_any(float x, float y) { return __builtin_elementwise_maximum(x, y); }
-__device__ __forceinline__ float xor_max(float v, int m) { return fmax_any(v, __shfl_xor(v, m)); }
-__device__ __forceinline__ float xor_sum(float v, int m) { return v + __shfl_xor(v, m); }
 
-// Four values y0..y3, each a fixed-point integer plus 0x808080 (0x8080 for two digits), to
-// one dword per digit k whose byte i is the signed digit k of value i ((byte k of y_i) ^ 0x80).
+// Four values y0..y3, each a fixed-point integer plus 0x808080, to one dword per digit k whose
+// byte i is the signed digit k of value i ((byte k of y_i) ^ 0x80).
 __device__ __forceinline__ void digits4(uint32_t y0, uint32_t y1, uint32_t y2, uint32_t y3, uint32_t& d0,
                                         uint32_t& d1, uint32_t& d2) {
     const uint32_t t01 = perm(y1, y0, 0x05010400u), t23 = perm(y3, y2, 0x05010400u);
@@ -111,12 +106,6 @@ __device__ __forceinline__ void digits4(uint32_t y0, uint32_t y1, uint32_t y2, u
     d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
     const uint32_t u01 = perm(y1, y0, 0x0c0c0602u), u23 = perm(y3, y2, 0x0c0c0602u);
     d2 = perm(u23, u01, 0x05040100u) ^ 0x80808080u;
-}
-__device__ __forceinline__ void digits4_2(uint32_t y0, uint32_t y1, uint32_t y2, uint32_t y3, uint32_t& d0,
-                                          uint32_t& d1) {
-    const uint32_t t01 = perm(y1, y0, 0x05010400u), t23 = perm(y3, y2, 0x05010400u);
-    d0 = perm(t23, t01, 0x05040100u) ^ 0x80808080u;
-    d1 = perm(t23, t01, 0x07060302u) ^ 0x80808080u;
 }
 
 // Body tiles are read once per decode step: non-temporal 16-byte loads stream them from HBM
@@ -126,14 +115,8 @@ __device__ __forceinline__ uint4 load_stream(const uint8_t* p) {
 }
 
 // Body tile addressing.  Dense bodies: tile blk of a stream at stream * max_blocks + blk.
-// Paged bodies: tile kvh of pool block block_table[b][blk].  block_id gives what tile_index
-// takes: the block index (dense) or the pool block id (paged).
-__device__ __forceinline__ int block_id(const DecodeArgs& a, int b, int blk) {
-    return a.block_table ? a.block_table[(size_t)b * a.max_blocks + blk] : blk;
-}
-__device__ __forceinline__ size_t tile_index(const DecodeArgs& a, int stream, int kvh, int id) {
-    return a.block_table ? (size_t)id * a.n_kv + kvh : (size_t)stream * a.max_blocks + id;
-}
+// Paged bodies: tile kvh of pool block block_table[b][blk].  block_id_t gives the block index
+// (dense) or the pool block id (paged) of the stream's body tile blk.
 template <int PG>
 __device__ __forceinline__ int block_id_t(const DecodeArgs& a, int b, int blk) {
     if constexpr (PG) return a.block_table[(size_t)b * a.max_blocks + blk];
@@ -151,57 +134,6 @@ __device__ __forceinline__ bool body_ids_ok(const DecodeArgs& a, int b, int blk0
     if (!__any(bad)) return true;
     if (l == 0 && a.err_word) __hip_atomic_fetch_or(a.err_word, 2u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     return false;
-}
-
-// The aux of one K tile and one V tile, as loaded by a wave: fp32 aux is 3 KB, three 16-byte
-// pieces per lane (pieces l, l + 64, l + 128 of K aux || V aux); compact aux is 1 KB, one piece
-// per lane (lanes 0-31 the K tile's 512 bytes, lanes 32-63 the V tile's).
-struct AuxRegs {
-    uint4 p0, p1, p2;
-};
-template <int CMP>
-__device__ __forceinline__ void load_aux_regs(AuxRegs& r, const uint8_t* kt, const uint8_t* vt, size_t cb, int l) {
-    if constexpr (CMP) {
-        r.p0 = load_stream((l < 32 ? kt : vt) + cb + (l & 31) * 16);
-        r.p1 = r.p2 = make_uint4(0u, 0u, 0u, 0u);  // unused
-    } else {
-        r.p0 = load_stream(kt + cb + l * 16);
-        r.p1 = load_stream((l < 32 ? kt : vt) + cb + (l < 32 ? (64 + l) * 16 : (l - 32) * 16));
-        r.p2 = load_stream(vt + cb + (32 + l) * 16);
-    }
-}
-// Loaded aux -> fp32 rows a_K b_K s2_K a_V b_V s2_V in LDS.  A compact piece is 8 binary16
-// offsets (pieces 0-15 of a tile) or 16 E4M3 scales (pieces 16-23: a, 24-31: s2); both
-// conversions are exact.
-template <int CMP>
-__device__ __forceinline__ void stage_aux(float (&aux)[6][kD], const AuxRegs& r, int l) {
-    if constexpr (!CMP) {
-        reinterpret_cast<uint4*>(&aux[0][0])[l] = r.p0;
-        reinterpret_cast<uint4*>(&aux[0][0])[l + 64] = r.p1;
-        reinterpret_cast<uint4*>(&aux[0][0])[l + 128] = r.p2;
-        return;
-    }
-    const int part = l >> 5, p = l & 31;
-    const uint32_t w[4] = {r.p0.x, r.p0.y, r.p0.z, r.p0.w};
-    if (p < 16) {
-        float v[8];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            v[2 * k] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] & 0xFFFFu));
-            v[2 * k + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[k] >> 16));
-        }
-        float4* row = reinterpret_cast<float4*>(&aux[3 * part + 1][8 * p]);
-        row[0] = make_float4(v[0], v[1], v[2], v[3]);
-        row[1] = make_float4(v[4], v[5], v[6], v[7]);
-    } else {
-        float4* row = reinterpret_cast<float4*>(&aux[3 * part + (p < 24 ? 0 : 2)][16 * ((p - 16) & 7)]);
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const auto lo = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[k], false);  // bytes 0, 1
-            const auto hi = __builtin_amdgcn_cvt_pk_f32_fp8((int)w[k], true);   // bytes 2, 3
-            row[k] = make_float4(lo[0], lo[1], hi[0], hi[1]);
-        }
-    }
 }
 
 // The aux of one K tile and one V tile as loaded for the row-digit kernels: lane l holds entries
@@ -257,15 +189,6 @@ __device__ __forceinline__ void stage_half_aux(float (&aux)[6][kD], int r0, cons
     *reinterpret_cast<float2*>(&aux[r0 + 1][2 * l]) = make_float2(b0, b1);
     *reinterpret_cast<float2*>(&aux[r0 + 2][2 * l]) = make_float2(s0, s1);
 }
-
-template <int GQ>
-struct Smem {
-    float q[GQ][kD];        // rotated q; reused for the inverse rotation of the output
-    float aux[6][kD];       // a_K b_K s2_K a_V b_V s2_V of the current tile
-    uint4 qp[3][2][4][GQ];  // q~ digits in B-operand order [digit][kappa][G][head]
-    float hv[GQ][4];        // per head: beta, q~ step, alpha, l
-    float p[GQ][kG];        // probabilities of a bf16 chunk (sink / residual)
-};
 
 // LDS butterflies (stride 1..64) over rows [0, g) of x; 64 threads.  Unnormalized.
 template <int GQ>
@@ -359,385 +282,6 @@ __device__ __forceinline__ void pv_plain(float (&oplain)[NHS][2], const float (&
                     oplain[hh][0] = fmaf(pv[i], __uint_as_float(v2[u + i] << 16), oplain[hh][0]);
                     oplain[hh][1] = fmaf(pv[i], __uint_as_float(v2[u + i] & 0xFFFF0000u), oplain[hh][1]);
                 }
-            }
-        }
-    }
-}
-
-template <int BITS, int GQ, int CMP>
-__global__ __launch_bounds__(64) void k_decode(DecodeArgs a) {
-    __shared__ Smem<GQ> sm;
-    constexpr int WPU = BITS / 2;                        // words per 16-code unit
-    constexpr int QMAX = BITS == 2 ? 4194303 : 1048575;  // |q~ fixed point| < 2^22 (2^20)
-    // p~ fixed point in [0, 32639]: the largest value whose two balanced base-256 digits
-    // (x + 0x8080 split into bytes, each minus 128) stay in range
-    constexpr float PMAX = 32639.f;
-    const int l = threadIdx.x, G = l >> 4, n = l & 15;
-    const int g = a.g;
-    const bool head_lane = n < g;
-    const int hn = n < GQ ? n : GQ - 1;
-    const int split = blockIdx.x % a.n_split;
-    const int stream = blockIdx.x / a.n_split;
-    const int b = stream / a.n_kv, kvh = stream % a.n_kv;
-    const int len = max(a.seq_len[b], 0);
-    const int ns = min(len, a.n_sink);
-    const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
-    const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
-    // the last split attends sink + residual; with res_split it holds nothing else
-    const bool last = split == a.n_split - 1;
-    const bool res_only = a.res_split && last;
-    const bool body_last = split == a.n_split - 1 - a.res_split;  // takes any excess of body tiles
-    const int blk0 = res_only ? 0 : split * a.bps;
-    int blk1 = res_only ? 0 : (body_last ? nbody : min(blk0 + a.bps, nbody));
-    if (blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
-    const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;    // first query head of the group
-    const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
-
-    float m_run = -INFINITY, l_run = 0.f;  // per head n; l_run is this lane's partial sum
-    float orot[8][4];                      // head n, channel 16*mt + 4*G + i (rotated domain)
-    float oplain[GQ][2];                   // head h, channel 2*l + j (unrotated)
-#pragma unroll
-    for (int mt = 0; mt < 8; ++mt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) orot[mt][i] = 0.f;
-#pragma unroll
-    for (int h = 0; h < GQ; ++h) oplain[h][0] = oplain[h][1] = 0.f;
-
-    // Online-softmax step shared by body tiles and bf16 chunks: lg holds 32 logits of head n
-    // (log2 units, -inf for absent tokens); turns lg into p and returns the rescale factor.
-    auto softmax_update = [&](float (&lg)[32]) -> float {
-        float mx = lg[0];
-#pragma unroll
-        for (int k = 1; k < 32; ++k) mx = fmaxf(mx, lg[k]);
-        mx = xor_max(xor_max(mx, 16), 32);
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = m_run == -INFINITY ? 0.f : exp2f(m_run - m_new);
-        float s = 0.f;
-#pragma unroll
-        for (int k = 0; k < 32; ++k) {
-            lg[k] = lg[k] == -INFINITY ? 0.f : exp2f(lg[k] - m_new);
-            s += lg[k];
-        }
-        l_run = l_run * alpha + s;
-        m_run = m_new;
-        return alpha;
-    };
-
-    if (blk0 < blk1) {
-        // Lane l's part of a tile: its K and V code units (32*WPU bytes per 64-token half) and
-        // its pieces of the aux.  The first tile's loads go out before the query set-up; the
-        // prefetch of the next tile is unconditional (past the last tile it re-reads it) so that
-        // no load sits behind a branch.
-        uint4 kc[2][2 * WPU], vc[2][2 * WPU];
-        AuxRegs ar;
-        auto load_tile = [&](int blk) {
-            const size_t ti = tile_index(a, stream, kvh, block_id(a, b, blk));
-            const uint8_t* kt = a.k_body + ti * tb;
-            const uint8_t* vt = a.v_body + ti * tb;
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) {
-                    kc[s][k] = load_stream(kt + 16 * (s * 128 * WPU + 64 * k + l));
-                    vc[s][k] = load_stream(vt + 16 * (s * 128 * WPU + 64 * k + l));
-                }
-            load_aux_regs<CMP>(ar, kt, vt, cb, l);
-        };
-        load_tile(blk0);
-
-        q_to_lds<GQ>(sm.q, a, qrow, g, l);
-        __syncthreads();
-        if (a.rotate) {
-            lds_hadamard<GQ>(sm.q, g);
-            for (int idx = l; idx < g * kD; idx += 64) sm.q[idx >> 7][idx & 127] *= kInvSqrt128;
-        }
-
-        for (int blk = blk0; blk < blk1; ++blk) {
-            __syncthreads();  // the previous tile is done with sm.aux / sm.qp
-            stage_aux<CMP>(sm.aux, ar, l);
-            uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
-#pragma unroll
-            for (int s = 0; s < 2; ++s)
-#pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) {
-                    kw[s][4 * k] = kc[s][k].x; kw[s][4 * k + 1] = kc[s][k].y;
-                    kw[s][4 * k + 2] = kc[s][k].z; kw[s][4 * k + 3] = kc[s][k].w;
-                    vw[s][4 * k] = vc[s][k].x; vw[s][4 * k + 1] = vc[s][k].y;
-                    vw[s][4 * k + 2] = vc[s][k].z; vw[s][4 * k + 3] = vc[s][k].w;
-                }
-            load_tile(min(blk + 1, blk1 - 1));  // prefetch, consumed next iteration
-            __syncthreads();
-            // value offsets as ratios b_V / a_V (read after the next barrier)
-            sm.aux[4][2 * l] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l]);
-            sm.aux[4][2 * l + 1] *= __builtin_amdgcn_rcpf(sm.aux[3][2 * l + 1]);
-
-            // ---- q~ = q_rot * a_K as three base-256 digits, spread over all 64 lanes ----------
-            // group gi = (head, kappa, G', s) covers channels 64*kappa + 16*G' + 4*s .. +3
-            for (int gi0 = 0; gi0 < g * 32; gi0 += 64) {
-                const int gi = gi0 + l;
-                const bool valid = gi < g * 32;
-                const int h = min(gi >> 5, g - 1), rem = gi & 31;
-                const int kap = rem >> 4, Gp = (rem >> 2) & 3, s = rem & 3;
-                const int c0 = 64 * kap + 16 * Gp + 4 * s;
-                float qt[4], mx = 0.f;
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const float qv = valid ? sm.q[h][c0 + k] : 0.f;
-                    qt[k] = qv * sm.aux[0][c0 + k];
-                    mx = fmaxf(mx, fabsf(qt[k]));
-                }
-#pragma unroll
-                for (int m = 1; m < 32; m <<= 1) mx = xor_max(mx, m);
-                const float sc = mx > kTinyMax ? (float)QMAX / mx : 0.f;
-                // beta in q~ grid units: sum over channels of the rounded q~ times b_K / a_K
-                float bs = 0.f;
-                uint32_t y[4];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const int xi = __float2int_rn(qt[k] * sc);
-                    bs = fmaf((float)xi, sm.aux[1][c0 + k] * __builtin_amdgcn_rcpf(sm.aux[0][c0 + k]), bs);
-                    y[k] = (uint32_t)(xi + 0x808080);
-                }
-#pragma unroll
-                for (int m = 1; m < 32; m <<= 1) bs = xor_sum(bs, m);
-                uint32_t d0, d1, d2;
-                digits4(y[0], y[1], y[2], y[3], d0, d1, d2);
-                if (valid) {
-                    reinterpret_cast<uint32_t*>(&sm.qp[0][kap][Gp][h])[s] = d0;
-                    reinterpret_cast<uint32_t*>(&sm.qp[1][kap][Gp][h])[s] = d1;
-                    reinterpret_cast<uint32_t*>(&sm.qp[2][kap][Gp][h])[s] = d2;
-                    if ((l & 31) == 0) {
-                        sm.hv[h][0] = bs;
-                        sm.hv[h][1] = mx / (float)QMAX;
-                    }
-                }
-            }
-            __syncthreads();
-            v4i bq[3][2];
-#pragma unroll
-            for (int d = 0; d < 3; ++d)
-#pragma unroll
-                for (int kap = 0; kap < 2; ++kap) {
-                    const uint4 u = sm.qp[d][kap][G][hn];
-                    bq[d][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
-                }
-            const float beta = head_lane ? sm.hv[hn][0] : 0.f;  // in q~ grid units
-            const float fq = head_lane ? sm.hv[hn][1] : 0.f;    // q~ grid step
-
-            // ---- logits: S^T = codes x q~^T, token 64*sg + 16*tau + 4*G + i -------------------
-            float lg[32];
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau) {
-                    v4i c0 = {0, 0, 0, 0}, c1 = {0, 0, 0, 0}, c2 = {0, 0, 0, 0};
-#pragma unroll
-                    for (int kap = 0; kap < 2; ++kap) {
-                        const v4i A = unit_i8<BITS>(&kw[sg][(2 * tau + kap) * WPU]);
-                        c0 = mfma_i8(A, bq[0][kap], c0);
-                        c1 = mfma_i8(A, bq[1][kap], c1);
-                        c2 = mfma_i8(A, bq[2][kap], c2);
-                    }
-                    const float4 s2 = *reinterpret_cast<const float4*>(&sm.aux[2][64 * sg + 16 * tau + 4 * G]);
-                    const float s2v[4] = {s2.x, s2.y, s2.z, s2.w};
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int raw = (int)((uint32_t)c2[i] << 16) + (int)((uint32_t)c1[i] << 8) + c0[i];
-                        lg[16 * sg + 4 * tau + i] = ((float)raw + beta) * (fq * a.scale_log2 * s2v[i]);
-                    }
-                }
-            const float alpha = softmax_update(lg);  // lg now holds p
-
-            // ---- p~ = p * a_V as two base-256 digits; gamma from the same digits ----------------
-            float pmx = 0.f;
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau) {
-                    const float4 av = *reinterpret_cast<const float4*>(&sm.aux[3][64 * sg + 16 * tau + 4 * G]);
-                    float* p = &lg[16 * sg + 4 * tau];
-                    p[0] *= av.x;
-                    p[1] *= av.y;
-                    p[2] *= av.z;
-                    p[3] *= av.w;
-                    pmx = fmaxf(pmx, fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])));
-                }
-            pmx = xor_max(xor_max(pmx, 16), 32);
-            const float psc = pmx > kTinyMax ? PMAX / pmx : 0.f;
-            float gam = 0.f;  // gamma in p~ grid units: sum of rounded p~ times b_V / a_V
-            v4i bp[2][2];
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg) {
-                uint32_t d0[4], d1[4];
-#pragma unroll
-                for (int tau = 0; tau < 4; ++tau) {
-                    const float* p = &lg[16 * sg + 4 * tau];
-                    const float4 rv = *reinterpret_cast<const float4*>(&sm.aux[4][64 * sg + 16 * tau + 4 * G]);
-                    const float r[4] = {rv.x, rv.y, rv.z, rv.w};
-                    uint32_t y[4];
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const int xi = __float2int_rn(p[i] * psc);
-                        gam = fmaf((float)xi, r[i], gam);
-                        y[i] = (uint32_t)(xi + 0x8080);
-                    }
-                    digits4_2(y[0], y[1], y[2], y[3], d0[tau], d1[tau]);
-                }
-                bp[sg][0] = v4i{(int)d0[0], (int)d0[1], (int)d0[2], (int)d0[3]};
-                bp[sg][1] = v4i{(int)d1[0], (int)d1[1], (int)d1[2], (int)d1[3]};
-            }
-            gam = xor_sum(xor_sum(gam, 16), 32);
-
-            // ---- O^T += codes_V^T x p~^T, channel 16*mt + 4*G + i ------------------------------
-            v4i acc[8][2];
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) acc[mt][0] = acc[mt][1] = v4i{0, 0, 0, 0};
-#pragma unroll
-            for (int sg = 0; sg < 2; ++sg)
-#pragma unroll
-                for (int mt = 0; mt < 8; ++mt) {
-                    const v4i A = unit_i8<BITS>(&vw[sg][mt * WPU]);
-                    acc[mt][0] = mfma_i8(A, bp[sg][0], acc[mt][0]);
-                    acc[mt][1] = mfma_i8(A, bp[sg][1], acc[mt][1]);
-                }
-            const float fp = pmx / PMAX;
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt) {
-                const float4 s2 = *reinterpret_cast<const float4*>(&sm.aux[5][16 * mt + 4 * G]);
-                const float s2v[4] = {s2.x, s2.y, s2.z, s2.w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int cint = (int)((uint32_t)acc[mt][1][i] << 8) + acc[mt][0][i];
-                    orot[mt][i] = fmaf((float)cint + gam, fp * s2v[i], orot[mt][i] * alpha);
-                }
-            }
-        }
-    }
-
-    // ---- sink and residual (bf16, unrotated): last split only ------------------------------
-    if (last && ns + nr > 0) {
-        // q as the bf16 B operand (hi, plus lo when q is fp32): lane (G, n) holds q[n][32k + 8G ..]
-        v8bf qh[4], ql[4];
-        {
-            size_t qi[4];
-            float qv[4][8];
-#pragma unroll
-            for (int k = 0; k < 4; ++k) qi[k] = (qrow + min(hn, g - 1)) * kD + 32 * k + 8 * G;
-            load_q_runs<4>(a, qi, qv);
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    const float v = head_lane ? qv[k][e] : 0.f;
-                    const __bf16 hi = (__bf16)v;
-                    qh[k][e] = hi;
-                    ql[k][e] = (__bf16)(v - (float)hi);
-                }
-        }
-        const bool two = !a.q_bf16;
-        const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
-        for (int chunk = 0; chunk <= nsc; ++chunk) {
-            const bool in_sink = chunk < nsc;
-            const int t0 = in_sink ? chunk * kG : 0;
-            const int cn = in_sink ? min(kG, ns - t0) : nr;
-            if (cn <= 0) continue;
-            const uint16_t* Kp = in_sink ? a.k_sink + ((size_t)stream * a.n_sink + t0) * kD
-                                         : a.k_resid + (size_t)stream * kG * kD;
-            const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
-                                         : a.v_resid + (size_t)stream * kG * kD;
-            float lg[32];
-#pragma unroll
-            for (int tau = 0; tau < 8; ++tau) {
-                v4f acc = {0.f, 0.f, 0.f, 0.f};
-                // A row of this lane; rows past the chunk read its last row (their logits are masked)
-                const int arow = min(16 * tau + (l & 15), cn - 1);
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint4 u = *reinterpret_cast<const uint4*>(Kp + (size_t)arow * kD + 32 * k + 8 * G);
-                    v8bf A;
-                    __builtin_memcpy(&A, &u, 16);
-                    acc = mfma_bf16(A, qh[k], acc);
-                    if (two) acc = mfma_bf16(A, ql[k], acc);
-                }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int t = 16 * tau + 4 * G + i;
-                    lg[4 * tau + i] = t < cn ? acc[i] * a.scale_log2 : -INFINITY;
-                }
-            }
-            const float alpha = softmax_update(lg);
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) orot[mt][i] *= alpha;
-            __syncthreads();  // the previous chunk is done with sm.p / sm.hv
-            // every head slot writes its row (slots past g: p = 0, alpha = 1), so that the PV
-            // loop below runs over all slots without a branch per head and token
-            if (n < GQ) {
-#pragma unroll
-                for (int tau = 0; tau < 8; ++tau)
-#pragma unroll
-                    for (int i = 0; i < 4; ++i) sm.p[hn][16 * tau + 4 * G + i] = head_lane ? lg[4 * tau + i] : 0.f;
-                if (G == 0) sm.hv[hn][2] = head_lane ? alpha : 1.f;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int h = 0; h < GQ; ++h) {
-                const float al = sm.hv[h][2];
-                oplain[h][0] *= al;
-                oplain[h][1] *= al;
-            }
-            pv_plain<GQ>(oplain, sm.p, Vp, cn, l);
-        }
-    }
-
-    // ---- finish: per-head sum, then the output or a partial --------------------------------
-    const float lt = xor_sum(xor_sum(l_run, 16), 32);
-    if (a.n_split == 1) {
-        __syncthreads();
-        if (head_lane) {
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) sm.q[hn][16 * mt + 4 * G + i] = orot[mt][i];
-            if (G == 0) sm.hv[hn][3] = lt;
-        }
-        __syncthreads();
-        if (a.rotate) lds_hadamard<GQ>(sm.q, g);
-        const float rs = a.rotate ? kInvSqrt128 : 1.f;
-#pragma unroll
-        for (int h = 0; h < GQ; ++h) {
-            if (h < g) {
-                const float L = sm.hv[h][3];
-                float o0 = sm.q[h][2 * l] * rs + oplain[h][0];
-                float o1 = sm.q[h][2 * l + 1] * rs + oplain[h][1];
-                o0 = L > 0.f ? o0 / L : 0.f;
-                o1 = L > 0.f ? o1 / L : 0.f;
-                const size_t idx = (qrow + h) * kD + 2 * l;
-                if (a.out_bf16)
-                    reinterpret_cast<uint32_t*>(a.out)[idx >> 1] =
-                        (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
-                else
-                    *reinterpret_cast<float2*>(static_cast<float*>(a.out) + idx) = make_float2(o0, o1);
-            }
-        }
-    } else {
-        if (head_lane) {
-            float* P = a.ws + ((qrow + hn) * a.n_split + split) * kPart;
-#pragma unroll
-            for (int mt = 0; mt < 8; ++mt)
-                *reinterpret_cast<float4*>(P + 4 + 16 * mt + 4 * G) =
-                    make_float4(orot[mt][0], orot[mt][1], orot[mt][2], orot[mt][3]);
-            if (G == 0) {
-                P[0] = m_run;
-                P[1] = lt;
-            }
-        }
-#pragma unroll
-        for (int h = 0; h < GQ; ++h) {
-            if (h < g) {
-                float* P = a.ws + ((qrow + h) * a.n_split + split) * kPart;
-                *reinterpret_cast<float2*>(P + 132 + 2 * l) = make_float2(oplain[h][0], oplain[h][1]);
             }
         }
     }
@@ -903,9 +447,13 @@ void k_decode4(DecodeArgs a) {
     constexpr uint32_t MAGIC_BITS = 0x4B400000u;
     // output role: head 4*hg + G, column n; A-operand role: row 4*h + j (digit j of head 4*hg + h)
     const int l = threadIdx.x, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
-    const int g = a.g;
+    // wave = (head chunk, stream, split), the chunk slowest: the chunks of a stream read the
+    // same tiles, n_streams * n_split workgroups apart, which keeps them on one XCD when that
+    // distance is a multiple of 8
     const int split = blockIdx.x % a.n_split;
-    const int stream = blockIdx.x / a.n_split;
+    const int cs = blockIdx.x / a.n_split;
+    const int stream = cs % a.n_streams, chunk = cs / a.n_streams;
+    const int g = min(a.g_chunk, a.g - chunk * a.g_chunk);  // query heads of this wave
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
     const int len = max(a.seq_len[b], 0);
     const int ns = min(len, a.n_sink);
@@ -918,7 +466,7 @@ void k_decode4(DecodeArgs a) {
     const int blk0 = res_only ? 0 : split * a.bps;
     int blk1 = res_only ? 0 : (body_last ? nbody : min(blk0 + a.bps, nbody));
     if (PG && blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
-    const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * g;
+    const size_t qrow = (size_t)b * a.n_q + (size_t)kvh * a.g + (size_t)chunk * a.g_chunk;
     const size_t tb = tile_bytes(BITS, CMP), cb = code_bytes(BITS);
 
     float m_run[NH], l_run[NH];  // head 4*hg + G; l_run is this lane's partial sum
@@ -1306,7 +854,9 @@ void k_decode4(DecodeArgs a) {
             size_t qi[4];
             float qv[4][8];
 #pragma unroll
-            for (int k = 0; k < 4; ++k) qi[k] = (qrow + NHX - 1) * kD + 32 * k + 8 * G;
+            // (clamped to a head of the chunk: the extra slot may be empty in a chunk of a larger
+            // group, and its results are then not written)
+            for (int k = 0; k < 4; ++k) qi[k] = (qrow + min(NHX - 1, g - 1)) * kD + 32 * k + 8 * G;
             load_q_runs<4>(a, qi, qv);
 #pragma unroll
             for (int k = 0; k < 4; ++k)
@@ -1445,7 +995,7 @@ void k_decode4(DecodeArgs a) {
                 }
             }
         }
-        if constexpr (X1) {
+        if (X1 && g == NHX) {  // a chunk of a larger group may leave the extra head slot empty
             float* P = a.ws + ((qrow + NHX - 1) * a.n_split + split) * kPart;
 #pragma unroll
             for (int q = 0; q < 2; ++q) P[4 + 16 * (4 * q + G) + n] = orot4[q];
@@ -1538,7 +1088,7 @@ __global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
 template <int BITS, int GQ, int CMP>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
-    const dim3 grid((unsigned)(streams * a.n_split));
+    const dim3 grid((unsigned)(streams * a.n_split * a.n_chunk));
     const bool pg = a.block_table != nullptr;
     if constexpr (GQ == 4) {
         if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 0>), grid, dim3(64), 0, stream, a);
@@ -1549,8 +1099,7 @@ hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     } else if constexpr (GQ == 8) {
         if (pg) hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 1, 0>), grid, dim3(64), 0, stream, a);
         else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0, 0>), grid, dim3(64), 0, stream, a);
-    } else
-        hipLaunchKernelGGL((k_decode<BITS, GQ, CMP>), dim3((unsigned)(streams * a.n_split)), dim3(64), 0, stream, a);
+    }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_split == 1) return e;
     hipLaunchKernelGGL(k_decode_merge, dim3((unsigned)(batch * a.n_q)), dim3(128), 0, stream, a);
@@ -1559,10 +1108,9 @@ hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
 
 template <int BITS, int CMP>
 hipError_t launch_bits(const DecodeArgs& a, int batch, hipStream_t stream) {
-    if (a.g <= 4) return launch_cfg<BITS, 4, CMP>(a, batch, stream);
-    if (a.g == 5) return launch_cfg<BITS, 5, CMP>(a, batch, stream);
-    if (a.g <= 8) return launch_cfg<BITS, 8, CMP>(a, batch, stream);
-    return launch_cfg<BITS, 16, CMP>(a, batch, stream);
+    if (a.g_chunk <= 4) return launch_cfg<BITS, 4, CMP>(a, batch, stream);
+    if (a.g_chunk == 5) return launch_cfg<BITS, 5, CMP>(a, batch, stream);
+    return launch_cfg<BITS, 8, CMP>(a, batch, stream);
 }
 
 }  // namespace
@@ -1572,12 +1120,17 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     int nb = max_len > n_sink ? (max_len - n_sink) / kG : 0;
     if (nb > max_blocks) nb = max_blocks;
     p.max_blocks_used = nb;
-    const int streams = batch * n_kv;
     const int g = n_kv > 0 ? n_q / n_kv : 1;
-    // one wave per (split, stream).  Aim for one round of resident waves (the kernels'
+    // Groups above 8 query heads go to the row-digit kernels in chunks of at most 8 heads (as
+    // even as possible), one wave per chunk; the chunks of a stream read the same tiles.
+    p.n_chunk = (g + 7) / 8;
+    p.g_chunk = (g + p.n_chunk - 1) / p.n_chunk;
+    const int gc = p.g_chunk;
+    const int streams = batch * n_kv * p.n_chunk;  // waves per split
+    // one wave per (split, chunk, stream).  Aim for one round of resident waves (the kernels'
     // occupancy on 1024 SIMDs), with at least 4 body tiles per split so that the per-wave
     // setup and the merge stay small against the streaming.
-    const int per_simd = g <= 4 ? (bits == 2 ? 3 : 2) : (g <= 8 ? 2 : 1);
+    const int per_simd = gc <= 4 ? (bits == 2 ? 3 : 2) : 2;
     int want = (1024 * per_simd + streams - 1) / streams;
     if (want > nb / 4) want = nb / 4;
     p.res_split = 0;
@@ -1632,6 +1185,9 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
     a.res_split = plan.res_split;
+    a.n_streams = c.batch * c.n_kv;
+    a.n_chunk = plan.n_chunk;
+    a.g_chunk = plan.g_chunk;
     a.ws = ws;
     if (compact) return bits == 2 ? launch_bits<2, 1>(a, c.batch, stream) : launch_bits<4, 1>(a, c.batch, stream);
     return bits == 2 ? launch_bits<2, 0>(a, c.batch, stream) : launch_bits<4, 0>(a, c.batch, stream);
