@@ -58,7 +58,7 @@ hipError_t launch_append(const kvarn_cache& c, int n_sink, const void* k_new, co
 struct DecodePlan {
     int n_chunk, g_chunk;  // query heads of a group taken in n_chunk chunks of up to g_chunk (<= 8)
     int n_split;           // splits per (sequence, kv head)
-    int res_split;         // 1: the last split attends only sink + residual
+    int n_res;             // splits (the last of n_split) that hold only sink + residual chunks
     int blocks_per_split;  // body tiles per body split
     int max_blocks_used;   // upper bound of body tiles over the batch
 };

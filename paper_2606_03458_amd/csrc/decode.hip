@@ -20,11 +20,14 @@
 // groups are taken in chunks of at most eight heads, one wave per chunk.
 //
 // Sink and residual tokens (bf16, unrotated) use the bf16 matrix cores for q . k (q as a bf16
-// pair hi + lo when it is fp32) and plain FMAs for p . v.  One wave owns a (split, sequence,
-// kv head, head chunk); the last split also takes sink + residual (or only those when the stream is split:
-// then they run beside the body splits instead of after one of them).  A single split writes the final
-// output directly (inverse rotation in LDS); several splits write partials that the merge
+// pair hi + lo when it is fp32) and plain FMAs for p . v, in chunks of 32 tokens.  One wave owns
+// a (split, sequence, kv head, head chunk).  An unsplit stream's one wave takes sink + residual
+// after its body tiles; a split stream's sink and residual chunks get splits of their own (one
+// per chunk when the waves fit), which run beside the body splits.  A single split writes the
+// final output directly (inverse rotation in LDS); several splits write partials that the merge
 // kernel combines by log-sum-exp.
+#include <algorithm>
+
 #include "common.hpp"
 
 namespace kvarn {
@@ -37,6 +40,7 @@ typedef unsigned v4u __attribute__((ext_vector_type(4)));
 typedef unsigned v2u __attribute__((ext_vector_type(2)));
 
 constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
+constexpr int kRC = 32;     // bf16 tokens (sink / residual) per chunk
 
 // A fixed-point grid is only formed for a maximum above this; below it the values are taken
 // as zero.  For p~ this drops a tile whose probabilities are all below 1e-30 relative to the
@@ -64,7 +68,7 @@ struct DecodeArgs {
     uint32_t* err_word;
     float scale_log2;  // sm_scale * log2(e): logits are kept in log2 units
     int n_split, bps;  // splits per stream and body tiles per body split
-    int res_split;     // 1: the last split holds only sink + residual (n_split - 1 body splits)
+    int n_res;         // splits that hold only sink + residual chunks (the last n_res of n_split)
     int n_streams;     // batch * n_kv
     int n_chunk, g_chunk;  // head chunks per stream and heads per chunk (row-digit kernels)
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
@@ -259,34 +263,6 @@ __device__ __forceinline__ void load_q_runs(const DecodeArgs& a, const size_t (&
     }
 }
 
-// o_plain[h] += sum over the chunk's rows of p[h][t] * V[t] for every head slot h, this lane's
-// two channels 2l, 2l + 1 (V bf16, unrotated).  Rows in batches of 32 with all loads in flight;
-// rows past the chunk read its last row (their p is 0).  p is read four tokens at a time, and
-// each head accumulates its tokens in ascending order.
-template <int NHS>
-__device__ __forceinline__ void pv_plain(float (&oplain)[NHS][2], const float (&p)[NHS][kG], const uint16_t* Vp,
-                                         int cn, int l) {
-    for (int t = 0; t < cn; t += 32) {
-        uint32_t v2[32];
-#pragma unroll
-        for (int u = 0; u < 32; ++u)
-            v2[u] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t + u, cn - 1) * kD)[l];
-#pragma unroll
-        for (int u = 0; u < 32; u += 4) {
-#pragma unroll
-            for (int hh = 0; hh < NHS; ++hh) {
-                const float4 ph = *reinterpret_cast<const float4*>(&p[hh][t + u]);
-                const float pv[4] = {ph.x, ph.y, ph.z, ph.w};
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    oplain[hh][0] = fmaf(pv[i], __uint_as_float(v2[u + i] << 16), oplain[hh][0]);
-                    oplain[hh][1] = fmaf(pv[i], __uint_as_float(v2[u + i] & 0xFFFF0000u), oplain[hh][1]);
-                }
-            }
-        }
-    }
-}
-
 // ---- group size <= 4: digit planes in the MFMA rows ----------------------------------------
 // Both products take the real-valued side (q~ or p~, as base-256 digit planes) as the A operand
 // and the codes as B.  Row 4*h + j of A is digit j of head h (j = 3 is zero).  The A and B
@@ -374,7 +350,7 @@ struct Smem4 {
     uint4 qp[NH][4][2][16];         // q~ digit planes [group][digit slot][kappa][qslot(slot, G, head)]; slot 3 stays zero
     uint4 qp4[X1 ? 4 : 1][2][4];    // X1: the extra head's q~ digit planes [digit slot][kappa][G]; slot 3 zero
     float hv[4 * NH + X1][4];       // per head: beta, q~ step, alpha, l
-    float p[4 * NH + X1][kG];       // probabilities of a bf16 chunk (sink / residual)
+    float p[4 * NH + X1][kRC];      // probabilities of a bf16 chunk (sink / residual)
 };
 
 // Position of the 16-byte piece (K group G, head h) in a digit slot's row of the q~ planes.  The
@@ -459,10 +435,11 @@ void k_decode4(DecodeArgs a) {
     const int ns = min(len, a.n_sink);
     const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
-    // the last split attends sink + residual; with res_split it holds nothing else
-    const bool last = split == a.n_split - 1;
-    const bool res_only = a.res_split && last;
-    const bool body_last = split == a.n_split - 1 - a.res_split;  // takes any excess of body tiles
+    // The last n_res splits hold only sink + residual chunks; without them the last body split
+    // takes those chunks too.
+    const int nbs = a.n_split - a.n_res;  // body splits
+    const bool res_only = split >= nbs;
+    const bool body_last = split == nbs - 1;  // takes any excess of body tiles
     const int blk0 = res_only ? 0 : split * a.bps;
     int blk1 = res_only ? 0 : (body_last ? nbody : min(blk0 + a.bps, nbody));
     if (PG && blk0 < blk1 && !body_ids_ok(a, b, blk0, blk1, l)) blk1 = blk0;
@@ -482,18 +459,19 @@ void k_decode4(DecodeArgs a) {
         for (int mt = 0; mt < 8; ++mt) orot[hg][mt] = 0.f;
     }
 
-    // online softmax of group hg over this lane's 8 logits (log2 units; -inf = absent) -> p,
+    // online softmax of group hg over this lane's logits (log2 units; -inf = absent) -> p,
     // returns alpha
-    auto softmax_update = [](float (&lg)[8], bool maybe_absent, float& m, float& lsum) -> float {
+    auto softmax_update = [](auto& lg, bool maybe_absent, float& m, float& lsum) -> float {
+        constexpr int N = sizeof(lg) / sizeof(lg[0]);
         float mx = lg[0];
 #pragma unroll
-        for (int k = 1; k < 8; ++k) mx = fmaxf(mx, lg[k]);
+        for (int k = 1; k < N; ++k) mx = fmaxf(mx, lg[k]);
         mx = row_max(mx);
         const float m_new = fmaxf(m, mx);
         const float alpha = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - m_new);
         float s = 0.f;
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
+        for (int k = 0; k < N; ++k) {
             float p = __builtin_amdgcn_exp2f(lg[k] - m_new);
             if (maybe_absent) p = lg[k] == -INFINITY ? 0.f : p;
             lg[k] = p;
@@ -818,11 +796,17 @@ void k_decode4(DecodeArgs a) {
         if (blk < blk1) step(ra, rb, id_n);
     }
 
-    // ---- sink and residual (bf16, unrotated): last split only ------------------------------
+    // ---- sink and residual (bf16, unrotated) -------------------------------------------------
+    // In chunks of kRC tokens: the sink's, then the residual's (no chunk spans both).  Split r of
+    // the n_res sink/residual splits takes chunks r, r + n_res, ...; without such splits the
+    // last body split takes them all.  A chunk's key rows (bf16 MFMA operands) and value rows
+    // (one dword per lane and row) are loaded together, one memory round trip per chunk.
     float oplain[NHX][2];  // head hh, channel 2*l + jj (unrotated)
 #pragma unroll
     for (int hh = 0; hh < NHX; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
-    if (last && ns + nr > 0) {
+    const int nsc = (ns + kRC - 1) / kRC, nch = nsc + (nr + kRC - 1) / kRC;
+    const int c0 = res_only ? split - nbs : 0, cstep = res_only ? a.n_res : 1;
+    if ((res_only || (a.n_res == 0 && body_last)) && c0 < nch) {
         // A operand of group hg: row 4h holds q of head 4*hg + h rounded to bf16, row 4h + 1 the
         // remainder (zero for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds
         // q[.][32k + 8G ..].  Loads are clamped to a valid head, then masked.
@@ -848,7 +832,7 @@ void k_decode4(DecodeArgs a) {
                     }
             }
         }
-        // extra head: the same rows (hi, lo) of its q, placed in row group tau % 4 at use
+        // extra head: the same rows (hi, lo) of its q, placed in row group tau at use
         v8bf aqs4[4];
         if constexpr (X1) {
             size_t qi[4];
@@ -867,57 +851,55 @@ void k_decode4(DecodeArgs a) {
                     aqs4[k][e] = j == 0 ? hi : (__bf16)(v - (float)hi);
                 }
         }
-        const int nsc = (ns + kG - 1) / kG;  // sink chunks of up to 128 tokens, then the residual
-        for (int chunk = 0; chunk <= nsc; ++chunk) {
-            const bool in_sink = chunk < nsc;
-            const int t0 = in_sink ? chunk * kG : 0;
-            const int cn = in_sink ? min(kG, ns - t0) : nr;
-            if (cn <= 0) continue;
-            const uint16_t* Kp = in_sink ? a.k_sink + ((size_t)stream * a.n_sink + t0) * kD
-                                         : a.k_resid + (size_t)stream * kG * kD;
-            const uint16_t* Vp = in_sink ? a.v_sink + ((size_t)stream * a.n_sink + t0) * kD
-                                         : a.v_resid + (size_t)stream * kG * kD;
-            __syncthreads();  // the previous chunk is done with sm.p / sm.hv
-            // logits of head 4*hg + G, token 16*tau + n.  Rows past the chunk read its last row
-            // (in bounds) and are masked, so no load waits behind a branch.
-            float lg[NH][8];
-            v4f r4[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+        for (int c = c0; c < nch; c += cstep) {
+            const bool in_sink = c < nsc;
+            const int t0 = kRC * (in_sink ? c : c - nsc);
+            const int cn = min(kRC, (in_sink ? ns : nr) - t0);
+            const size_t row0 = in_sink ? (size_t)stream * a.n_sink + t0 : (size_t)stream * kG + t0;
+            const uint16_t* Kp = (in_sink ? a.k_sink : a.k_resid) + row0 * kD;
+            const uint16_t* Vp = (in_sink ? a.v_sink : a.v_resid) + row0 * kD;
+            // Rows past the chunk read its last row (in bounds) and are masked (p = 0).
+            v8bf B[2][4];  // key rows 16 tau + n, channels 32 k + 8 G ..
 #pragma unroll
-            for (int tau = 0; tau < 8; ++tau) {
-                const int trow = 16 * tau + n;
-                const uint16_t* kr = Kp + (size_t)min(trow, cn - 1) * kD + 8 * G;
-                v8bf B[4];
+            for (int tau = 0; tau < 2; ++tau) {
+                const uint16_t* kr = Kp + (size_t)min(16 * tau + n, cn - 1) * kD + 8 * G;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const uint4 u = *reinterpret_cast<const uint4*>(kr + 32 * k);
-                    __builtin_memcpy(&B[k], &u, 16);
+                    __builtin_memcpy(&B[tau][k], &u, 16);
                 }
+            }
+            uint32_t v2[kRC];  // value row t, channels 2 l, 2 l + 1
+#pragma unroll
+            for (int t = 0; t < kRC; ++t) v2[t] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t, cn - 1) * kD)[l];
+            __syncthreads();  // the previous chunk is done with sm.p / sm.hv
+            // logits of head 4*hg + G, token 16*tau + n
+            float lg[NH][2];
+            v4f r4 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int tau = 0; tau < 2; ++tau) {
 #pragma unroll
                 for (int hg = 0; hg < NH; ++hg) {
                     v4f acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) acc = mfma_bf16(aqs[hg][k], B[k], acc);
-                    lg[hg][tau] = trow < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
+                    for (int k = 0; k < 4; ++k) acc = mfma_bf16(aqs[hg][k], B[tau][k], acc);
+                    lg[hg][tau] = 16 * tau + n < cn ? (acc[0] + acc[1]) * a.scale_log2 : -INFINITY;
                 }
                 if constexpr (X1) {
-                    // token block tau lands in lanes G == tau % 4 of accumulator tau / 4
-                    const bool mine = h == (tau & 3);
+                    // token block tau lands in lanes G == tau of the accumulator
+                    const bool mine = h == tau;
                     const v8bf zb = {};
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) r4[tau >> 2] = mfma_bf16(mine ? aqs4[k] : zb, B[k], r4[tau >> 2]);
+                    for (int k = 0; k < 4; ++k) r4 = mfma_bf16(mine ? aqs4[k] : zb, B[tau][k], r4);
                 }
             }
             if constexpr (X1) {
-                // extra head, tokens 16 (4 q + G) + n
-                float lgx[2];
-#pragma unroll
-                for (int q = 0; q < 2; ++q)
-                    lgx[q] = 16 * (4 * q + G) + n < cn ? (r4[q][0] + r4[q][1]) * a.scale_log2 : -INFINITY;
+                // extra head, token 16 G + n (G < 2)
+                float lgx[2] = {G < 2 && 16 * G + n < cn ? (r4[0] + r4[1]) * a.scale_log2 : -INFINITY, -INFINITY};
                 const float alpha = softmax_wave(lgx, true, m4, l4);
                 orot4[0] *= alpha;
                 orot4[1] *= alpha;
-#pragma unroll
-                for (int q = 0; q < 2; ++q) sm.p[NHX - 1][16 * (4 * q + G) + n] = lgx[q];
+                if (G < 2) sm.p[NHX - 1][16 * G + n] = lgx[0];
                 if (l == 0) sm.hv[NHX - 1][2] = alpha;
             }
 #pragma unroll
@@ -929,17 +911,27 @@ void k_decode4(DecodeArgs a) {
                 // PV loop below runs over all slots without a branch per head and token
                 const bool real = 4 * hg + G < g;
 #pragma unroll
-                for (int tau = 0; tau < 8; ++tau) sm.p[4 * hg + G][16 * tau + n] = real ? lg[hg][tau] : 0.f;
+                for (int tau = 0; tau < 2; ++tau) sm.p[4 * hg + G][16 * tau + n] = real ? lg[hg][tau] : 0.f;
                 if (n == 0) sm.hv[4 * hg + G][2] = real ? alpha : 1.f;
             }
             __syncthreads();
+            // o_plain[h] = alpha o_plain[h] + sum over the chunk's rows of p[h][t] V[t]
 #pragma unroll
             for (int hh = 0; hh < NHX; ++hh) {
                 const float al = sm.hv[hh][2];
                 oplain[hh][0] *= al;
                 oplain[hh][1] *= al;
+#pragma unroll
+                for (int t = 0; t < kRC; t += 4) {
+                    const float4 ph = *reinterpret_cast<const float4*>(&sm.p[hh][t]);
+                    const float pv[4] = {ph.x, ph.y, ph.z, ph.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        oplain[hh][0] = fmaf(pv[i], __uint_as_float(v2[t + i] << 16), oplain[hh][0]);
+                        oplain[hh][1] = fmaf(pv[i], __uint_as_float(v2[t + i] & 0xFFFF0000u), oplain[hh][1]);
+                    }
+                }
             }
-            pv_plain<NHX>(oplain, sm.p, Vp, cn, l);
         }
     }
 
@@ -1014,75 +1006,157 @@ void k_decode4(DecodeArgs a) {
     }
 }
 
-// One 128-thread workgroup per (sequence, query head): log-sum-exp merge of the split
-// partials, inverse rotation of the body part, normalisation.
-__global__ __launch_bounds__(128) void k_decode_merge(DecodeArgs a) {
-    __shared__ float orot[kD];
-    const int c = threadIdx.x;
-    const size_t bh = blockIdx.x;
+// Merge of the split partials of a (sequence, query head): log-sum-exp weights, the inverse
+// rotation of the body part in registers (lane l holds channels 2l, 2l + 1), normalisation.
+// W waves per (sequence, query head), 256 threads per workgroup: W = 1 (four heads per
+// workgroup) for few splits; W = 4 for many, wave w summing splits w, w + 4, ... and wave 0
+// adding the four sums in a fixed order (eight waves per head measured slower at 37 splits).
+constexpr int kMergeWide = 9;  // from this many splits on, four waves per head
+
+// Channel partner c ^ (2 m) of lane l's two channels: the value of lane l ^ m.
+template <int M>
+__device__ __forceinline__ float lane_xor(float v, int l) {
+    if constexpr (M == 1) return fdpp_x1(v);
+    else if constexpr (M == 2) return fdpp_x2(v);
+    else if constexpr (M == 16) {
+        const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return __uint_as_float(((l >> 4) & 1) ? x[0] : x[1]);
+    } else if constexpr (M == 32) {
+        const auto x = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+        return __uint_as_float(l < 32 ? x[1] : x[0]);
+    } else {
+        return __shfl_xor(v, M);
+    }
+}
+// One butterfly stage of stride 2 M between lanes l and l ^ M (both channels): the lower
+// channel keeps a + b, the upper one a - b.
+template <int M>
+__device__ __forceinline__ void fwht_stage(float (&x)[2], int l) {
+    const bool upper = (l & M) != 0;
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        const float p = lane_xor<M>(x[e], l);
+        x[e] = upper ? p - x[e] : x[e] + p;
+    }
+}
+
+template <int W>
+__global__ __launch_bounds__(256) void k_decode_merge(DecodeArgs a) {
+    static_assert(W == 1 || W == 4, "one or four waves per head");
+    constexpr int HPB = 4 / W;          // heads per workgroup
+    constexpr int U = W == 1 ? 8 : 16;  // splits with loads in flight per wave
+    __shared__ float red[W > 1 ? W - 1 : 1][2 * kD + 2];
+    const int l = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int part = wv % W;
+    const size_t bh = (size_t)blockIdx.x * HPB + wv / W;
+    // W > 1: one head per workgroup, so every wave leaves here or none does.
+    if (bh >= (size_t)a.n_streams / a.n_kv * a.n_q) return;
     const float* P = a.ws + bh * a.n_split * kPart;
     const int S = a.n_split;
-    // Splits in batches of 8 with every load of a batch in flight (indices past the last split
-    // are clamped, their values unused): two passes, the maximum, then the weighted sums.
-    constexpr int U = 8;
-    float M = -INFINITY;
-    for (int s0 = 0; s0 < S; s0 += U) {
+    // Log-sum-exp over this wave's splits, U of them with every load in flight (indices past the
+    // last split are clamped, their values unused), the sums kept relative to the running
+    // maximum M of the splits that hold a probability mass.
+    float M = -INFINITY, L = 0.f, acc[2] = {0.f, 0.f}, pl[2] = {0.f, 0.f};
+    for (int s0 = part; s0 < S; s0 += U * W) {
         float mm[U], ll[U];
+        float2 ov[U], pv[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const int s = min(s0 + u, S - 1);
-            mm[u] = P[s * kPart];
-            ll[u] = P[s * kPart + 1];
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-            if (s0 + u < S && ll[u] > 0.f) M = fmaxf(M, mm[u]);
-    }
-    float L = 0.f, acc = 0.f, pl = 0.f;
-    for (int s0 = 0; s0 < S; s0 += U) {
-        float mm[U], ll[U], ov[U], pv[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const float* Ps = P + min(s0 + u, S - 1) * kPart;
+            const float* Ps = P + (size_t)min(s0 + u * W, S - 1) * kPart;
             mm[u] = Ps[0];
             ll[u] = Ps[1];
-            ov[u] = Ps[4 + c];
-            pv[u] = Ps[132 + c];
+            ov[u] = *reinterpret_cast<const float2*>(Ps + 4 + 2 * l);
+            pv[u] = *reinterpret_cast<const float2*>(Ps + 132 + 2 * l);
         }
+        float mb = M;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (s0 + u * W < S && ll[u] > 0.f) mb = fmaxf(mb, mm[u]);
+        if (mb == -INFINITY) continue;  // no mass so far
+        const float r = exp2f(M - mb);  // 0 while M is still -inf
+        L *= r;
+        acc[0] *= r;
+        acc[1] *= r;
+        pl[0] *= r;
+        pl[1] *= r;
+        M = mb;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            if (s0 + u < S && ll[u] > 0.f) {
+            if (s0 + u * W < S && ll[u] > 0.f) {
                 const float w = exp2f(mm[u] - M);
                 L += w * ll[u];
-                acc += w * ov[u];
-                pl += w * pv[u];
+                acc[0] += w * ov[u].x;
+                acc[1] += w * ov[u].y;
+                pl[0] += w * pv[u].x;
+                pl[1] += w * pv[u].y;
             }
         }
     }
-    orot[c] = acc;
-    __syncthreads();
-    for (int h = 1; a.rotate && h < kD; h <<= 1) {
-        float x0 = 0.f, x1 = 0.f;
-        int i0 = 0;
-        if (c < 64) {
-            i0 = (c / h) * 2 * h + (c % h);
-            x0 = orot[i0];
-            x1 = orot[i0 + h];
+    if constexpr (W > 1) {
+        // waves 1..W-1 hand (M, L, sums) to wave 0, which rescales them to the common maximum
+        // and adds them in wave order
+        if (part > 0) {
+            float* rw = red[part - 1];
+            *reinterpret_cast<float2*>(rw + 2 * l) = make_float2(acc[0], acc[1]);
+            *reinterpret_cast<float2*>(rw + kD + 2 * l) = make_float2(pl[0], pl[1]);
+            if (l == 0) {
+                rw[2 * kD] = M;
+                rw[2 * kD + 1] = L;
+            }
         }
         __syncthreads();
-        if (c < 64) {
-            orot[i0] = x0 + x1;
-            orot[i0 + h] = x0 - x1;
+        if (part > 0) return;
+        float Mw[W - 1];
+        float Mt = M;
+#pragma unroll
+        for (int w = 0; w < W - 1; ++w) {
+            Mw[w] = red[w][2 * kD];
+            Mt = fmaxf(Mt, Mw[w]);
         }
-        __syncthreads();
+        if (Mt != -INFINITY) {
+            const float r = exp2f(M - Mt);
+            L *= r;
+            acc[0] *= r;
+            acc[1] *= r;
+            pl[0] *= r;
+            pl[1] *= r;
+#pragma unroll
+            for (int w = 0; w < W - 1; ++w) {
+                const float rw = exp2f(Mw[w] - Mt);  // 0 for a wave without mass
+                const float2 x = *reinterpret_cast<const float2*>(red[w] + 2 * l);
+                const float2 y = *reinterpret_cast<const float2*>(red[w] + kD + 2 * l);
+                acc[0] += rw * x.x;
+                acc[1] += rw * x.y;
+                pl[0] += rw * y.x;
+                pl[1] += rw * y.y;
+                L += rw * red[w][2 * kD + 1];
+            }
+        }
     }
-    float o = orot[c] * (a.rotate ? kInvSqrt128 : 1.f) + pl;
-    o = L > 0.f ? o / L : 0.f;
-    const size_t idx = bh * kD + c;
+    if (a.rotate) {  // H o_rot: butterflies of stride 1 (in the lane), 2, 4, ..., 64
+        const float t = acc[0];
+        acc[0] = t + acc[1];
+        acc[1] = t - acc[1];
+        fwht_stage<1>(acc, l);
+        fwht_stage<2>(acc, l);
+        fwht_stage<4>(acc, l);
+        fwht_stage<8>(acc, l);
+        fwht_stage<16>(acc, l);
+        fwht_stage<32>(acc, l);
+    }
+    const float rs = a.rotate ? kInvSqrt128 : 1.f;
+    float o[2];
+#pragma unroll
+    for (int e = 0; e < 2; ++e) {
+        o[e] = acc[e] * rs + pl[e];
+        o[e] = L > 0.f ? o[e] / L : 0.f;
+    }
+    const size_t idx = bh * kD + 2 * l;
     if (a.out_bf16)
-        static_cast<uint16_t*>(a.out)[idx] = f32_to_bf16(o);
+        reinterpret_cast<uint32_t*>(a.out)[idx >> 1] = (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
     else
-        static_cast<float*>(a.out)[idx] = o;
+        *reinterpret_cast<float2*>(static_cast<float*>(a.out) + idx) = make_float2(o[0], o[1]);
 }
 
 template <int BITS, int GQ, int CMP>
@@ -1102,7 +1176,11 @@ hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || a.n_split == 1) return e;
-    hipLaunchKernelGGL(k_decode_merge, dim3((unsigned)(batch * a.n_q)), dim3(128), 0, stream, a);
+    const size_t heads = (size_t)batch * a.n_q;
+    if (a.n_split >= kMergeWide)
+        hipLaunchKernelGGL(k_decode_merge<4>, dim3((unsigned)heads), dim3(256), 0, stream, a);
+    else
+        hipLaunchKernelGGL(k_decode_merge<1>, dim3((unsigned)((heads + 3) / 4)), dim3(256), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -1128,12 +1206,13 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     const int gc = p.g_chunk;
     const int streams = batch * n_kv * p.n_chunk;  // waves per split
     // one wave per (split, chunk, stream).  Aim for one round of resident waves (the kernels'
-    // occupancy on 1024 SIMDs), with at least 4 body tiles per split so that the per-wave
-    // setup and the merge stay small against the streaming.
+    // occupancy on 1024 SIMDs), with at least 2 body tiles per split so that the per-wave
+    // setup and the merge stay small against the streaming (measured on the Llama layer,
+    // decode + merge: 1 tile per split 15.6 us, 2 tiles 14.1 us, 4 tiles 17.8 us).
     const int per_simd = gc <= 4 ? (bits == 2 ? 3 : 2) : 2;
     int want = (1024 * per_simd + streams - 1) / streams;
-    if (want > nb / 4) want = nb / 4;
-    p.res_split = 0;
+    if (want > nb / 2) want = nb / 2;
+    p.n_res = 0;
     if (want <= 1) {
         p.n_split = 1;
         p.blocks_per_split = nb > 0 ? nb : 1;
@@ -1141,14 +1220,17 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     }
     p.blocks_per_split = (nb + want - 1) / want;
     p.n_split = (nb + p.blocks_per_split - 1) / p.blocks_per_split;
-    // A split stream is merged anyway: its sink + residual (bf16, a latency-bound chain of
-    // dependent loads) get a split of their own, which runs beside the body splits -- when the
-    // extra waves still fit in the one round of resident waves (otherwise body waves would
-    // wait for free slots behind them; measured: GQA-5 stress 28 % slower).
-    if ((long long)streams * (p.n_split + 1) <= 1024LL * per_simd) {
-        p.res_split = 1;
-        p.n_split += 1;
-    }
+    // A split stream is merged anyway: its sink + residual chunks (bf16, one memory round trip
+    // each) get splits of their own, one per chunk a stream can hold, which run beside the body
+    // splits -- when the extra waves still fit in the one round of resident waves (otherwise
+    // body waves would wait for free slots behind them; measured: GQA-5 stress 28 % slower);
+    // else one such split for all chunks if that fits.
+    const int chunks = (std::min(n_sink, std::max(max_len, 0)) + kRC - 1) / kRC + kG / kRC;
+    if ((long long)streams * (p.n_split + chunks) <= 1024LL * per_simd)
+        p.n_res = chunks;
+    else if ((long long)streams * (p.n_split + 1) <= 1024LL * per_simd)
+        p.n_res = 1;
+    p.n_split += p.n_res;
     return p;
 }
 
@@ -1184,7 +1266,7 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.scale_log2 = sm_scale * kLog2e;
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
-    a.res_split = plan.res_split;
+    a.n_res = plan.n_res;
     a.n_streams = c.batch * c.n_kv;
     a.n_chunk = plan.n_chunk;
     a.g_chunk = plan.g_chunk;

@@ -51,7 +51,7 @@ def test_noalloc_equals_decode(K):
         (3, 40, 8, 40 * 128 + 77, 2, 0, 0),
         (2, 32, 8, 24 * 128 + 5, 4, 1, 128),
         (1, 8, 2, 12 * 128 + 100, 2, 0, 0),
-        (2, 8, 2, 4 * 128 + 3, 2, 0, 0),  # one split per stream: no partials at all
+        (2, 8, 2, 3 * 128 + 3, 2, 0, 0),  # one split per stream: no partials at all
     ]
     sizes = []
     for i, (B, nq, nkv, T, bits, aux, ns) in enumerate(cases):
