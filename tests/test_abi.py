@@ -154,7 +154,7 @@ def test_decode_validation(K):
     keep, buf = _fake(1 << 20)
     need = K.kvarn_decode_workspace_bytes(p, c, 8, 4096)  # 4 streams x 32 tiles: split
     assert need > 0
-    assert K.kvarn_decode_workspace_bytes(p, c, 8, 512) == 0  # 4 tiles: one split, no partials
+    assert K.kvarn_decode_workspace_bytes(p, c, 8, 384) == 0  # 3 tiles: one split, no partials
     good = dict(n_q=8, q=buf, q_dtype=1, out=buf, out_dtype=1, sm_scale=0.088, max_len_hint=4096, workspace=buf,
                 workspace_bytes=need)
 
