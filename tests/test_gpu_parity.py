@@ -162,7 +162,7 @@ def test_decode_llama_layer(K, out_dtype):
 
 
 @pytest.mark.parametrize("bits,n_sink,name", [(2, 128, "llama"), (4, 0, "llama"), (2, 0, "stress"),
-                                              (4, 128, "stress")])
+                                              (4, 128, "stress"), (2, 100, "llama"), (4, 100, "stress")])
 def test_decode_variants(K, bits, n_sink, name):
     """Sink region, 4-bit codes, GQA 5, ragged lengths (including 0 and sink-only) and a
     residual, on a small batch that the split-K plan divides into many splits."""
@@ -171,6 +171,30 @@ def test_decode_variants(K, bits, n_sink, name):
     lens = [built.length, n_sink + 2 * 128, n_sink + 131, n_sink // 2 if n_sink else 0, 0]
     built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
     q = workloads.decode_queries(built, seed=3)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
+@pytest.mark.parametrize("batch,n_sink,body,n_split", [
+    (2, 100, 20, 18),   # 10 body splits + one per sink / residual chunk (4 + 4)
+    (32, 0, 20, 11),    # 10 body splits + one split for all chunks (one per chunk would not fit)
+    (32, 0, 24, 12),    # 12 body splits, the last one also taking the chunks
+])
+def test_decode_residual_placement(K, batch, n_sink, body, n_split):
+    """The three places the split plan gives a stream's sink and residual chunks (32 tokens
+    each): a split per chunk, one split for all chunks, or the last body split.  Ragged lengths
+    give every residual size class (empty, one token, a partial and full chunks, 127 tokens) and a
+    sink-only sequence; the split count is checked through the workspace size."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", n_sink=n_sink, context=n_sink + body * 128 + 77, batch=batch)
+    L = built.length
+    base = n_sink + (body - 1) * 128
+    cycle = [L, base, base + 1, base + 31, base + 32, base + 33, base + 100, base + 127, n_sink // 2]
+    lens = [cycle[i % len(cycle)] for i in range(batch)]
+    built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    ws_bytes = K.kvarn_decode_workspace_bytes(built.params, built.cache, built.n_q, L + 1)
+    assert ws_bytes == batch * built.n_q * n_split * 1040
+    q = workloads.decode_queries(built, seed=9)
     out = _decode(K, built, q)
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
