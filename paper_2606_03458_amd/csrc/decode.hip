@@ -310,10 +310,13 @@ __device__ __forceinline__ float row_sum(float v) {
 }
 
 // The digit-weighted sum of one output lane: register i holds the partial sum of digit i.  The
-// true sum fits int32, so the wrapping arithmetic below is exact.  Horner form: two
-// shift-and-add instructions.
+// true sum fits int32, so the wrapping arithmetic below is exact.  Horner form, two
+// shift-and-add instructions (v_lshl_add_u32); the empty asm statement keeps the compiler from
+// distributing the outer shift over the inner sum, which costs a third instruction.
 __device__ __forceinline__ int digit_sum(v4i c) {
-    return (int)(((((uint32_t)c[2] << 8) + (uint32_t)c[1]) << 8) + (uint32_t)c[0]);
+    uint32_t t = ((uint32_t)c[2] << 8) + (uint32_t)c[1];
+    asm("" : "+v"(t));
+    return (int)((t << 8) + (uint32_t)c[0]);
 }
 
 // Lane j of a quad holds y (row j of a 4 x 4 byte matrix); returns column j: byte i of the
