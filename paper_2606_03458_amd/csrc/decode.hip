@@ -71,6 +71,7 @@ struct DecodeArgs {
     int n_res;         // splits that hold only sink + residual chunks (the last n_res of n_split)
     int n_streams;     // batch * n_kv
     int n_chunk, g_chunk;  // head chunks per stream and heads per chunk (row-digit kernels)
+    int pair;          // 1: the two splits of a stream are the two waves of one workgroup
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
 };
 
@@ -194,10 +195,18 @@ __device__ __forceinline__ void stage_half_aux(float (&aux)[6][kD], int r0, cons
     *reinterpret_cast<float2*>(&aux[r0 + 2][2 * l]) = make_float2(s0, s1);
 }
 
-// LDS butterflies (stride 1..64) over rows [0, g) of x; 64 threads.  Unnormalized.
+// Orders this wave's accesses to its own LDS: a wave's LDS operations execute in issue order,
+// so no wait is needed, only a point that the compiler does not move memory operations across.
+// (Each wave of a decode workgroup has an LDS block of its own.)
+__device__ __forceinline__ void wave_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// LDS butterflies (stride 1..64) over rows [0, g) of x; one wave.  Unnormalized.
 template <int GQ>
 __device__ __forceinline__ void lds_hadamard(float (&x)[GQ][kD], int g) {
-    const int l = threadIdx.x;
+    const int l = threadIdx.x & 63;
     for (int h = 1; h < kD; h <<= 1) {
         for (int idx = l; idx < g * 64; idx += 64) {
             const int j = idx >> 6, r = idx & 63;
@@ -206,7 +215,7 @@ __device__ __forceinline__ void lds_hadamard(float (&x)[GQ][kD], int g) {
             x[j][i0] = x0 + x1;
             x[j][i0 + h] = x0 - x1;
         }
-        __syncthreads();
+        wave_sync();
     }
 }
 
@@ -409,10 +418,13 @@ __device__ __forceinline__ uint32_t rows_digit_reduce_scatter4(uint32_t x0, uint
 // channels 16 (4 q + G) + n (sg, q = 0, 1): two values per lane, no padded head slots and no
 // MFMA of its own.
 template <int BITS, int NH, int CMP, int PG, int X1>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
+__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
     static_assert(X1 == 0 || NH == 1, "the extra head is only for one head group");
-    __shared__ Smem4<NH, X1> sm;
+    // one LDS block per wave (dynamic: one or two waves per workgroup)
+    extern __shared__ __align__(16) unsigned char dyn_lds[];
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    Smem4<NH, X1>& sm = reinterpret_cast<Smem4<NH, X1>*>(dyn_lds)[wave];
     constexpr int WPU = BITS / 2;
     constexpr int NHD = 4 * NH;   // head slots of the head groups
     constexpr int NHX = NHD + X1;  // all head slots
@@ -425,12 +437,13 @@ void k_decode4(DecodeArgs a) {
     constexpr float MAGIC = 12582912.f;  // 1.5 * 2^23: x + MAGIC rounds x to an integer
     constexpr uint32_t MAGIC_BITS = 0x4B400000u;
     // output role: head 4*hg + G, column n; A-operand role: row 4*h + j (digit j of head 4*hg + h)
-    const int l = threadIdx.x, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
+    const int l = threadIdx.x & 63, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
     // wave = (head chunk, stream, split), the chunk slowest: the chunks of a stream read the
-    // same tiles, n_streams * n_split workgroups apart, which keeps them on one XCD when that
-    // distance is a multiple of 8
-    const int split = blockIdx.x % a.n_split;
-    const int cs = blockIdx.x / a.n_split;
+    // same tiles, n_streams * n_split waves apart, which keeps them on one XCD when that
+    // distance in workgroups is a multiple of 8.  In pair mode a workgroup's two waves are the
+    // stream's two splits.
+    const int split = a.pair ? wave : blockIdx.x % a.n_split;
+    const int cs = a.pair ? blockIdx.x : blockIdx.x / a.n_split;
     const int stream = cs % a.n_streams, chunk = cs / a.n_streams;
     const int g = min(a.g_chunk, a.g - chunk * a.g_chunk);  // query heads of this wave
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
@@ -538,7 +551,7 @@ void k_decode4(DecodeArgs a) {
         for (int idx = l; idx < NH * 32; idx += 64)
             sm.qp[idx >> 5][3][(idx >> 4) & 1][idx & 15] = make_uint4(0u, 0u, 0u, 0u);
         if (X1 && l < 8) sm.qp4[X1 ? 3 : 0][l >> 2][l & 3] = make_uint4(0u, 0u, 0u, 0u);
-        __syncthreads();
+        wave_sync();
         if (a.rotate) lds_hadamard<NHX>(sm.q, g);
         // q~ role: head 4*hg + G, channels 8n .. 8n + 7 (rotated and normalized, or as given)
         const float qs = a.rotate ? kInvSqrt128 : 1.f;
@@ -564,12 +577,12 @@ void k_decode4(DecodeArgs a) {
 
         // One tile: consume cur, prefetch tile id_next into nxt.
         auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
-            __syncthreads();  // the previous tile is done with sm.aux / sm.qp / sm.hv
+            wave_sync();  // the previous tile is done with sm.aux / sm.qp / sm.hv
             // aux rows a_K, b_K, s2_K (keys: per channel), a_V, b_V, s2_V (values: per token)
             stage_half_aux<CMP>(sm.aux, 0, cur.ak, l);
             stage_half_aux<CMP>(sm.aux, 3, cur.av, l);
             load_aux(nxt, id_next);
-            __syncthreads();
+            wave_sync();
             uint32_t kw[2][8 * WPU], vw[2][8 * WPU];
 #pragma unroll
             for (int s = 0; s < 2; ++s)
@@ -659,7 +672,7 @@ void k_decode4(DecodeArgs a) {
                     }
                 }
             }
-            __syncthreads();
+            wave_sync();
 
             // logits of head 4*hg + G, token 64*sg + 16*tau + n.  Tokens outer, head groups
             // inner: the code planes of a token block are extracted once and used at once.
@@ -875,7 +888,7 @@ void k_decode4(DecodeArgs a) {
             uint32_t v2[kRC];  // value row t, channels 2 l, 2 l + 1
 #pragma unroll
             for (int t = 0; t < kRC; ++t) v2[t] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t, cn - 1) * kD)[l];
-            __syncthreads();  // the previous chunk is done with sm.p / sm.hv
+            wave_sync();  // the previous chunk is done with sm.p / sm.hv
             // logits of head 4*hg + G, token 16*tau + n
             float lg[NH][2];
             v4f r4 = {0.f, 0.f, 0.f, 0.f};
@@ -917,7 +930,7 @@ void k_decode4(DecodeArgs a) {
                 for (int tau = 0; tau < 2; ++tau) sm.p[4 * hg + G][16 * tau + n] = real ? lg[hg][tau] : 0.f;
                 if (n == 0) sm.hv[4 * hg + G][2] = real ? alpha : 1.f;
             }
-            __syncthreads();
+            wave_sync();
             // o_plain[h] = alpha o_plain[h] + sum over the chunk's rows of p[h][t] V[t]
 #pragma unroll
             for (int hh = 0; hh < NHX; ++hh) {
@@ -942,9 +955,76 @@ void k_decode4(DecodeArgs a) {
     float lt[NH];
 #pragma unroll
     for (int hg = 0; hg < NH; ++hg) lt[hg] = row_sum(l_run[hg]);
-    const float lt4 = X1 ? wave_sum(l4) : 0.f;
-    if (a.n_split == 1) {
+    float lt4 = X1 ? wave_sum(l4) : 0.f;
+    if (a.pair) {
+        // Log-sum-exp of the two splits inside the workgroup: wave 1 leaves its part (rotated
+        // output per head and channel, plain output, m and l per head slot) in its own LDS
+        // block, wave 0 adds it to its own, rescaled to the common maximum, and writes the output
+        // as an unsplit stream does.
+        float* xb = reinterpret_cast<float*>(reinterpret_cast<Smem4<NH, X1>*>(dyn_lds) + 1);
+        float* xo = xb;                 // [NHX][kD] rotated output
+        float* xp = xb + NHX * kD;      // [NHX][kD] plain output
+        float* xm = xb + 2 * NHX * kD;  // [NHX] m, then [NHX] l of wave 1, then [NHX] m of wave 0
+        static_assert(sizeof(Smem4<NH, X1>) >= sizeof(float) * (2 * NHX * kD + 3 * NHX), "pair exchange area");
+        if (wave == 1) {
+#pragma unroll
+            for (int hg = 0; hg < NH; ++hg) {
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) xo[(4 * hg + G) * kD + 16 * mt + n] = orot[hg][mt];
+                if (n == 0) {
+                    xm[4 * hg + G] = m_run[hg];
+                    xm[NHX + 4 * hg + G] = lt[hg];
+                }
+            }
+            if constexpr (X1) {
+#pragma unroll
+                for (int q = 0; q < 2; ++q) xo[(NHX - 1) * kD + 16 * (4 * q + G) + n] = orot4[q];
+                if (l == 0) {
+                    xm[NHX - 1] = m4;
+                    xm[2 * NHX - 1] = lt4;
+                }
+            }
+#pragma unroll
+            for (int hh = 0; hh < NHX; ++hh)
+                *reinterpret_cast<float2*>(xp + hh * kD + 2 * l) = make_float2(oplain[hh][0], oplain[hh][1]);
+        }
         __syncthreads();
+        if (wave == 1) return;
+        // weights of the two parts of every head slot (0 for a part without probability mass)
+        auto weights = [](float m0, float m1, float& w0, float& w1) {
+            const float M = fmaxf(m0, m1);
+            w0 = m0 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
+            w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
+        };
+#pragma unroll
+        for (int hg = 0; hg < NH; ++hg) {
+            float w0, w1;
+            weights(m_run[hg], xm[4 * hg + G], w0, w1);
+#pragma unroll
+            for (int mt = 0; mt < 8; ++mt) orot[hg][mt] = fmaf(w1, xo[(4 * hg + G) * kD + 16 * mt + n], w0 * orot[hg][mt]);
+            lt[hg] = fmaf(w1, xm[NHX + 4 * hg + G], w0 * lt[hg]);
+            if (n == 0) xm[2 * NHX + 4 * hg + G] = m_run[hg];
+        }
+        if constexpr (X1) {
+            float w0, w1;
+            weights(m4, xm[NHX - 1], w0, w1);
+#pragma unroll
+            for (int q = 0; q < 2; ++q) orot4[q] = fmaf(w1, xo[(NHX - 1) * kD + 16 * (4 * q + G) + n], w0 * orot4[q]);
+            lt4 = fmaf(w1, xm[2 * NHX - 1], w0 * lt4);
+            if (l == 0) xm[3 * NHX - 1] = m4;
+        }
+        wave_sync();
+#pragma unroll
+        for (int hh = 0; hh < NHX; ++hh) {
+            float w0, w1;
+            weights(xm[2 * NHX + hh], xm[hh], w0, w1);
+            const float2 y = *reinterpret_cast<const float2*>(xp + hh * kD + 2 * l);
+            oplain[hh][0] = fmaf(w1, y.x, w0 * oplain[hh][0]);
+            oplain[hh][1] = fmaf(w1, y.y, w0 * oplain[hh][1]);
+        }
+    }
+    if (a.n_split == 1 || a.pair) {
+        wave_sync();
 #pragma unroll
         for (int hg = 0; hg < NH; ++hg) {
             if (4 * hg + G < g) {
@@ -958,7 +1038,7 @@ void k_decode4(DecodeArgs a) {
             for (int q = 0; q < 2; ++q) sm.q[NHX - 1][16 * (4 * q + G) + n] = orot4[q];
             if (l == 0) sm.hv[NHX - 1][3] = lt4;
         }
-        __syncthreads();
+        wave_sync();
         if (a.rotate) lds_hadamard<NHX>(sm.q, g);
         const float rs = a.rotate ? kInvSqrt128 : 1.f;
 #pragma unroll
@@ -1165,20 +1245,25 @@ __global__ __launch_bounds__(256) void k_decode_merge(DecodeArgs a) {
 template <int BITS, int GQ, int CMP>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
-    const dim3 grid((unsigned)(streams * a.n_split * a.n_chunk));
+    // pair mode: one two-wave workgroup per (stream, chunk); else one wave per workgroup
+    const int wpg = a.pair ? 2 : 1;
+    const dim3 grid((unsigned)(streams * a.n_chunk * (a.pair ? 1 : a.n_split))), block(64 * wpg);
     const bool pg = a.block_table != nullptr;
     if constexpr (GQ == 4) {
-        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 0>), grid, dim3(64), 0, stream, a);
-        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0, 0>), grid, dim3(64), 0, stream, a);
+        const size_t lds = wpg * sizeof(Smem4<1, 0>);
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 0>), grid, block, lds, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0, 0>), grid, block, lds, stream, a);
     } else if constexpr (GQ == 5) {
-        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 1>), grid, dim3(64), 0, stream, a);
-        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0, 1>), grid, dim3(64), 0, stream, a);
+        const size_t lds = wpg * sizeof(Smem4<1, 1>);
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 1, 1>), grid, block, lds, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 1, CMP, 0, 1>), grid, block, lds, stream, a);
     } else if constexpr (GQ == 8) {
-        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 1, 0>), grid, dim3(64), 0, stream, a);
-        else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0, 0>), grid, dim3(64), 0, stream, a);
+        const size_t lds = wpg * sizeof(Smem4<2, 0>);
+        if (pg) hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 1, 0>), grid, block, lds, stream, a);
+        else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0, 0>), grid, block, lds, stream, a);
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || a.n_split == 1) return e;
+    if (e != hipSuccess || a.n_split == 1 || a.pair) return e;
     const size_t heads = (size_t)batch * a.n_q;
     if (a.n_split >= kMergeWide)
         hipLaunchKernelGGL(k_decode_merge<4>, dim3((unsigned)heads), dim3(256), 0, stream, a);
@@ -1216,6 +1301,7 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     int want = (1024 * per_simd + streams - 1) / streams;
     if (want > nb / 2) want = nb / 2;
     p.n_res = 0;
+    p.pair = 0;
     if (want <= 1) {
         p.n_split = 1;
         p.blocks_per_split = nb > 0 ? nb : 1;
@@ -1234,11 +1320,14 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     else if ((long long)streams * (p.n_split + 1) <= 1024LL * per_simd)
         p.n_res = 1;
     p.n_split += p.n_res;
+    // Two splits and no sink/residual split: the two waves of one workgroup, merged there (no
+    // partials in memory, no merge launch).
+    p.pair = p.n_split == 2 && p.n_res == 0;
     return p;
 }
 
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan) {
-    if (plan.n_split == 1) return 0;
+    if (plan.n_split == 1 || plan.pair) return 0;
     return (size_t)batch * n_q * plan.n_split * kPart * sizeof(float);
 }
 
@@ -1270,6 +1359,7 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
     a.n_res = plan.n_res;
+    a.pair = plan.pair;
     a.n_streams = c.batch * c.n_kv;
     a.n_chunk = plan.n_chunk;
     a.g_chunk = plan.g_chunk;

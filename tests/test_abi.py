@@ -175,8 +175,8 @@ def test_decode_validation(K):
 
 
 def test_decode_noalloc_validation(K):
-    """The allocation-free decode validates like kvarn_decode_attention, and rejects a plan whose
-    split partials exceed its scratch array, all before any HIP call."""
+    """The allocation-free decode validates like kvarn_decode_attention, before any HIP call, and
+    every split plan's partials fit its scratch array."""
     p = K.kvarn_params_init(2)
     c = _HostCache(K, batch=2, n_kv=2, max_blocks=32)
     keep, buf = _fake(1 << 20)
@@ -186,13 +186,13 @@ def test_decode_noalloc_validation(K):
         with pytest.raises(K.KVarNError) as e:
             K.kvarn_decode_attention_noalloc(p, c, **{**good, **kw}, stream=0)
         assert e.value.status == code, kw
-    # 1023 streams of 16 query heads over 2048 tiles: the largest split plan, 32.5 MiB of partials
+    # The largest split plan: 1023 streams of 8 query heads in 3 splits (one round of waves
+    # overshot by the rounding up), 24.4 MiB of partials.  (Plans of two splits and no
+    # sink/residual split merge inside the workgroup and need none: 1023 streams of 16 heads.)
     big = _HostCache(K, batch=1023, n_kv=1, max_blocks=2049)
-    need = K.kvarn_decode_workspace_bytes(p, big, 16, 2048 * 128)
-    assert need > K.NOALLOC_SCRATCH_BYTES
-    with pytest.raises(K.KVarNError) as e:
-        K.kvarn_decode_attention_noalloc(p, big, **{**good, "n_q": 16, "max_len_hint": 2048 * 128}, stream=0)
-    assert e.value.status == -5
+    need = K.kvarn_decode_workspace_bytes(p, big, 8, 2048 * 128)
+    assert need == 1023 * 8 * 3 * 1040 <= K.NOALLOC_SCRATCH_BYTES
+    assert K.kvarn_decode_workspace_bytes(p, big, 16, 2048 * 128) == 0
 
 
 def test_no_cpu_fallback(K, monkeypatch, tmp_path):
