@@ -199,6 +199,31 @@ def test_decode_residual_placement(K, batch, n_sink, body, n_split):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
+@pytest.mark.parametrize("bits,n_q,batch,aux,n_sink", [
+    (2, 8, 768, 0, 0),     # group 4: 1536 streams, two splits each
+    (4, 8, 512, 1, 128),   # group 4 at 4 bits, compact aux, a sink for the second split
+    (2, 10, 512, 0, 0),    # group 5 (the extra-head variant)
+    (4, 16, 512, 0, 100),  # group 8 (two head groups) at 4 bits, partial sink chunks
+])
+def test_decode_pair_mode(K, bits, n_q, batch, aux, n_sink):
+    """Streams of exactly two splits and no sink/residual split (batch x 2 kv heads just below two
+    rounds of resident waves) run as the two waves of one workgroup and merge there: no
+    workspace.  Ragged lengths give a second split without body tiles, a sink-only and an empty
+    sequence."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", bits=bits, n_q=n_q, n_kv=2, batch=batch, aux=aux, n_sink=n_sink,
+                               context=n_sink + 4 * 128 + 77)
+    L = built.length
+    cycle = [L, n_sink + 2 * 128 + 5, n_sink + 128, n_sink + 3, n_sink // 2, 0, L - 64]
+    lens = [cycle[i % len(cycle)] for i in range(batch)]
+    built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    # (one split per stream would leave a third of the wave slots empty: the plan is two splits)
+    assert K.kvarn_decode_workspace_bytes(built.params, built.cache, n_q, L + 1) == 0
+    q = workloads.decode_queries(built, seed=10)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
 @pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (10, 2), (12, 2), (32, 2)])
 def test_decode_group_sizes(K, n_q, n_kv):
     """Every query-group size class (1 .. 4, 5, 6 .. 8, 9 .. 16 take different kernels), with a
