@@ -212,7 +212,7 @@ KVARN_API int kvarn_append_token(const kvarn_params *p, const kvarn_cache *cache
                        int32_t dtype, int32_t host_len_before, hipStream_t stream);
 
 /* Workspace bytes that kvarn_decode_attention needs for these sizes (split partials); 0 when
- * the plan keeps every (sequence, kv head) in one split or in two splits merged inside one
+ * the plan keeps every (sequence, kv head) in one split or in a few splits merged inside one
  * workgroup, or when an argument is invalid. */
 KVARN_API size_t kvarn_decode_workspace_bytes(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q,
                                     int32_t max_len_hint);

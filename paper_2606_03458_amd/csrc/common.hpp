@@ -59,7 +59,7 @@ struct DecodePlan {
     int n_chunk, g_chunk;  // query heads of a group taken in n_chunk chunks of up to g_chunk (<= 8)
     int n_split;           // splits per (sequence, kv head)
     int n_res;             // splits (the last of n_split) that hold only sink + residual chunks
-    int pair;              // 1: two splits per stream, the two waves of one workgroup (no partials)
+    int group;             // > 1: the n_split splits of a stream are the waves of one workgroup
     int blocks_per_split;  // body tiles per body split
     int max_blocks_used;   // upper bound of body tiles over the batch
 };

@@ -41,6 +41,7 @@ typedef unsigned v2u __attribute__((ext_vector_type(2)));
 
 constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
 constexpr int kRC = 32;     // bf16 tokens (sink / residual) per chunk
+constexpr int kMaxGroup = 8;  // splits of a stream that may form one workgroup
 
 // A fixed-point grid is only formed for a maximum above this; below it the values are taken
 // as zero.  For p~ this drops a tile whose probabilities are all below 1e-30 relative to the
@@ -71,7 +72,7 @@ struct DecodeArgs {
     int n_res;         // splits that hold only sink + residual chunks (the last n_res of n_split)
     int n_streams;     // batch * n_kv
     int n_chunk, g_chunk;  // head chunks per stream and heads per chunk (row-digit kernels)
-    int pair;          // 1: the two splits of a stream are the two waves of one workgroup
+    int group;         // > 1: the n_split splits of a stream are the waves of one workgroup
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
 };
 
@@ -418,7 +419,7 @@ __device__ __forceinline__ uint32_t rows_digit_reduce_scatter4(uint32_t x0, uint
 // channels 16 (4 q + G) + n (sg, q = 0, 1): two values per lane, no padded head slots and no
 // MFMA of its own.
 template <int BITS, int NH, int CMP, int PG, int X1>
-__global__ __launch_bounds__(128) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
+__global__ __launch_bounds__(64 * kMaxGroup) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
     static_assert(X1 == 0 || NH == 1, "the extra head is only for one head group");
     // one LDS block per wave (dynamic: one or two waves per workgroup)
@@ -440,10 +441,10 @@ void k_decode4(DecodeArgs a) {
     const int l = threadIdx.x & 63, G = l >> 4, n = l & 15, h = (l >> 2) & 3, j = l & 3;
     // wave = (head chunk, stream, split), the chunk slowest: the chunks of a stream read the
     // same tiles, n_streams * n_split waves apart, which keeps them on one XCD when that
-    // distance in workgroups is a multiple of 8.  In pair mode a workgroup's two waves are the
-    // stream's two splits.
-    const int split = a.pair ? wave : blockIdx.x % a.n_split;
-    const int cs = a.pair ? blockIdx.x : blockIdx.x / a.n_split;
+    // distance in workgroups is a multiple of 8.  In group mode a workgroup's waves are the
+    // stream's splits.
+    const int split = a.group > 1 ? wave : blockIdx.x % a.n_split;
+    const int cs = a.group > 1 ? blockIdx.x : blockIdx.x / a.n_split;
     const int stream = cs % a.n_streams, chunk = cs / a.n_streams;
     const int g = min(a.g_chunk, a.g - chunk * a.g_chunk);  // query heads of this wave
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
@@ -956,74 +957,96 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
     for (int hg = 0; hg < NH; ++hg) lt[hg] = row_sum(l_run[hg]);
     float lt4 = X1 ? wave_sum(l4) : 0.f;
-    if (a.pair) {
-        // Log-sum-exp of the two splits inside the workgroup: wave 1 leaves its part (rotated
-        // output per head and channel, plain output, m and l per head slot) in its own LDS
-        // block, wave 0 adds it to its own, rescaled to the common maximum, and writes the output
-        // as an unsplit stream does.
-        float* xb = reinterpret_cast<float*>(reinterpret_cast<Smem4<NH, X1>*>(dyn_lds) + 1);
-        float* xo = xb;                 // [NHX][kD] rotated output
-        float* xp = xb + NHX * kD;      // [NHX][kD] plain output
-        float* xm = xb + 2 * NHX * kD;  // [NHX] m, then [NHX] l of wave 1, then [NHX] m of wave 0
-        static_assert(sizeof(Smem4<NH, X1>) >= sizeof(float) * (2 * NHX * kD + 3 * NHX), "pair exchange area");
-        if (wave == 1) {
+    if (a.group > 1) {
+        // Log-sum-exp of the splits inside the workgroup: every wave w > 0 leaves its part
+        // (rotated output per head and channel, plain output, m and l per head slot) in its own
+        // LDS block; wave 0 rescales all parts to their common maximum, adds them in wave order
+        // and writes the output as an unsplit stream does.
+        auto part = [&](int w) { return reinterpret_cast<float*>(reinterpret_cast<Smem4<NH, X1>*>(dyn_lds) + w); };
+        // in each block: [NHX][kD] rotated output, [NHX][kD] plain output, [NHX] m, [NHX] l; block
+        // 1 also [NHX] m of wave 0
+        constexpr int XP = NHX * kD, XM = 2 * NHX * kD;
+        static_assert(sizeof(Smem4<NH, X1>) >= sizeof(float) * (2 * NHX * kD + 3 * NHX), "exchange area");
+        if (wave > 0) {
+            float* xb = part(wave);
 #pragma unroll
             for (int hg = 0; hg < NH; ++hg) {
 #pragma unroll
-                for (int mt = 0; mt < 8; ++mt) xo[(4 * hg + G) * kD + 16 * mt + n] = orot[hg][mt];
+                for (int mt = 0; mt < 8; ++mt) xb[(4 * hg + G) * kD + 16 * mt + n] = orot[hg][mt];
                 if (n == 0) {
-                    xm[4 * hg + G] = m_run[hg];
-                    xm[NHX + 4 * hg + G] = lt[hg];
+                    xb[XM + 4 * hg + G] = m_run[hg];
+                    xb[XM + NHX + 4 * hg + G] = lt[hg];
                 }
             }
             if constexpr (X1) {
 #pragma unroll
-                for (int q = 0; q < 2; ++q) xo[(NHX - 1) * kD + 16 * (4 * q + G) + n] = orot4[q];
+                for (int q = 0; q < 2; ++q) xb[(NHX - 1) * kD + 16 * (4 * q + G) + n] = orot4[q];
                 if (l == 0) {
-                    xm[NHX - 1] = m4;
-                    xm[2 * NHX - 1] = lt4;
+                    xb[XM + NHX - 1] = m4;
+                    xb[XM + 2 * NHX - 1] = lt4;
                 }
             }
 #pragma unroll
             for (int hh = 0; hh < NHX; ++hh)
-                *reinterpret_cast<float2*>(xp + hh * kD + 2 * l) = make_float2(oplain[hh][0], oplain[hh][1]);
+                *reinterpret_cast<float2*>(xb + XP + hh * kD + 2 * l) = make_float2(oplain[hh][0], oplain[hh][1]);
         }
         __syncthreads();
-        if (wave == 1) return;
-        // weights of the two parts of every head slot (0 for a part without probability mass)
-        auto weights = [](float m0, float m1, float& w0, float& w1) {
-            const float M = fmaxf(m0, m1);
-            w0 = m0 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m0 - M);
-            w1 = m1 == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m1 - M);
-        };
+        if (wave > 0) return;
+        const int np = a.group;
+        auto ex = [](float m, float M) { return m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - M); };
 #pragma unroll
         for (int hg = 0; hg < NH; ++hg) {
-            float w0, w1;
-            weights(m_run[hg], xm[4 * hg + G], w0, w1);
+            const int hs = 4 * hg + G;
+            float M = m_run[hg];
+            for (int w = 1; w < np; ++w) M = fmaxf(M, part(w)[XM + hs]);
+            const float w0 = ex(m_run[hg], M);
+            lt[hg] *= w0;
 #pragma unroll
-            for (int mt = 0; mt < 8; ++mt) orot[hg][mt] = fmaf(w1, xo[(4 * hg + G) * kD + 16 * mt + n], w0 * orot[hg][mt]);
-            lt[hg] = fmaf(w1, xm[NHX + 4 * hg + G], w0 * lt[hg]);
-            if (n == 0) xm[2 * NHX + 4 * hg + G] = m_run[hg];
+            for (int mt = 0; mt < 8; ++mt) orot[hg][mt] *= w0;
+            for (int w = 1; w < np; ++w) {
+                const float* xb = part(w);
+                const float ww = ex(xb[XM + hs], M);
+                lt[hg] = fmaf(ww, xb[XM + NHX + hs], lt[hg]);
+#pragma unroll
+                for (int mt = 0; mt < 8; ++mt) orot[hg][mt] = fmaf(ww, xb[hs * kD + 16 * mt + n], orot[hg][mt]);
+            }
+            if (n == 0) part(1)[XM + 2 * NHX + hs] = m_run[hg];
         }
         if constexpr (X1) {
-            float w0, w1;
-            weights(m4, xm[NHX - 1], w0, w1);
+            float M = m4;
+            for (int w = 1; w < np; ++w) M = fmaxf(M, part(w)[XM + NHX - 1]);
+            const float w0 = ex(m4, M);
+            lt4 *= w0;
+            orot4[0] *= w0;
+            orot4[1] *= w0;
+            for (int w = 1; w < np; ++w) {
+                const float* xb = part(w);
+                const float ww = ex(xb[XM + NHX - 1], M);
+                lt4 = fmaf(ww, xb[XM + 2 * NHX - 1], lt4);
 #pragma unroll
-            for (int q = 0; q < 2; ++q) orot4[q] = fmaf(w1, xo[(NHX - 1) * kD + 16 * (4 * q + G) + n], w0 * orot4[q]);
-            lt4 = fmaf(w1, xm[2 * NHX - 1], w0 * lt4);
-            if (l == 0) xm[3 * NHX - 1] = m4;
+                for (int q = 0; q < 2; ++q) orot4[q] = fmaf(ww, xb[(NHX - 1) * kD + 16 * (4 * q + G) + n], orot4[q]);
+            }
+            if (l == 0) part(1)[XM + 3 * NHX - 1] = m4;
         }
         wave_sync();
 #pragma unroll
         for (int hh = 0; hh < NHX; ++hh) {
-            float w0, w1;
-            weights(xm[2 * NHX + hh], xm[hh], w0, w1);
-            const float2 y = *reinterpret_cast<const float2*>(xp + hh * kD + 2 * l);
-            oplain[hh][0] = fmaf(w1, y.x, w0 * oplain[hh][0]);
-            oplain[hh][1] = fmaf(w1, y.y, w0 * oplain[hh][1]);
+            const float m0 = part(1)[XM + 2 * NHX + hh];
+            float M = m0;
+            for (int w = 1; w < np; ++w) M = fmaxf(M, part(w)[XM + hh]);
+            const float w0 = ex(m0, M);
+            oplain[hh][0] *= w0;
+            oplain[hh][1] *= w0;
+            for (int w = 1; w < np; ++w) {
+                const float* xb = part(w);
+                const float ww = ex(xb[XM + hh], M);
+                const float2 y = *reinterpret_cast<const float2*>(xb + XP + hh * kD + 2 * l);
+                oplain[hh][0] = fmaf(ww, y.x, oplain[hh][0]);
+                oplain[hh][1] = fmaf(ww, y.y, oplain[hh][1]);
+            }
         }
     }
-    if (a.n_split == 1 || a.pair) {
+    if (a.n_split == 1 || a.group > 1) {
         wave_sync();
 #pragma unroll
         for (int hg = 0; hg < NH; ++hg) {
@@ -1245,9 +1268,9 @@ __global__ __launch_bounds__(256) void k_decode_merge(DecodeArgs a) {
 template <int BITS, int GQ, int CMP>
 hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
     const int streams = batch * a.n_kv;
-    // pair mode: one two-wave workgroup per (stream, chunk); else one wave per workgroup
-    const int wpg = a.pair ? 2 : 1;
-    const dim3 grid((unsigned)(streams * a.n_chunk * (a.pair ? 1 : a.n_split))), block(64 * wpg);
+    // group mode: one workgroup of n_split waves per (stream, chunk); else one wave per workgroup
+    const int wpg = a.group > 1 ? a.group : 1;
+    const dim3 grid((unsigned)(streams * a.n_chunk * (a.group > 1 ? 1 : a.n_split))), block(64 * wpg);
     const bool pg = a.block_table != nullptr;
     if constexpr (GQ == 4) {
         const size_t lds = wpg * sizeof(Smem4<1, 0>);
@@ -1263,7 +1286,7 @@ hipError_t launch_cfg(const DecodeArgs& a, int batch, hipStream_t stream) {
         else hipLaunchKernelGGL((k_decode4<BITS, 2, CMP, 0, 0>), grid, block, lds, stream, a);
     }
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || a.n_split == 1 || a.pair) return e;
+    if (e != hipSuccess || a.n_split == 1 || a.group > 1) return e;
     const size_t heads = (size_t)batch * a.n_q;
     if (a.n_split >= kMergeWide)
         hipLaunchKernelGGL(k_decode_merge<4>, dim3((unsigned)heads), dim3(256), 0, stream, a);
@@ -1301,7 +1324,7 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     int want = (1024 * per_simd + streams - 1) / streams;
     if (want > nb / 2) want = nb / 2;
     p.n_res = 0;
-    p.pair = 0;
+    p.group = 0;
     if (want <= 1) {
         p.n_split = 1;
         p.blocks_per_split = nb > 0 ? nb : 1;
@@ -1320,14 +1343,15 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     else if ((long long)streams * (p.n_split + 1) <= 1024LL * per_simd)
         p.n_res = 1;
     p.n_split += p.n_res;
-    // Two splits and no sink/residual split: the two waves of one workgroup, merged there (no
-    // partials in memory, no merge launch).
-    p.pair = p.n_split == 2 && p.n_res == 0;
+    // Up to kMaxGroup splits: the waves of one workgroup, merged there (no partials in memory,
+    // no merge launch), when their LDS blocks fit the workgroup's 64 KB.
+    const size_t blk = gc <= 4 ? sizeof(Smem4<1, 0>) : gc == 5 ? sizeof(Smem4<1, 1>) : sizeof(Smem4<2, 0>);
+    if (p.n_split <= kMaxGroup && p.n_split * blk <= 65536) p.group = p.n_split;
     return p;
 }
 
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan) {
-    if (plan.n_split == 1 || plan.pair) return 0;
+    if (plan.n_split == 1 || plan.group > 1) return 0;
     return (size_t)batch * n_q * plan.n_split * kPart * sizeof(float);
 }
 
@@ -1359,7 +1383,7 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.n_split = plan.n_split;
     a.bps = plan.blocks_per_split;
     a.n_res = plan.n_res;
-    a.pair = plan.pair;
+    a.group = plan.group;
     a.n_streams = c.batch * c.n_kv;
     a.n_chunk = plan.n_chunk;
     a.g_chunk = plan.g_chunk;

@@ -224,6 +224,31 @@ def test_decode_pair_mode(K, bits, n_q, batch, aux, n_sink):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
+@pytest.mark.parametrize("bits,n_q,batch,tiles,aux,n_sink,splits", [
+    (2, 32, 64, 8, 0, 0, 5),     # group 4: 4 body splits + one sink/residual split
+    (2, 32, 64, 12, 1, 0, 6),    # group 4, compact aux: 6 body splits, the last takes the chunks
+    (4, 32, 64, 12, 0, 128, 4),  # group 4 at 4 bits with a sink: 4 body splits
+    (2, 40, 48, 12, 0, 0, 6),    # group 5 (the extra-head variant): 6 body splits
+    (2, 64, 64, 12, 0, 0, 4),    # group 8 (two head groups): 4 body splits
+])
+def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink, splits):
+    """Streams of a few splits (batch x 8 kv heads, 512 or 384 streams) run as the waves of one
+    workgroup and merge there: no workspace.  Ragged lengths leave later splits without body
+    tiles, and give sink-only and empty sequences."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", bits=bits, n_q=n_q, n_kv=8, batch=batch, aux=aux, n_sink=n_sink,
+                               context=n_sink + tiles * 128 + 77)
+    L = built.length
+    cycle = [L, n_sink + 5 * 128 + 1, n_sink + 2 * 128 + 100, n_sink + 40, n_sink // 2, 0, L - 100, n_sink + 128]
+    lens = [cycle[i % len(cycle)] for i in range(batch)]
+    built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    # (the same plan with partials in memory would need batch * n_q * splits * 1040 bytes)
+    assert K.kvarn_decode_workspace_bytes(built.params, built.cache, n_q, L + 1) == 0
+    q = workloads.decode_queries(built, seed=11)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
 @pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (10, 2), (12, 2), (32, 2)])
 def test_decode_group_sizes(K, n_q, n_kv):
     """Every query-group size class (1 .. 4, 5, 6 .. 8, 9 .. 16 take different kernels), with a
