@@ -41,7 +41,9 @@ typedef unsigned v2u __attribute__((ext_vector_type(2)));
 
 constexpr int kPart = 260;  // floats per partial: m, l, 2 pad, o_rot[128], o_plain[128]
 constexpr int kRC = 32;     // bf16 tokens (sink / residual) per chunk
-constexpr int kMaxGroup = 8;  // splits of a stream that may form one workgroup
+// splits of a stream that may form one workgroup (one wave per SIMD; groups of 5-6 waves
+// measured slower than the separate merge on the 2-bit streaming runs)
+constexpr int kMaxGroup = 4;
 
 // A fixed-point grid is only formed for a maximum above this; below it the values are taken
 // as zero.  For p~ this drops a tile whose probabilities are all below 1e-30 relative to the

@@ -186,13 +186,13 @@ def test_decode_noalloc_validation(K):
         with pytest.raises(K.KVarNError) as e:
             K.kvarn_decode_attention_noalloc(p, c, **{**good, **kw}, stream=0)
         assert e.value.status == code, kw
-    # The largest plan with partials in memory: 409 streams of 8 query heads in 6 splits (whose
-    # six LDS blocks exceed a workgroup's 64 KB, so they do not merge inside one), 19.5 MiB.
-    # Plans of up to 8 splits whose blocks fit merge inside the workgroup and need none
-    # (1023 streams of 8 heads in 3 splits, of 16 heads in 2).
-    mid = _HostCache(K, batch=409, n_kv=1, max_blocks=2049)
+    # The largest plan with partials in memory: 511 streams of 8 query heads in 5 splits (more
+    # than merge inside one workgroup), 20.3 MiB.  Plans of up to 4 splits whose LDS blocks fit
+    # merge inside the workgroup and need none (1023 streams of 8 heads in 3 splits, of 16 heads
+    # in 2).
+    mid = _HostCache(K, batch=511, n_kv=1, max_blocks=2049)
     need = K.kvarn_decode_workspace_bytes(p, mid, 8, 2048 * 128)
-    assert need == 409 * 8 * 6 * 1040 <= K.NOALLOC_SCRATCH_BYTES
+    assert need == 511 * 8 * 5 * 1040 <= K.NOALLOC_SCRATCH_BYTES
     big = _HostCache(K, batch=1023, n_kv=1, max_blocks=2049)
     assert K.kvarn_decode_workspace_bytes(p, big, 8, 2048 * 128) == 0
     assert K.kvarn_decode_workspace_bytes(p, big, 16, 2048 * 128) == 0

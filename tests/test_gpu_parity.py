@@ -224,16 +224,16 @@ def test_decode_pair_mode(K, bits, n_q, batch, aux, n_sink):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
-@pytest.mark.parametrize("bits,n_q,batch,tiles,aux,n_sink,splits", [
-    (2, 32, 64, 8, 0, 0, 5),     # group 4: 4 body splits + one sink/residual split
-    (2, 32, 64, 12, 1, 0, 6),    # group 4, compact aux: 6 body splits, the last takes the chunks
-    (4, 32, 64, 12, 0, 128, 4),  # group 4 at 4 bits with a sink: 4 body splits
-    (2, 40, 48, 12, 0, 0, 6),    # group 5 (the extra-head variant): 6 body splits
-    (2, 64, 64, 12, 0, 0, 4),    # group 8 (two head groups): 4 body splits
+@pytest.mark.parametrize("bits,n_q,batch,tiles,aux,n_sink", [
+    (2, 32, 80, 8, 0, 0),     # group 4: 4 body splits, the last takes the residual chunks
+    (2, 32, 96, 6, 1, 0),     # group 4, compact aux: 3 body splits + one sink/residual split
+    (4, 32, 64, 12, 0, 128),  # group 4 at 4 bits with a sink: 4 body splits
+    (2, 40, 48, 6, 0, 0),     # group 5 (the extra-head variant): 3 body splits + one residual split
+    (2, 64, 64, 12, 0, 0),    # group 8 (two head groups): 4 body splits
 ])
-def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink, splits):
-    """Streams of a few splits (batch x 8 kv heads, 512 or 384 streams) run as the waves of one
-    workgroup and merge there: no workspace.  Ragged lengths leave later splits without body
+def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink):
+    """Streams of four splits (batch x 8 kv heads, 384 to 768 streams) run as the four waves of
+    one workgroup and merge there: no workspace.  Ragged lengths leave later splits without body
     tiles, and give sink-only and empty sequences."""
     from paper_2606_03458_amd import workloads
     built, _ = workloads.build("llama", bits=bits, n_q=n_q, n_kv=8, batch=batch, aux=aux, n_sink=n_sink,
@@ -242,7 +242,6 @@ def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink, splits):
     cycle = [L, n_sink + 5 * 128 + 1, n_sink + 2 * 128 + 100, n_sink + 40, n_sink // 2, 0, L - 100, n_sink + 128]
     lens = [cycle[i % len(cycle)] for i in range(batch)]
     built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
-    # (the same plan with partials in memory would need batch * n_q * splits * 1040 bytes)
     assert K.kvarn_decode_workspace_bytes(built.params, built.cache, n_q, L + 1) == 0
     q = workloads.decode_queries(built, seed=11)
     out = _decode(K, built, q)
