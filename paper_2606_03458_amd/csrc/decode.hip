@@ -24,8 +24,9 @@
 // a (split, sequence, kv head, head chunk).  An unsplit stream's one wave takes sink + residual
 // after its body tiles; a split stream's sink and residual chunks get splits of their own (one
 // per chunk when the waves fit), which run beside the body splits.  A single split writes the
-// final output directly (inverse rotation in LDS); several splits write partials that the merge
-// kernel combines by log-sum-exp.
+// final output directly (inverse rotation in LDS); up to four splits of a stream are the waves of
+// one workgroup and combine by log-sum-exp through LDS before writing it; more write partials
+// that the merge kernel combines.
 #include <algorithm>
 
 #include "common.hpp"
@@ -424,7 +425,7 @@ template <int BITS, int NH, int CMP, int PG, int X1>
 __global__ __launch_bounds__(64 * kMaxGroup) __attribute__((amdgpu_waves_per_eu(BITS == 2 && NH == 1 && !X1 ? 3 : 2, 8)))
 void k_decode4(DecodeArgs a) {
     static_assert(X1 == 0 || NH == 1, "the extra head is only for one head group");
-    // one LDS block per wave (dynamic: one or two waves per workgroup)
+    // one LDS block per wave (dynamic: one to kMaxGroup waves per workgroup)
     extern __shared__ __align__(16) unsigned char dyn_lds[];
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     Smem4<NH, X1>& sm = reinterpret_cast<Smem4<NH, X1>*>(dyn_lds)[wave];
