@@ -246,6 +246,19 @@ def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink):
     q = workloads.decode_queries(built, seed=11)
     out = _decode(K, built, q)
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+    # the same cache behind a block table over a permuted pool: bit-equal
+    c = built.cache
+    B, H, MB = c.batch, c.n_kv, c.max_blocks
+    paged = K.Cache(built.params, B, H, MB, n_phys=B * MB)
+    perm = torch.randperm(B * MB, generator=torch.Generator().manual_seed(bits + n_q)).cuda()
+    paged.block_table.copy_(perm.view(B, MB).to(torch.int32))
+    for src, dst in ((c.k_body, paged.k_body), (c.v_body, paged.v_body)):
+        dst.index_copy_(0, perm, src.permute(0, 2, 1, 3).reshape(B * MB, H, -1))
+    for f in ("k_resid", "v_resid", "k_sink", "v_sink", "seq_len"):
+        if getattr(c, f) is not None:
+            getattr(paged, f).copy_(getattr(c, f))
+    built.cache = paged
+    assert torch.equal(_decode(K, built, q), out)
 
 
 @pytest.mark.parametrize("n_q,n_kv", [(2, 2), (4, 2), (6, 2), (8, 2), (10, 2), (12, 2), (32, 2)])

@@ -134,7 +134,7 @@ def test_paged_every_kernel(K, bits, aux, g):
     """Every decode kernel (code width x aux format x query-group class 1-4, 5, 6-8, 9-16) on a
     permuted pool: bit-equal to the dense layout and within the output bar of the oracle, with
     ragged lengths (a residual, an exact block boundary, a sequence shorter than one block)."""
-    lens = [9 * 128 + 77, 3 * 128, 90]  # 9 body tiles: the plan splits the longest stream in two
+    lens = [9 * 128 + 77, 3 * 128, 90]  # 9 body tiles: split streams, merged by the merge kernel
     B, H, MB = len(lens), 2, 10
     k, v, cu = _prompts(lens, H, torch.bfloat16, seed=11 + bits + 2 * aux + g)
     p = K.kvarn_params_init(bits, aux_format=aux)
