@@ -230,10 +230,11 @@ def test_decode_pair_mode(K, bits, n_q, batch, aux, n_sink):
     (4, 32, 64, 12, 0, 128),  # group 4 at 4 bits with a sink: 4 body splits
     (2, 40, 48, 6, 0, 0),     # group 5 (the extra-head variant): 3 body splits + one residual split
     (2, 64, 64, 12, 0, 0),    # group 8 (two head groups): 4 body splits
+    (2, 128, 48, 12, 0, 0),   # group 16 (two chunks of 8 heads, a workgroup per chunk): 3 body splits
 ])
 def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink):
-    """Streams of four splits (batch x 8 kv heads, 384 to 768 streams) run as the four waves of
-    one workgroup and merge there: no workspace.  Ragged lengths leave later splits without body
+    """Streams of three or four splits (batch x 8 kv heads, 384 to 768 streams) run as the waves
+    of one workgroup and merge there: no workspace.  Ragged lengths leave later splits without body
     tiles, and give sink-only and empty sequences."""
     from paper_2606_03458_amd import workloads
     built, _ = workloads.build("llama", bits=bits, n_q=n_q, n_kv=8, batch=batch, aux=aux, n_sink=n_sink,
