@@ -317,23 +317,29 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
                 }
             }
         }
+        // Cross-lane stages as one multiply-add each, x + p * B with B = +1 in the lower lane of
+        // a pair and -1 in the upper one: the upper lane then holds -(a - b) instead of a - b.
+        // Partners always hold values of the same sign, so the signs stay consistent and every
+        // value is exactly +- the butterfly's (round to nearest is symmetric); after the four
+        // stages lane tc holds (-1)^popcount(tc) times it, which the final scaling removes.
 #pragma unroll
         for (int m = 1; m < 16; m <<= 1) {  // channel stride 8*m lives in lane tc ^ m
-            const bool upper = (L.tc & m) != 0;
+            const float B = (L.tc & m) ? -1.f : 1.f;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     // partners ^1 and ^2 by DPP quad permutes, ^4 and ^8 through the LDS crossbar
                     const float p = m == 1 ? dppf<0xB1>(x[i][j]) : (m == 2 ? dppf<0x4E>(x[i][j]) : __shfl_xor(x[i][j], m));
-                    x[i][j] = upper ? (p - x[i][j]) : (x[i][j] + p);
+                    x[i][j] = fmaf(p, B, x[i][j]);
                 }
             }
         }
+        const float scale = (__builtin_popcount(L.tc) & 1) ? -kInvSqrt128 : kInvSqrt128;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) x[i][j] *= kInvSqrt128;
+            for (int j = 0; j < 8; ++j) x[i][j] *= scale;
         }
     }
 
