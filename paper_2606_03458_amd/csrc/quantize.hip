@@ -531,9 +531,14 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         float den[8];
 #pragma unroll
         for (int m = 0; m < 8; ++m) den[m] = mx[m] > mn[m] ? mx[m] - mn[m] : 1.f;
+        // With fp32 aux the offset is the group minimum itself, so v - off >= 0 exactly, and at
+        // the group maximum the quotient is qmax within a few ulps (correctly rounded step and
+        // reciprocal, or division): rounding lands in [0, qmax] without a clamp.  The compact
+        // aux rounds the offset to binary16 and the step up to E4M3, so its codes are clamped.
         auto code = [&](float v, int m) -> uint32_t {
             const float u = kExact ? ((v - off[m]) * qmax) / den[m] : (v - off[m]) * inv_s[m];
-            return (uint32_t)clampf(rintf(u), 0.f, qmax);
+            if constexpr (COMPACT) return (uint32_t)clampf(rintf(u), 0.f, qmax);
+            else return (uint32_t)rintf(u);
         };
         if (kind == KVARN_KEYS) {
 #pragma unroll
