@@ -535,32 +535,35 @@ __device__ void quantize_tile(const void* src, bool bf16, int64_t tstride, int k
         // the group maximum the quotient is qmax within a few ulps (correctly rounded step and
         // reciprocal, or division): rounding lands in [0, qmax] without a clamp.  The compact
         // aux rounds the offset to binary16 and the step up to E4M3, so its codes are clamped.
+        // The code in the low byte of a word: u + 1.5 * 2^23 rounds u (0 <= u <= 15) to the
+        // nearest integer, ties to even as rintf, into the low mantissa bits.
         auto code = [&](float v, int m) -> uint32_t {
-            const float u = kExact ? ((v - off[m]) * qmax) / den[m] : (v - off[m]) * inv_s[m];
-            if constexpr (COMPACT) return (uint32_t)clampf(rintf(u), 0.f, qmax);
-            else return (uint32_t)rintf(u);
+            float u = kExact ? ((v - off[m]) * qmax) / den[m] : (v - off[m]) * inv_s[m];
+            if constexpr (COMPACT) u = clampf(u, 0.f, qmax);  // (before rounding: the same codes)
+            return __float_as_uint(u + 12582912.f);
+        };
+        // four such words -> their low bytes in order, by two byte permutes
+        auto pack4 = [](uint32_t a, uint32_t b, uint32_t c, uint32_t d) {
+            return __builtin_amdgcn_perm(__builtin_amdgcn_perm(d, c, 0x0c0c0400u), __builtin_amdgcn_perm(b, a, 0x0c0c0400u),
+                                         0x05040100u);
         };
         if (kind == KVARN_KEYS) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                uint32_t lo = 0, hi = 0;
+                uint32_t q[8];
 #pragma unroll
-                for (int j = 0; j < 8; ++j) {
-                    const uint32_t q = code(x[i][j], j);
-                    if (j < 4) lo |= q << (8 * j); else hi |= q << (8 * (j - 4));
-                }
-                *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tr + i) * kD + 8 * L.tc]) = make_uint2(lo, hi);
+                for (int j = 0; j < 8; ++j) q[j] = code(x[i][j], j);
+                *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tr + i) * kD + 8 * L.tc]) =
+                    make_uint2(pack4(q[0], q[1], q[2], q[3]), pack4(q[4], q[5], q[6], q[7]));
             }
         } else {
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                uint32_t lo = 0, hi = 0;
+                uint32_t q[8];
 #pragma unroll
-                for (int i = 0; i < 8; ++i) {
-                    const uint32_t q = code(x[i][j], i);
-                    if (i < 4) lo |= q << (8 * i); else hi |= q << (8 * (i - 4));
-                }
-                *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tc + j) * kG + 8 * L.tr]) = make_uint2(lo, hi);
+                for (int i = 0; i < 8; ++i) q[i] = code(x[i][j], i);
+                *reinterpret_cast<uint2*>(&sm.codes[(8 * L.tc + j) * kG + 8 * L.tr]) =
+                    make_uint2(pack4(q[0], q[1], q[2], q[3]), pack4(q[4], q[5], q[6], q[7]));
             }
         }
     };
