@@ -81,14 +81,29 @@ __device__ __forceinline__ float across_rows(float v) {
 // values.
 // With STAT, the same LDS round also carries one (max, min) pair per wave (xmax, xmin: the
 // wave's values in, the workgroup's out).
+// The four rows of the wave go as a reduce-scatter: permlane16_swap of two different values
+// leaves, in every lane, the even-row and odd-row partials of one of them (rows 0, 2: the first,
+// rows 1, 3: the second), and permlane32_swap of two such words the two half sums; the operands
+// and their order are those of across_rows, so the sums are the same, but no lane computes
+// results it then discards.  Row r of a wave ends with columns 8 tc + r and 8 tc + 4 + r.
 template <class Op, bool STAT = false>
 __device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& buf, const Lane& L,
                                             float* xmax = nullptr, float* xmin = nullptr) {
+    float t[4], rr[2];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s[j] = across_rows<Op>(s[j]);
-    if (L.lane < 16) {
+    for (int p = 0; p < 4; ++p) {
+        const auto x = __builtin_amdgcn_permlane16_swap(__float_as_uint(s[2 * p]), __float_as_uint(s[2 * p + 1]), false, false);
+        t[p] = Op::f(__uint_as_float(x[0]), __uint_as_float(x[1]));
+    }
 #pragma unroll
-        for (int j = 0; j < 8; ++j) sm.red[buf][L.wave][8 * L.tc + j] = s[j];
+    for (int k = 0; k < 2; ++k) {
+        const auto y = __builtin_amdgcn_permlane32_swap(__float_as_uint(t[2 * k]), __float_as_uint(t[2 * k + 1]), false, false);
+        rr[k] = Op::f(__uint_as_float(y[0]), __uint_as_float(y[1]));
+    }
+    {
+        const int r = L.lane >> 4;
+        sm.red[buf][L.wave][8 * L.tc + r] = rr[0];
+        sm.red[buf][L.wave][8 * L.tc + 4 + r] = rr[1];
     }
     if (STAT && L.lane == 0) {
         sm.rstat[buf][L.wave][0] = *xmax;
