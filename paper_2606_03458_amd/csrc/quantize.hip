@@ -17,6 +17,7 @@ constexpr int kThreads = 256;
 
 struct QuantSmem {
     float red[2][4][kD];          // column partials [buffer][wave][channel]
+    alignas(16) float tot[2][kD];  // column totals [buffer][channel]
     float rpick[4][4][8];         // row variances of each DPP row [wave][row][token], for the row update
     float rstat[2][4][2];         // per-wave row max / min [buffer][wave][max, min]
     alignas(16) uint8_t codes[kG * kD];  // keys: [token][channel]; values: [channel][token]
@@ -114,11 +115,17 @@ __device__ __forceinline__ void reduce_cols(float (&s)[8], QuantSmem& sm, int& b
         *xmax = fmax_any(fmax_any(sm.rstat[buf][0][0], sm.rstat[buf][1][0]), fmax_any(sm.rstat[buf][2][0], sm.rstat[buf][3][0]));
         *xmin = fmin_any(fmin_any(sm.rstat[buf][0][1], sm.rstat[buf][1][1]), fmin_any(sm.rstat[buf][2][1], sm.rstat[buf][3][1]));
     }
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int c = 8 * L.tc + j;
-        s[j] = Op::f(Op::f(Op::f(sm.red[buf][0][c], sm.red[buf][1][c]), sm.red[buf][2][c]), sm.red[buf][3][c]);
+    // each column's four wave partials are combined once (thread c of the first two waves),
+    // then every thread of the channel block reads its eight totals
+    if (L.tid < kD) {
+        const int c = L.tid;
+        sm.tot[buf][c] = Op::f(Op::f(Op::f(sm.red[buf][0][c], sm.red[buf][1][c]), sm.red[buf][2][c]), sm.red[buf][3][c]);
     }
+    __syncthreads();
+    const float4 lo = *reinterpret_cast<const float4*>(&sm.tot[buf][8 * L.tc]);
+    const float4 hi = *reinterpret_cast<const float4*>(&sm.tot[buf][8 * L.tc + 4]);
+    s[0] = lo.x; s[1] = lo.y; s[2] = lo.z; s[3] = lo.w;
+    s[4] = hi.x; s[5] = hi.y; s[6] = hi.z; s[7] = hi.w;
     buf ^= 1;
 }
 
