@@ -122,7 +122,8 @@ typedef enum { KVARN_AUX_F32 = 0, KVARN_AUX_COMPACT = 1 } kvarn_aux_format;
  *   err_word         one uint32 or NULL: a kernel that finds no room sets bit 0 and drops
  *                    the write instead of writing out of bounds (a backstop only: the host
  *                    check of kvarn_append_token catches overflow from its length hint); an
- *                    invalid block id (below) sets bit 1.
+ *                    invalid block id (below) sets bit 1; a fused append step over a
+ *                    sequence whose length is not the host's (kvarn_append_decode) sets bit 2.
  *   block_table      NULL for the dense body above.  Otherwise the paged layout of serving
  *                    engines: block_table is [batch][max_blocks] int32 on the device and
  *                    k_body, v_body are pools of n_phys blocks, [n_phys][n_kv] tiles each;
@@ -234,6 +235,30 @@ KVARN_API size_t kvarn_decode_workspace_bytes(const kvarn_params *p, const kvarn
 KVARN_API int kvarn_decode_attention(const kvarn_params *p, const kvarn_cache *cache, int32_t n_q, const void *q,
                            int32_t q_dtype, void *out, int32_t out_dtype, float sm_scale, int32_t max_len_hint,
                            void *workspace, size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * One decode step of a lock-step batch (Fig. 4: each generated token is appended to the cache,
+ * then attended over it, new token included; App. D three-region cache): the results of
+ * kvarn_append_token(p, cache, k_new, v_new, kv_dtype, host_len_before) followed by
+ * kvarn_decode_attention(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale,
+ * host_len_before + 1, workspace, workspace_bytes), bit for bit, in cache and output.
+ *   host_len_before  required: the length of every sequence before the call (seq_len on the
+ *           device must hold it).
+ *   workspace  as for kvarn_decode_attention with max_len_hint = host_len_before + 1.
+ * When the token goes to the residual without filling it, is bf16 and k_new, v_new are 16-byte
+ * aligned, the append runs inside the decode launch: the wave that attends the residual's last
+ * chunk reads the new row from k_new / v_new and stores it into the residual, and seq_len is
+ * set to host_len_before + 1 without the decode reading it; one launch instead of two.  A
+ * sequence whose seq_len is not host_len_before is then left unchanged and bit 2 of err_word
+ * is set (its output is not meaningful).  Otherwise (a sink token, a flush, fp32 tokens) the
+ * call runs the two entry points' kernels in turn.
+ * Errors: those of both entry points, all checked before anything is enqueued; KVARN_EINVAL for
+ * host_len_before < 0 or = INT32_MAX.
+ */
+KVARN_API int kvarn_append_decode(const kvarn_params *p, const kvarn_cache *cache, const void *k_new,
+                                  const void *v_new, int32_t kv_dtype, int32_t host_len_before, int32_t n_q,
+                                  const void *q, int32_t q_dtype, void *out, int32_t out_dtype, float sm_scale,
+                                  void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Decode attention that allocates nothing, for callers that cannot allocate device memory:

@@ -52,6 +52,11 @@ int check_params(const kvarn_params* p) {
     return KVARN_OK;
 }
 
+// Arguments of an append; *flush: whether the call has to launch the flush (always without the
+// length hint, else when the token fills the residual).
+int append_check(const kvarn_params* p, const kvarn_cache* cache, const void* k_new, const void* v_new, int32_t dtype,
+                 int32_t host_len_before, bool* flush);
+
 QParams qparams(const kvarn_params* p) {
     return QParams{p->bits, p->varn_iters, p->var_min, p->var_max, p->log_lo, p->log_hi,
                    p->aux_format == KVARN_AUX_COMPACT ? 1 : 0, p->rotate};
@@ -73,6 +78,32 @@ int check_cache(const kvarn_params* p, const kvarn_cache* c) {
 }
 
 int check_dtype(int32_t d) { return (d == KVARN_F32 || d == KVARN_BF16) ? KVARN_OK : KVARN_EINVAL; }
+
+int append_check(const kvarn_params* p, const kvarn_cache* cache, const void* k_new, const void* v_new, int32_t dtype,
+                 int32_t host_len_before, bool* flush) {
+    int st = check_params(p);
+    if (st) return st;
+    st = check_cache(p, cache);
+    if (st) return st;
+    if (check_dtype(dtype)) return KVARN_EINVAL;
+    if (!k_new || !v_new) return KVARN_EINVAL;
+    const size_t va = dtype == KVARN_BF16 ? 8 : 16;
+    if (!aligned(k_new, va) || !aligned(v_new, va)) return KVARN_EINVAL;
+    if (host_len_before < -1) return KVARN_EINVAL;
+    *flush = true;
+    if (host_len_before >= 0) {
+        const int len = host_len_before;
+        *flush = false;
+        if (len >= p->n_sink) {
+            const int r = (len - p->n_sink) % kG, nb = (len - p->n_sink) / kG;
+            if (r == kG - 1) {
+                if (nb >= cache->max_blocks) return KVARN_ECAPACITY;
+                *flush = true;
+            }
+        }
+    }
+    return KVARN_OK;
+}
 
 }  // namespace
 
@@ -138,27 +169,9 @@ int kvarn_quantize_block(const kvarn_params* p, int32_t kind, const void* x, int
 
 int kvarn_append_token(const kvarn_params* p, const kvarn_cache* cache, const void* k_new, const void* v_new,
                        int32_t dtype, int32_t host_len_before, hipStream_t stream) {
-    int st = check_params(p);
-    if (st) return st;
-    st = check_cache(p, cache);
-    if (st) return st;
-    if (check_dtype(dtype)) return KVARN_EINVAL;
-    if (!k_new || !v_new) return KVARN_EINVAL;
-    const size_t va = dtype == KVARN_BF16 ? 8 : 16;
-    if (!aligned(k_new, va) || !aligned(v_new, va)) return KVARN_EINVAL;
-    if (host_len_before < -1) return KVARN_EINVAL;
     bool flush = true;
-    if (host_len_before >= 0) {
-        const int len = host_len_before;
-        flush = false;
-        if (len >= p->n_sink) {
-            const int r = (len - p->n_sink) % kG, nb = (len - p->n_sink) / kG;
-            if (r == kG - 1) {
-                if (nb >= cache->max_blocks) return KVARN_ECAPACITY;
-                flush = true;
-            }
-        }
-    }
+    const int st = append_check(p, cache, k_new, v_new, dtype, host_len_before, &flush);
+    if (st) return st;
     hipError_t e = launch_append(*cache, p->n_sink, k_new, v_new, dtype == KVARN_BF16, stream);
     if (e != hipSuccess) return KVARN_EHIP;
     if (flush) {
@@ -193,11 +206,12 @@ size_t kvarn_decode_workspace_bytes(const kvarn_params* p, const kvarn_cache* ca
 
 namespace {
 
-// Validation, planning and launch shared by both decode entry points.  ws == nullptr with
-// use_scratch: the partials go to the library's per-device scratch array.
-int decode_impl(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q, int32_t q_dtype,
-                void* out, int32_t out_dtype, float sm_scale, int32_t max_len_hint, void* workspace,
-                size_t workspace_bytes, bool use_scratch, hipStream_t stream) {
+// Validation and planning shared by the decode entry points; nothing is enqueued.  ws == nullptr
+// with use_scratch: the partials go to the library's per-device scratch array (*workspace is set
+// to it).
+int decode_check(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q, int32_t q_dtype,
+                 const void* out, int32_t out_dtype, float sm_scale, int32_t max_len_hint, void** workspace,
+                 size_t workspace_bytes, bool use_scratch, DecodePlan* plan) {
     int st = check_params(p);
     if (st) return st;
     st = check_cache(p, cache);
@@ -206,19 +220,35 @@ int decode_impl(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, co
     if (check_dtype(q_dtype) || check_dtype(out_dtype)) return KVARN_EINVAL;
     if (!q || !out || !std::isfinite(sm_scale) || max_len_hint < 0) return KVARN_EINVAL;
     if (!aligned(q, 4) || !aligned(out, 8)) return KVARN_EINVAL;
-    const DecodePlan plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
-    const size_t need = decode_workspace_bytes(cache->batch, n_q, plan);
+    *plan = plan_decode(cache->batch, cache->n_kv, n_q, p->bits, max_len_hint, p->n_sink, cache->max_blocks);
+    const size_t need = decode_workspace_bytes(cache->batch, n_q, *plan);
     if (use_scratch) {
         if (need > KVARN_NOALLOC_SCRATCH_BYTES) return KVARN_EWORKSPACE;
-        workspace = nullptr;
-        if (need > 0 && scratch_ptr(&workspace) != hipSuccess) return KVARN_EHIP;
-    } else if (need > 0 && (!workspace || workspace_bytes < need || !aligned(workspace, 16))) {
+        *workspace = nullptr;
+        if (need > 0 && scratch_ptr(workspace) != hipSuccess) return KVARN_EHIP;
+    } else if (need > 0 && (!*workspace || workspace_bytes < need || !aligned(*workspace, 16))) {
         return KVARN_EWORKSPACE;
     }
-    hipError_t e = launch_decode(*cache, p->bits, p->aux_format == KVARN_AUX_COMPACT, p->rotate, p->n_sink, n_q, q,
-                                 q_dtype == KVARN_BF16, out, out_dtype == KVARN_BF16, sm_scale, plan,
-                                 static_cast<float*>(workspace), stream);
+    return KVARN_OK;
+}
+
+int decode_launch(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q, int32_t q_dtype,
+                  void* out, int32_t out_dtype, float sm_scale, const DecodePlan& plan, void* workspace,
+                  hipStream_t stream, const StepAppend* step = nullptr) {
+    const hipError_t e = launch_decode(*cache, p->bits, p->aux_format == KVARN_AUX_COMPACT, p->rotate, p->n_sink, n_q,
+                                       q, q_dtype == KVARN_BF16, out, out_dtype == KVARN_BF16, sm_scale, plan,
+                                       static_cast<float*>(workspace), stream, step);
     return e == hipSuccess ? KVARN_OK : KVARN_EHIP;
+}
+
+int decode_impl(const kvarn_params* p, const kvarn_cache* cache, int32_t n_q, const void* q, int32_t q_dtype,
+                void* out, int32_t out_dtype, float sm_scale, int32_t max_len_hint, void* workspace,
+                size_t workspace_bytes, bool use_scratch, hipStream_t stream) {
+    DecodePlan plan;
+    const int st = decode_check(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, max_len_hint, &workspace,
+                                workspace_bytes, use_scratch, &plan);
+    if (st) return st;
+    return decode_launch(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, plan, workspace, stream);
 }
 
 }  // namespace
@@ -236,6 +266,28 @@ int kvarn_decode_attention_noalloc(const kvarn_params* p, const kvarn_cache* cac
                                    int32_t q_dtype, void* out, int32_t out_dtype, float sm_scale,
                                    int32_t max_len_hint, hipStream_t stream) {
     return decode_impl(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, max_len_hint, nullptr, 0, true, stream);
+}
+
+int kvarn_append_decode(const kvarn_params* p, const kvarn_cache* cache, const void* k_new, const void* v_new,
+                        int32_t kv_dtype, int32_t host_len_before, int32_t n_q, const void* q, int32_t q_dtype,
+                        void* out, int32_t out_dtype, float sm_scale, void* workspace, size_t workspace_bytes,
+                        hipStream_t stream) {
+    if (host_len_before < 0 || host_len_before == INT32_MAX) return KVARN_EINVAL;
+    bool flush = true;
+    int st = append_check(p, cache, k_new, v_new, kv_dtype, host_len_before, &flush);
+    if (st) return st;
+    DecodePlan plan;
+    st = decode_check(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, host_len_before + 1, &workspace,
+                      workspace_bytes, false, &plan);
+    if (st) return st;
+    if (kv_dtype == KVARN_BF16 && host_len_before >= p->n_sink && !flush && aligned(k_new, 16) && aligned(v_new, 16)) {
+        const StepAppend step{host_len_before, k_new, v_new};
+        return decode_launch(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, plan, workspace, stream, &step);
+    }
+    hipError_t e = launch_append(*cache, p->n_sink, k_new, v_new, kv_dtype == KVARN_BF16, stream);
+    if (e == hipSuccess && flush) e = launch_flush(qparams(p), *cache, p->n_sink, true, stream);
+    if (e != hipSuccess) return KVARN_EHIP;
+    return decode_launch(p, cache, n_q, q, q_dtype, out, out_dtype, sm_scale, plan, workspace, stream);
 }
 
 }  // extern "C"

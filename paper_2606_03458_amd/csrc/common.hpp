@@ -67,8 +67,15 @@ struct DecodePlan {
 DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int n_sink, int max_blocks);
 size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan);
 
+// A lock-step decode step's token, appended by the decode launch itself (bf16 rows [batch][n_kv][128],
+// 16-byte aligned; len_before >= n_sink and the token does not fill the residual).
+struct StepAppend {
+    int len_before;
+    const void* k_new;
+    const void* v_new;
+};
 hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate, int n_sink, int n_q, const void* q,
                          bool q_bf16, void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
-                         hipStream_t stream);
+                         hipStream_t stream, const StepAppend* step = nullptr);
 
 }  // namespace kvarn

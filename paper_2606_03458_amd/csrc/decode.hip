@@ -45,6 +45,9 @@ constexpr int kRC = 32;     // bf16 tokens (sink / residual) per chunk
 // splits of a stream that may form one workgroup (one wave per SIMD; groups of 5-6 waves
 // measured slower than the separate merge on the 2-bit streaming runs)
 constexpr int kMaxGroup = 4;
+// body tiles below which a stream planned with at most kMaxGroup splits keeps one for its sink
+// and residual chunks
+constexpr int kShortBody = 48;
 
 // A fixed-point grid is only formed for a maximum above this; below it the values are taken
 // as zero.  For p~ this drops a tile whose probabilities are all below 1e-30 relative to the
@@ -56,11 +59,11 @@ constexpr float kTinyMax = 1e-30f;
 struct DecodeArgs {
     const uint8_t* k_body;
     const uint8_t* v_body;
-    const uint16_t* k_resid;
-    const uint16_t* v_resid;
+    uint16_t* k_resid;  // written only by a fused append (step_len > 0)
+    uint16_t* v_resid;
     const uint16_t* k_sink;
     const uint16_t* v_sink;
-    const int32_t* seq_len;
+    int32_t* seq_len;   // read, and written only by a fused append
     const void* q;
     int q_bf16;
     void* out;
@@ -77,6 +80,12 @@ struct DecodeArgs {
     int n_chunk, g_chunk;  // head chunks per stream and heads per chunk (row-digit kernels)
     int group;         // > 1: the n_split splits of a stream are the waves of one workgroup
     float* ws;         // [batch][n_q][n_split][kPart] when n_split > 1
+    // Fused append of a lock-step step: > 0 the common length of the sequences with the token of
+    // k_new / v_new ([batch][n_kv][kD] bf16) appended as their last residual row; 0: lengths
+    // from seq_len and no append.
+    int step_len;
+    const uint16_t* k_new;
+    const uint16_t* v_new;
 };
 
 __device__ __forceinline__ v4i mfma_i8(v4i a, v4i b, v4i c) {
@@ -451,12 +460,17 @@ void k_decode4(DecodeArgs a) {
     const int stream = cs % a.n_streams, chunk = cs / a.n_streams;
     const int g = min(a.g_chunk, a.g - chunk * a.g_chunk);  // query heads of this wave
     const int b = stream / a.n_kv, kvh = stream % a.n_kv;
-    const int len = max(a.seq_len[b], 0);
+    // A fused append takes the step's length from the host.  The stored length must then be the
+    // one before the append, or the one after it (kv head 0 stores it, perhaps already); else the
+    // sequence is left as it is and bit 2 of err_word is set.
+    const int stored = a.seq_len[b];
+    const bool step_ok = a.step_len == 0 || stored == a.step_len - 1 || stored == a.step_len;
+    const int len = a.step_len > 0 ? a.step_len : max(stored, 0);
     const int ns = min(len, a.n_sink);
     const int nbody = min(len > a.n_sink ? (len - a.n_sink) / kG : 0, a.max_blocks);
     const int nr = len > a.n_sink ? (len - a.n_sink) % kG : 0;
-    // The last n_res splits hold only sink + residual chunks; without them the last body split
-    // takes those chunks too.
+    // The last n_res splits hold only sink + residual chunks; without them the body splits share
+    // those chunks.
     const int nbs = a.n_split - a.n_res;  // body splits
     const bool res_only = split >= nbs;
     const bool body_last = split == nbs - 1;  // takes any excess of body tiles
@@ -818,15 +832,16 @@ void k_decode4(DecodeArgs a) {
 
     // ---- sink and residual (bf16, unrotated) -------------------------------------------------
     // In chunks of kRC tokens: the sink's, then the residual's (no chunk spans both).  Split r of
-    // the n_res sink/residual splits takes chunks r, r + n_res, ...; without such splits the
-    // last body split takes them all.  A chunk's key rows (bf16 MFMA operands) and value rows
-    // (one dword per lane and row) are loaded together, one memory round trip per chunk.
+    // the n_res sink/residual splits takes chunks r, r + n_res, ...; without such splits, split r
+    // of the stream takes chunks r, r + n_split, ....  A chunk's key rows (bf16 MFMA operands)
+    // and value rows (one dword per lane and row) are loaded together, one memory round trip per
+    // chunk.
     float oplain[NHX][2];  // head hh, channel 2*l + jj (unrotated)
 #pragma unroll
     for (int hh = 0; hh < NHX; ++hh) oplain[hh][0] = oplain[hh][1] = 0.f;
     const int nsc = (ns + kRC - 1) / kRC, nch = nsc + (nr + kRC - 1) / kRC;
-    const int c0 = res_only ? split - nbs : 0, cstep = res_only ? a.n_res : 1;
-    if ((res_only || (a.n_res == 0 && body_last)) && c0 < nch) {
+    const int c0 = res_only ? split - nbs : split, cstep = res_only ? a.n_res : a.n_split;
+    if ((res_only || a.n_res == 0) && c0 < nch) {
         // A operand of group hg: row 4h holds q of head 4*hg + h rounded to bf16, row 4h + 1 the
         // remainder (zero for bf16 q), rows 4h + 2, 4h + 3 zero; lane (G, 4h + j) holds
         // q[.][32k + 8G ..].  Loads are clamped to a valid head, then masked.
@@ -878,11 +893,17 @@ void k_decode4(DecodeArgs a) {
             const size_t row0 = in_sink ? (size_t)stream * a.n_sink + t0 : (size_t)stream * kG + t0;
             const uint16_t* Kp = (in_sink ? a.k_sink : a.k_resid) + row0 * kD;
             const uint16_t* Vp = (in_sink ? a.v_sink : a.v_resid) + row0 * kD;
+            // A fused append's token is the residual's last row (of the last chunk): read from
+            // the input, and stored into the residual below.
+            const bool new_row = a.step_len > 0 && c == nch - 1;
+            const uint16_t* Klast = new_row ? a.k_new + (size_t)stream * kD : Kp + (size_t)(cn - 1) * kD;
+            const uint16_t* Vlast = new_row ? a.v_new + (size_t)stream * kD : Vp + (size_t)(cn - 1) * kD;
             // Rows past the chunk read its last row (in bounds) and are masked (p = 0).
             v8bf B[2][4];  // key rows 16 tau + n, channels 32 k + 8 G ..
 #pragma unroll
             for (int tau = 0; tau < 2; ++tau) {
-                const uint16_t* kr = Kp + (size_t)min(16 * tau + n, cn - 1) * kD + 8 * G;
+                const int i = 16 * tau + n;
+                const uint16_t* kr = (i < cn - 1 ? Kp + (size_t)i * kD : Klast) + 8 * G;
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
                     const uint4 u = *reinterpret_cast<const uint4*>(kr + 32 * k);
@@ -891,7 +912,16 @@ void k_decode4(DecodeArgs a) {
             }
             uint32_t v2[kRC];  // value row t, channels 2 l, 2 l + 1
 #pragma unroll
-            for (int t = 0; t < kRC; ++t) v2[t] = reinterpret_cast<const uint32_t*>(Vp + (size_t)min(t, cn - 1) * kD)[l];
+            for (int t = 0; t < kRC; ++t) v2[t] = reinterpret_cast<const uint32_t*>(t < cn - 1 ? Vp + (size_t)t * kD : Vlast)[l];
+            if (new_row && chunk == 0 && step_ok) {
+                // the token into the residual (one head chunk writes it), and the step's length
+                // (kv head 0 of the sequence writes it)
+                reinterpret_cast<uint32_t*>(a.k_resid + (row0 + cn - 1) * kD)[l] = reinterpret_cast<const uint32_t*>(Klast)[l];
+                reinterpret_cast<uint32_t*>(a.v_resid + (row0 + cn - 1) * kD)[l] = reinterpret_cast<const uint32_t*>(Vlast)[l];
+                if (kvh == 0 && l == 0) __hip_atomic_store(a.seq_len + b, a.step_len, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            if (new_row && chunk == 0 && !step_ok && l == 0 && a.err_word)
+                __hip_atomic_fetch_or(a.err_word, 4u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             wave_sync();  // the previous chunk is done with sm.p / sm.hv
             // logits of head 4*hg + G, token 16*tau + n
             float lg[NH][2];
@@ -1325,10 +1355,24 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     // decode + merge: 1 tile per split 15.6 us, 2 tiles 14.1 us, 4 tiles 17.8 us).
     const int per_simd = gc <= 4 ? (bits == 2 ? 3 : 2) : 2;
     int want = (1024 * per_simd + streams - 1) / streams;
+    // When kMaxGroup splits per stream already give every SIMD a wave, stop there: the splits
+    // then merge inside their workgroup (no partials, no merge launch) and fewer, longer splits
+    // spend less on per-split set-up, which beats filling the round (measured on 2-bit tiles,
+    // 512 streams: 231 us instead of 242 at 32k tokens, 18-21 us instead of 23 at 1k; 256
+    // streams: 123 us instead of 138 at 32k).
+    const bool few = (long long)streams * kMaxGroup >= 1024;
+    if (few && want > kMaxGroup) want = kMaxGroup;
+    // Short streams there give one of those waves to the sink and residual chunks, which then run
+    // beside the body tiles instead of after them, if the extra wave still fits the round (512
+    // streams at 1k tokens: 17.9 us instead of 20.1, at 4k 39.4 instead of 41.3; from 8k on the
+    // body splits gain more than that).
+    const bool res_split = few && nb < kShortBody &&
+                           (long long)streams * (std::min(want, kMaxGroup - 1) + 1) <= 1024LL * per_simd;
+    if (res_split && want > kMaxGroup - 1) want = kMaxGroup - 1;
     if (want > nb / 2) want = nb / 2;
     p.n_res = 0;
     p.group = 0;
-    if (want <= 1) {
+    if (want < 1 || (want == 1 && !res_split)) {
         p.n_split = 1;
         p.blocks_per_split = nb > 0 ? nb : 1;
         return p;
@@ -1340,8 +1384,12 @@ DecodePlan plan_decode(int batch, int n_kv, int n_q, int bits, int max_len, int 
     // splits -- when the extra waves still fit in the one round of resident waves (otherwise
     // body waves would wait for free slots behind them; measured: GQA-5 stress 28 % slower);
     // else one such split for all chunks if that fits.
+    // (With kMaxGroup splits or fewer per stream the body splits share the chunks instead, unless
+    // a short stream keeps a split for them, above.)
     const int chunks = (std::min(n_sink, std::max(max_len, 0)) + kRC - 1) / kRC + kG / kRC;
-    if ((long long)streams * (p.n_split + chunks) <= 1024LL * per_simd)
+    if (few)
+        p.n_res = res_split ? 1 : 0;
+    else if ((long long)streams * (p.n_split + chunks) <= 1024LL * per_simd)
         p.n_res = chunks;
     else if ((long long)streams * (p.n_split + 1) <= 1024LL * per_simd)
         p.n_res = 1;
@@ -1360,7 +1408,7 @@ size_t decode_workspace_bytes(int batch, int n_q, const DecodePlan& plan) {
 
 hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate, int n_sink, int n_q, const void* q,
                          bool q_bf16, void* out, bool out_bf16, float sm_scale, const DecodePlan& plan, float* ws,
-                         hipStream_t stream) {
+                         hipStream_t stream, const StepAppend* step) {
     DecodeArgs a;
     a.rotate = rotate;
     a.block_table = c.block_table;
@@ -1368,8 +1416,8 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.err_word = c.err_word;
     a.k_body = static_cast<const uint8_t*>(c.k_body);
     a.v_body = static_cast<const uint8_t*>(c.v_body);
-    a.k_resid = static_cast<const uint16_t*>(c.k_resid);
-    a.v_resid = static_cast<const uint16_t*>(c.v_resid);
+    a.k_resid = static_cast<uint16_t*>(c.k_resid);
+    a.v_resid = static_cast<uint16_t*>(c.v_resid);
     a.k_sink = static_cast<const uint16_t*>(c.k_sink);
     a.v_sink = static_cast<const uint16_t*>(c.v_sink);
     a.seq_len = c.seq_len;
@@ -1391,6 +1439,9 @@ hipError_t launch_decode(const kvarn_cache& c, int bits, int compact, int rotate
     a.n_chunk = plan.n_chunk;
     a.g_chunk = plan.g_chunk;
     a.ws = ws;
+    a.step_len = step ? step->len_before + 1 : 0;
+    a.k_new = step ? static_cast<const uint16_t*>(step->k_new) : nullptr;
+    a.v_new = step ? static_cast<const uint16_t*>(step->v_new) : nullptr;
     if (compact) return bits == 2 ? launch_bits<2, 1>(a, c.batch, stream) : launch_bits<4, 1>(a, c.batch, stream);
     return bits == 2 ? launch_bits<2, 0>(a, c.batch, stream) : launch_bits<4, 0>(a, c.batch, stream);
 }

@@ -20,7 +20,7 @@ STATUS = {0: "KVARN_OK", -1: "KVARN_EINVAL", -2: "KVARN_EUNSUPPORTED", -3: "KVAR
           -5: "KVARN_EWORKSPACE"}
 EXPORTS = ("kvarn_params_init", "kvarn_tile_bytes", "kvarn_cache_sizes", "kvarn_quantize_block", "kvarn_prefill",
            "kvarn_append_token", "kvarn_decode_workspace_bytes", "kvarn_decode_attention",
-           "kvarn_decode_attention_noalloc")
+           "kvarn_decode_attention_noalloc", "kvarn_append_decode")
 NOALLOC_SCRATCH_BYTES = 32 << 20  # KVARN_NOALLOC_SCRATCH_BYTES
 
 
@@ -79,6 +79,8 @@ def lib():
         L.kvarn_decode_attention.restype = ctypes.c_int
         L.kvarn_decode_attention_noalloc.argtypes = [P, C, i32, vp, i32, vp, i32, ctypes.c_float, i32, vp]
         L.kvarn_decode_attention_noalloc.restype = ctypes.c_int
+        L.kvarn_append_decode.argtypes = [P, C, vp, vp, i32, i32, i32, vp, i32, vp, i32, ctypes.c_float, vp, sz, vp]
+        L.kvarn_append_decode.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -176,6 +178,16 @@ def kvarn_decode_attention_noalloc(p: kvarn_params, cache: "Cache", n_q: int, q,
     st = lib().kvarn_decode_attention_noalloc(ctypes.byref(p), ctypes.byref(d), n_q, _ptr(q), q_dtype, _ptr(out),
                                               out_dtype, sm_scale, max_len_hint, _stream(stream))
     _check("kvarn_decode_attention_noalloc", st)
+
+
+def kvarn_append_decode(p: kvarn_params, cache: "Cache", k_new, v_new, kv_dtype: int, host_len_before: int, n_q: int,
+                        q, q_dtype: int, out, out_dtype: int, sm_scale: float, workspace, workspace_bytes: int,
+                        stream=None) -> None:
+    d = cache.desc()
+    st = lib().kvarn_append_decode(ctypes.byref(p), ctypes.byref(d), _ptr(k_new), _ptr(v_new), kv_dtype, host_len_before,
+                                   n_q, _ptr(q), q_dtype, _ptr(out), out_dtype, sm_scale, _ptr(workspace),
+                                   workspace_bytes, _stream(stream))
+    _check("kvarn_append_decode", st)
 
 
 # ------------------------------------------------------------------------------------------

@@ -174,6 +174,27 @@ def test_decode_validation(K):
     assert K.kvarn_decode_workspace_bytes(p, c, 8, -1) == 0
 
 
+def test_append_decode_validation(K):
+    """The fused step validates the arguments of both halves before enqueuing anything: an error in
+    the decode's arguments enqueues no append either."""
+    p = K.kvarn_params_init(2)
+    c = _HostCache(K, batch=2, n_kv=2, max_blocks=32)
+    keep, buf = _fake(1 << 20)
+    need = K.kvarn_decode_workspace_bytes(p, c, 8, 4096 + 1)
+    assert need > 0
+    good = dict(k_new=buf, v_new=buf, kv_dtype=1, host_len_before=4096, n_q=8, q=buf, q_dtype=1, out=buf,
+                out_dtype=1, sm_scale=0.088, workspace=buf, workspace_bytes=need)
+    for kw, code in [(dict(host_len_before=-1), -1), (dict(host_len_before=2 ** 31 - 1), -1), (dict(k_new=None), -1),
+                     (dict(v_new=buf + 2), -1), (dict(kv_dtype=5), -1), (dict(n_q=7), -1), (dict(q=None), -1),
+                     (dict(out=buf + 4), -1), (dict(sm_scale=float("inf")), -1),
+                     (dict(workspace_bytes=need - 1), -5), (dict(workspace=None), -5),
+                     # a flush that would need body tile max_blocks
+                     (dict(host_len_before=32 * 128 + 127), -3)]:
+        with pytest.raises(K.KVarNError) as e:
+            K.kvarn_append_decode(K.kvarn_params_init(2), c, **{**good, **kw}, stream=0)
+        assert e.value.status == code, kw
+
+
 def test_decode_noalloc_validation(K):
     """The allocation-free decode validates like kvarn_decode_attention, before any HIP call, and
     every split plan's partials fit its scratch array."""
@@ -186,13 +207,14 @@ def test_decode_noalloc_validation(K):
         with pytest.raises(K.KVarNError) as e:
             K.kvarn_decode_attention_noalloc(p, c, **{**good, **kw}, stream=0)
         assert e.value.status == code, kw
-    # The largest plan with partials in memory: 511 streams of 8 query heads in 5 splits (more
-    # than merge inside one workgroup), 20.3 MiB.  Plans of up to 4 splits whose LDS blocks fit
-    # merge inside the workgroup and need none (1023 streams of 8 heads in 3 splits, of 16 heads
-    # in 2).
-    mid = _HostCache(K, batch=511, n_kv=1, max_blocks=2049)
+    # The largest plan with partials in memory: 255 streams of 8 query heads in 9 splits, 18.2 MiB
+    # (from 256 streams on, 4 splits per stream give every SIMD a wave and the plan stops there).
+    # Plans of up to 4 splits whose LDS blocks fit merge inside the workgroup and need none (511
+    # streams of 8 heads in 4 splits, 1023 in 3, 1023 streams of 16 heads in 2).
+    mid = _HostCache(K, batch=255, n_kv=1, max_blocks=2049)
     need = K.kvarn_decode_workspace_bytes(p, mid, 8, 2048 * 128)
-    assert need == 511 * 8 * 5 * 1040 <= K.NOALLOC_SCRATCH_BYTES
+    assert need == 255 * 8 * 9 * 1040 <= K.NOALLOC_SCRATCH_BYTES
+    assert K.kvarn_decode_workspace_bytes(p, _HostCache(K, batch=511, n_kv=1, max_blocks=2049), 8, 2048 * 128) == 0
     big = _HostCache(K, batch=1023, n_kv=1, max_blocks=2049)
     assert K.kvarn_decode_workspace_bytes(p, big, 8, 2048 * 128) == 0
     assert K.kvarn_decode_workspace_bytes(p, big, 16, 2048 * 128) == 0

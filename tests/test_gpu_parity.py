@@ -177,12 +177,13 @@ def test_decode_variants(K, bits, n_sink, name):
 
 @pytest.mark.parametrize("batch,n_sink,body,n_split", [
     (2, 100, 20, 18),   # 10 body splits + one per sink / residual chunk (4 + 4)
-    (32, 0, 20, 11),    # 10 body splits + one split for all chunks (one per chunk would not fit)
-    (32, 0, 24, 12),    # 12 body splits, the last one also taking the chunks
+    (31, 0, 20, 11),    # 10 body splits + one split for all chunks (one per chunk would not fit)
+    (31, 0, 24, 12),    # 12 body splits sharing the chunks
 ])
 def test_decode_residual_placement(K, batch, n_sink, body, n_split):
     """The three places the split plan gives a stream's sink and residual chunks (32 tokens
-    each): a split per chunk, one split for all chunks, or the last body split.  Ragged lengths
+    each) when the partials go to memory (fewer than 256 streams): a split per chunk, one split
+    for all chunks, or the body splits in turn.  Ragged lengths
     give every residual size class (empty, one token, a partial and full chunks, 127 tokens) and a
     sink-only sequence; the split count is checked through the workspace size."""
     from paper_2606_03458_amd import workloads
@@ -206,8 +207,8 @@ def test_decode_residual_placement(K, batch, n_sink, body, n_split):
     (4, 16, 512, 0, 100),  # group 8 (two head groups) at 4 bits, partial sink chunks
 ])
 def test_decode_pair_mode(K, bits, n_q, batch, aux, n_sink):
-    """Streams of exactly two splits and no sink/residual split (batch x 2 kv heads just below two
-    rounds of resident waves) run as the two waves of one workgroup and merge there: no
+    """Streams of exactly two splits that share the sink/residual chunks (batch x 2 kv heads just
+    below two rounds of resident waves) run as the two waves of one workgroup and merge there: no
     workspace.  Ragged lengths give a second split without body tiles, a sink-only and an empty
     sequence."""
     from paper_2606_03458_amd import workloads
@@ -225,11 +226,13 @@ def test_decode_pair_mode(K, bits, n_q, batch, aux, n_sink):
 
 
 @pytest.mark.parametrize("bits,n_q,batch,tiles,aux,n_sink", [
-    (2, 32, 80, 8, 0, 0),     # group 4: 4 body splits, the last takes the residual chunks
+    (2, 32, 80, 8, 0, 0),     # group 4: 3 body splits + one sink/residual split (a short stream)
+    (2, 32, 64, 50, 0, 0),    # group 4: 4 body splits sharing the residual chunks
     (2, 32, 96, 6, 1, 0),     # group 4, compact aux: 3 body splits + one sink/residual split
-    (4, 32, 64, 12, 0, 128),  # group 4 at 4 bits with a sink: 4 body splits
+    (4, 32, 64, 12, 0, 128),  # group 4 at 4 bits with a sink: 3 body splits + one sink/residual split
+    (4, 32, 64, 50, 1, 100),  # the same at 4 bits, compact aux, 4 body splits sharing the chunks
     (2, 40, 48, 6, 0, 0),     # group 5 (the extra-head variant): 3 body splits + one residual split
-    (2, 64, 64, 12, 0, 0),    # group 8 (two head groups): 4 body splits
+    (2, 64, 64, 12, 0, 0),    # group 8 (two head groups): 3 body splits + one residual split
     (2, 128, 48, 12, 0, 0),   # group 16 (two chunks of 8 heads, a workgroup per chunk): 3 body splits
 ])
 def test_decode_group_mode(K, bits, n_q, batch, tiles, aux, n_sink):
