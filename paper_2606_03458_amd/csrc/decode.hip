@@ -23,10 +23,14 @@
 // pair hi + lo when it is fp32) and plain FMAs for p . v, in chunks of 32 tokens.  One wave owns
 // a (split, sequence, kv head, head chunk).  An unsplit stream's one wave takes sink + residual
 // after its body tiles; a split stream's sink and residual chunks get splits of their own (one
-// per chunk when the waves fit), which run beside the body splits.  A single split writes the
-// final output directly (inverse rotation in LDS); up to four splits of a stream are the waves of
-// one workgroup and combine by log-sum-exp through LDS before writing it; more write partials
-// that the merge kernel combines.
+// per chunk when the waves fit), which run beside the body splits, or the body splits share
+// them.  A single split writes the final output directly (inverse rotation in LDS); up to four
+// splits of a stream are the waves of one workgroup and combine by log-sum-exp through LDS
+// before writing it; more write partials that the merge kernel combines.
+//
+// A lock-step decode step can append its token in the same launch (Fig. 4): the new row is the
+// residual's last, read from the token input by the wave that attends that chunk, which also
+// stores it into the residual; the step's length comes from the host.
 #include <algorithm>
 
 #include "common.hpp"
