@@ -206,3 +206,70 @@ def test_gpu_append_property(K, case):
     raw = lambda b, h, blk, kind: oracle.bf16_bits_to_f64(
         np.stack(hist[kind][b][ns + blk * 128:ns + (blk + 1) * 128])[:, h])
     check_end_to_end(out.cpu().numpy(), hc, gc, raw, q_to_host(q), False, SCALE)
+
+
+step_cases = st.fixed_dictionaries(dict(
+    bits=st.sampled_from([2, 4]), aux=st.sampled_from([0, 1]), n_sink=st.sampled_from([0, 3, 128]),
+    n_kv=st.sampled_from([1, 2, 8]), g=st.sampled_from([1, 4, 5, 8, 12, 16]), batch=st.integers(1, 48),
+    length=st.integers(0, 5 * 128 + 40), steps=st.integers(1, 6), paged=st.booleans(),
+    kv_f32=st.sampled_from([False, False, False, True]), seed=st.integers(0, 2 ** 31 - 1)))
+
+
+@settings(max_examples=20 * SCALE_EXAMPLES, **SETTINGS)
+@given(case=step_cases)
+def test_gpu_append_decode_property(K, case):
+    """Lock-step steps of kvarn_append_decode from a prefilled cache of random shape against
+    kvarn_append_token + kvarn_decode_attention on a copy: bit-equal outputs and cache buffers
+    after every step (sink steps, flushes and fp32 tokens take the two kernels inside the call,
+    the other steps the fused launch); the last step's output against the oracle's decode of the
+    resulting cache."""
+    _announce(case)
+    c = case
+    B, nkv, g, ns, L0 = c["batch"], c["n_kv"], c["g"], c["n_sink"], c["length"]
+    n_q = g * nkv
+    MB = max(1, (L0 + c["steps"] - ns) // 128 + 1)
+    gen = torch.Generator(device="cuda").manual_seed(c["seed"])
+    sc = torch.exp(torch.randn((1, nkv, 128), generator=gen, device="cuda"))
+    k = (torch.randn((max(B * L0, 1), nkv, 128), generator=gen, device="cuda") * sc).to(torch.bfloat16)
+    v = torch.randn((max(B * L0, 1), nkv, 128), generator=gen, device="cuda").to(torch.bfloat16)
+    cu = torch.tensor([b * L0 for b in range(B + 1)], dtype=torch.int32, device="cuda")
+    p = K.kvarn_params_init(c["bits"], aux_format=c["aux"], n_sink=ns)
+    n_phys = B * MB + 2 if c["paged"] else 0
+    caches = [K.Cache(p, B, nkv, MB, n_phys=n_phys) for _ in range(2)]
+    if c["paged"]:
+        perm = torch.randperm(n_phys, generator=torch.Generator().manual_seed(c["seed"]))[:B * MB]
+        for cache in caches:
+            cache.block_table.copy_(perm.view(B, MB).to(torch.int32))
+    for cache in caches:
+        K.kvarn_prefill(p, cache, k, v, K.KVARN_BF16, cu, L0)
+    fused, ref_cache = caches
+    dt, kvdt = (torch.float32, K.KVARN_F32) if c["kv_f32"] else (torch.bfloat16, K.KVARN_BF16)
+    ws_bytes = max(K.kvarn_decode_workspace_bytes(p, fused, n_q, L0 + s + 1) for s in range(c["steps"]))
+    ws = torch.empty(max(ws_bytes, 16), dtype=torch.uint8, device="cuda")
+    for s in range(c["steps"]):
+        kt = (torch.randn((B, nkv, 128), generator=gen, device="cuda") * sc).to(dt)
+        vt = torch.randn((B, nkv, 128), generator=gen, device="cuda").to(dt)
+        q = (torch.randn((B, n_q, 128), generator=gen, device="cuda") * 2.0).to(torch.bfloat16)
+        got = torch.full(q.shape, float("nan"), dtype=torch.float32, device="cuda")
+        ref = torch.full(q.shape, float("nan"), dtype=torch.float32, device="cuda")
+        K.kvarn_append_decode(p, fused, kt, vt, kvdt, L0 + s, n_q, q, K.KVARN_BF16, got, K.KVARN_F32, SCALE, ws,
+                              ws_bytes)
+        K.kvarn_append_token(p, ref_cache, kt, vt, kvdt, L0 + s)
+        K.kvarn_decode_attention(p, ref_cache, n_q, q, K.KVARN_BF16, ref, K.KVARN_F32, SCALE, L0 + s + 1, ws,
+                                 ws_bytes)
+        torch.cuda.synchronize()
+        assert torch.equal(got, ref), f"step {s}"
+        for f in ("k_body", "v_body", "k_resid", "v_resid", "k_sink", "v_sink", "seq_len", "err_word"):
+            if getattr(fused, f) is not None:
+                assert torch.equal(getattr(fused, f), getattr(ref_cache, f)), (s, f)
+    assert int(fused.err_word[0]) == 0
+    np.testing.assert_array_equal(fused.seq_len.cpu().numpy(), [L0 + c["steps"]] * B)
+    dense = fused
+    if c["paged"]:  # the oracle reads a dense body: gather the pool blocks through the table
+        dense = K.Cache(p, B, nkv, MB)
+        for f in ("k_body", "v_body"):
+            getattr(dense, f).copy_(getattr(fused, f)[fused.block_table.long()].permute(0, 2, 1, 3))
+        for f in ("k_resid", "v_resid", "k_sink", "v_sink", "seq_len"):
+            if getattr(fused, f) is not None:
+                getattr(dense, f).copy_(getattr(fused, f))
+    check_output(got.cpu().numpy(), oracle.decode(host_cache(dense), q_to_host(q), SCALE), bf16_out=False)
