@@ -82,7 +82,7 @@ extern "C" {
 typedef enum {
     KVARN_OK = 0,
     KVARN_EINVAL = -1,       /* null pointer, bad size, stride or dtype                      */
-    KVARN_EUNSUPPORTED = -2, /* valid request this build does not implement (e.g. bits=3)    */
+    KVARN_EUNSUPPORTED = -2, /* valid request the library does not implement (e.g. bits=3)  */
     KVARN_ECAPACITY = -3,    /* the cache has no room for the requested tokens              */
     KVARN_EHIP = -4,         /* a HIP launch or query failed                                */
     KVARN_EWORKSPACE = -5    /* workspace missing or smaller than kvarn_decode_workspace_bytes */

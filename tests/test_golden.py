@@ -38,7 +38,7 @@ def test_paper_bits_accounting():
 
 @pytest.mark.parametrize("bits,expect", [(2, 2.75), (4, 4.75)])
 def test_library_format_accounting(bits, expect):
-    """This build's tile stores three fp32 vectors of 128 per 128 x 128 tile (a, b per group,
+    """The library's tile stores three fp32 vectors of 128 per 128 x 128 tile (a, b per group,
     s2 per other-axis index), i.e. three fp32 values per group of 128 elements."""
     c = _constants()
     g = int(c["group"])
