@@ -598,7 +598,10 @@ void k_decode4(DecodeArgs a) {
         const int perm4 = (4 * G + h) * 4;
 
         // One tile: consume cur, prefetch tile id_next into nxt.
-        auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next) {
+        // zoff is 0; the odd last tile passes it through an empty asm statement, so that its LDS
+        // offsets are formed after the loop rather than held in registers across it (which spilled
+        // them in the largest variant)
+        auto step = [&](TileRegs& cur, TileRegs& nxt, int id_next, int zoff) {
             wave_sync();  // the previous tile is done with sm.aux / sm.qp / sm.hv
             // aux rows a_K, b_K, s2_K (keys: per channel), a_V, b_V, s2_V (values: per token)
             stage_half_aux<CMP>(sm.aux, 0, cur.ak, l);
@@ -706,7 +709,8 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
                 for (int kap = 0; kap < 2; ++kap) {
                     // X1: rows 3, 7, 11 (slot 3 of heads 0-2) take the extra head's digits 0-2
-                    const uint4 u = X1 && j == 3 && h < 3 ? sm.qp4[X1 ? h : 0][kap][G] : sm.qp[hg][j][kap][qslot(j, G, h)];
+                    const int jq = j + zoff;
+                    const uint4 u = X1 && j == 3 && h < 3 ? sm.qp4[X1 ? h : 0][kap][G] : sm.qp[hg][jq][kap][qslot(jq, G, h)];
                     aq[hg][kap] = v4i{(int)u.x, (int)u.y, (int)u.z, (int)u.w};
                 }
                 fqs[hg] = sm.hv[4 * hg + G][1] * a.scale_log2;
@@ -827,11 +831,15 @@ void k_decode4(DecodeArgs a) {
         int id_n = block_id_t<PG>(a, b, min(blk0 + 1, blk1 - 1));
         for (; blk + 1 < blk1; blk += 2) {
             const int id_nn = block_id_t<PG>(a, b, min(blk + 2, blk1 - 1));
-            step(ra, rb, id_n);
+            step(ra, rb, id_n, 0);
             id_n = block_id_t<PG>(a, b, min(blk + 3, blk1 - 1));
-            step(rb, ra, id_nn);
+            step(rb, ra, id_nn, 0);
         }
-        if (blk < blk1) step(ra, rb, id_n);
+        if (blk < blk1) {
+            int z = 0;
+            asm volatile("" : "+v"(z));
+            step(ra, rb, id_n, z);
+        }
     }
 
     // ---- sink and residual (bf16, unrotated) -------------------------------------------------
