@@ -200,6 +200,28 @@ def test_decode_residual_placement(K, batch, n_sink, body, n_split):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
+@pytest.mark.parametrize("bits,n_q,body,n_split", [
+    (2, 16, 64, 68),   # 32 body splits + one split per sink / residual chunk (32 + 4)
+    (2, 16, 3, 1),     # one wave per stream walks all 36 chunks after its 3 tiles
+    (4, 40, 20, 46),   # 4 bits, group size 10 (two chunks of 5 heads: the extra-head kernel)
+])
+def test_decode_max_sink(K, bits, n_q, body, n_split):
+    """The largest sink the library takes (1024 bf16 tokens: 32 chunks per stream) with a
+    residual, ragged lengths down to sink-only and empty; the split count through the workspace
+    size."""
+    from paper_2606_03458_amd import workloads
+    ns = 1024
+    built, _ = workloads.build("llama", bits=bits, n_q=n_q, n_kv=4, batch=4, n_sink=ns, context=ns + body * 128 + 77)
+    L = built.length
+    lens = [L, ns + 5, ns - 1, 0]
+    built.cache.seq_len.copy_(torch.tensor(lens, dtype=torch.int32))
+    ws_bytes = K.kvarn_decode_workspace_bytes(built.params, built.cache, built.n_q, L + 1)
+    assert ws_bytes == (4 * n_q * n_split * 1040 if n_split > 1 else 0)
+    q = workloads.decode_queries(built, seed=12)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
 @pytest.mark.parametrize("bits,n_q,batch,aux,n_sink", [
     (2, 8, 768, 0, 0),     # group 4: 1536 streams, two splits each
     (4, 8, 512, 1, 128),   # group 4 at 4 bits, compact aux, a sink for the second split
