@@ -222,6 +222,20 @@ def test_decode_max_sink(K, bits, n_q, body, n_split):
     check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
 
 
+def test_decode_long_context(K):
+    """One sequence of 262,221 tokens (2048 body tiles per kv head, 8 kv heads): 342 body splits
+    of 6 tiles and 4 residual-chunk splits per stream, merged by four waves per query head over
+    346 partials."""
+    from paper_2606_03458_amd import workloads
+    built, _ = workloads.build("llama", batch=1, context=2048 * 128 + 77)
+    L = built.length
+    ws_bytes = K.kvarn_decode_workspace_bytes(built.params, built.cache, built.n_q, L + 1)
+    assert ws_bytes == 1 * 32 * 346 * 1040
+    q = workloads.decode_queries(built, seed=13)
+    out = _decode(K, built, q)
+    check_output(out.cpu().numpy(), _ref(built, q), bf16_out=False)
+
+
 @pytest.mark.parametrize("bits,n_q,batch,aux,n_sink", [
     (2, 8, 768, 0, 0),     # group 4: 1536 streams, two splits each
     (4, 8, 512, 1, 128),   # group 4 at 4 bits, compact aux, a sink for the second split
