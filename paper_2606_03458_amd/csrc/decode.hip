@@ -175,14 +175,18 @@ __device__ __forceinline__ uint2 load_stream2(const uint8_t* p) {
 }
 template <int CMP>
 __device__ __forceinline__ void load_half_aux(HalfAux<CMP>& r, const uint8_t* t, size_t cb, int l) {
+    // (lane offsets as unsigned 32-bit values: the loads then take the uniform tile address as
+    // their scalar base, with no 64-bit address arithmetic per lane)
+    const uint8_t* x = t + cb;
+    const uint32_t u = (uint32_t)l;
     if constexpr (CMP) {
-        r.b = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(t + cb + 4 * l));
-        r.a = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(t + cb + 256 + 2 * l));
-        r.s = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(t + cb + 384 + 2 * l));
+        r.b = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(x + 4u * u));
+        r.a = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(x + (256u + 2u * u)));
+        r.s = __builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(x + (384u + 2u * u)));
     } else {
-        r.a = load_stream2(t + cb + 8 * l);
-        r.b = load_stream2(t + cb + 512 + 8 * l);
-        r.s = load_stream2(t + cb + 1024 + 8 * l);
+        r.a = load_stream2(x + 8u * u);
+        r.b = load_stream2(x + (512u + 8u * u));
+        r.s = load_stream2(x + (1024u + 8u * u));
     }
 }
 // -> fp32 rows a, b, s2 (rows r0, r0 + 1, r0 + 2 of aux), entries 2l and 2l + 1; both compact
@@ -562,7 +566,7 @@ void k_decode4(DecodeArgs a) {
 #pragma unroll
             for (int s = 0; s < 2; ++s)
 #pragma unroll
-                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16 * (s * 128 * WPU + 64 * k + l));
+                for (int k = 0; k < 2 * WPU; ++k) c[s][k] = load_stream(t + 16u * (unsigned)(s * 128 * WPU + 64 * k + l));
         };
         const int id0 = block_id_t<PG>(a, b, blk0);
         load_codes(tile_k(id0), ra.k);
