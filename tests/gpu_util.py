@@ -62,7 +62,12 @@ def _tile_mismatch(codes, a, b, s2, r, qmax):
     # products along both axes are independent of how a scale is split between the axes
     Pa, Pb, Ra, Rb = np.outer(a64, s264), np.outer(b64, s264), np.outer(ra, rs2), np.outer(rb, rs2)
     ea = np.abs(Pa - Ra) / np.abs(Ra)
-    eb = np.abs(Pb - Rb) / np.maximum(np.abs(Rb), qmax * np.abs(Ra))
+    # an offset is a group minimum out of the rotation, a sum of 128 terms: in fp32 its absolute
+    # error scales with the tile's magnitude, not with the (possibly cancelled) value itself, so
+    # the part of the difference within 2^-20 of the tile's largest rotated value is not counted
+    # (as for the compact format's binary16 offsets)
+    slack = 2.0 ** -20 * float(np.abs(r.T).max())
+    eb = np.maximum(np.abs(Pb - Rb) - slack, 0.0) / np.maximum(np.abs(Rb), qmax * np.abs(Ra))
     return hard, excused, float(max(ea.max(), eb.max()))
 
 
