@@ -200,7 +200,10 @@ def resolve_ties(hc, gc, raw_tile, params=None) -> dict:
             for blk in range(_body_tiles(hc, b)):
                 for kind, ob, gb in ((0, hc.k_body, gc.k_body), (1, hc.v_body, gc.v_body)):
                     st["tiles"] += 1
-                    if np.array_equal(ob[b, kh, blk, :cb], gb[b, kh, blk, :cb]):
+                    # compact aux values are exact on both sides except at rounding ties, so a
+                    # compact tile is compared whole: an s2 tie can leave every code unchanged
+                    n_cmp = cb if aux == 0 else ob.shape[-1]
+                    if np.array_equal(ob[b, kh, blk, :n_cmp], gb[b, kh, blk, :n_cmp]):
                         st["codes"] += 128 * 128
                         continue
                     X = raw_tile(b, kh, blk, kind)[None]
@@ -340,8 +343,11 @@ def _compact_tile_status(codes, a, b, s2, r, kind):
     s2_bad, a_bad = np.flatnonzero(s2 != r.s2), np.flatnonzero(a != r.a)
     if s2_bad.size or a_bad.size:
         pre_s2 = np.clip(r.pre[2], 2.0 ** -6, 448.0)
+        # the tile is quantized against the stored s2 (absorb, then round), so a rounding tie of
+        # an s2 entry moves the steps, offsets and codes of every group it enters: with s2 ties
+        # only, the group steps need no tie of their own
         tie = all(_near_e4m3_boundary(pre_s2[k], False) for k in s2_bad) and \
-            all(_near_e4m3_boundary(r.pre[0][k], True) for k in a_bad)
+            (s2_bad.size > 0 or all(_near_e4m3_boundary(r.pre[0][k], True) for k in a_bad))
         tie = tie or _near_shift_tie(r, kind)
         return ("tie" if tie else "mismatch"), 0, 0
     b_bad = np.flatnonzero(b != r.b)
