@@ -424,6 +424,10 @@ def compare_tiles_compact(gpu_tiles: np.ndarray, X: np.ndarray, kind: int, bits:
                     status, excused, b_steps = st
                     stats["forced"] += 1
                     break
+                if st[0] == "tie":
+                    # a tied iteration whose outcome differs only by a format tie: both ties are
+                    # allowed, so it is a tie tile (dequantization bound, counted)
+                    status = "tie"
         if status == "match":
             stats["codes"] += codes.size
             stats["excused"] += excused
